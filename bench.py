@@ -1,0 +1,273 @@
+#!/usr/bin/env python3
+"""Throughput of the quantized-convolution hot path on one MI355X.
+
+Default workload: the 1-bit-weight / 2-bit-activation 3x3 convolution over a
+batch of 256 x 128 x 32 x 32 fp32 activations with 128 output channels and a
+fused fp32 batch-norm epilogue.  One step = quantize + pack the fp32 input
+(qconv_pack_act) + the bitplane convolution with its epilogue
+(qconv_forward); weights are packed once beforehand, as at inference.
+
+Prints ONE JSON line: GOPS = 2 * MACs (all taps, padding included) / step
+time, plus the roofline of the dominant kernel (measured with HIP events on
+the launch stream) and the CPU oracle timed on a bounded sample.
+
+Other workloads: --workload 1w1a | 1w2a (default) | 3w3a-L{0..3} |
+convnet | resnet18 (the last two report images/s).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import paper_2003_04296_amd as q  # noqa: E402
+from paper_2003_04296_amd import synth  # noqa: E402
+
+METRIC = "quantized-conv GOPS (1W1A, 2W2A, 3W3A) + images/sec fwd; % of roofline"
+
+# MI355X figures: 256 CUs x 64 lanes x 2.4 GHz of 32-bit VALU issue.
+VALU_LANE_OPS = 256 * 64 * 2.4e9
+HBM_PEAK_GBS = 8000.0
+MFMA_I8_PEAK_TOPS = 5000.0
+# Minimal VALU recipe (lane-ops per 32-channel word pair) of the bitplane
+# product on gfx950, where v_bitop3_b32 fuses any 3-input bit function:
+#   1W1A: xor, bcnt                         -> 2
+#   1W2A / 2W1A: bitop3(xor & mask), bcnt   -> 2  (activation-only popcount amortised)
+#   2W2A: bitop3, and, and, 2 bcnt          -> 5
+#   3W3A: 9 and/and_or (shift classes), 5 x (bitop3 + 2 bcnt) -> 24
+LANE_OPS_PER_WORD = {(1, 1): 2, (2, 1): 2, (1, 2): 2, (2, 2): 5, (3, 3): 24}
+
+
+def valu_peak_gops(a_bits, w_bits):
+    ops = LANE_OPS_PER_WORD.get((a_bits, w_bits))
+    if ops is None:
+        return None
+    return VALU_LANE_OPS * 32.0 / ops * 2.0 / 1e9  # conv-ops (2 per MAC) per second, in G
+
+
+def _fold(bn, dev):
+    k, b = q.fold_bn(bn["gamma"].numpy(), bn["beta"].numpy(), bn["mean"].numpy(), bn["var"].numpy(), bn["eps"])
+    return torch.from_numpy(k).to(dev), torch.from_numpy(b).to(dev)
+
+
+class ConvWorkload:
+    """pack_act + qconv_forward on one synthetic layer."""
+
+    def __init__(self, case, dev, mode, algo):
+        self.case = case
+        self.dev = dev
+        self.mode = mode
+        self.algo = algo
+        n, c, h, w = case.x.shape
+        self.shape = (n, c, h, w)
+        self.cout = case.w.shape[0]
+        self.k = case.w.shape[2]
+        self.x = case.x.to(dev)
+        self.wq, self.scale = q.pack_weight(case.w.to(dev), case.w_bits)
+        if case.bn is not None:
+            self.bn_k, self.bn_b = _fold(case.bn, dev)
+        else:
+            self.bn_k = self.bn_b = None
+        self.act = torch.empty(q.packed_act_words(n, c, h, w, case.a_bits), dtype=torch.int32, device=dev)
+        ho = q.out_size(h, self.k, case.stride, case.pad)
+        wo = q.out_size(w, self.k, case.stride, case.pad)
+        self.out_shape = (n, self.cout, ho, wo)
+        dt = torch.int32 if mode == q.EPI_INT32 else torch.float32
+        self.out = torch.empty(self.out_shape, dtype=dt, device=dev)
+        self.macs = n * self.cout * ho * wo * c * self.k * self.k
+
+    def pack(self):
+        q.pack_act(self.x, self.case.a_bits, out=self.act)
+
+    def conv(self):
+        n, c, h, w = self.shape
+        q.conv(self.act, self.wq, n, c, h, w, self.cout, self.k, self.case.stride, self.case.pad,
+               self.case.a_bits, self.case.w_bits, mode=self.mode, scale=self.scale, bn_k=self.bn_k,
+               bn_b=self.bn_b, out=self.out, algo=self.algo)
+
+    def step(self):
+        self.pack()
+        self.conv()
+
+    def conv_bytes(self):
+        """Algorithmic HBM bytes of one conv launch: packed input + packed weights + output."""
+        n, c, h, w = self.shape
+        a = q.packed_act_words(n, c, h, w, self.case.a_bits) * 4
+        wb = q.packed_weight_words(self.cout, c, self.k, self.k, self.case.w_bits) * 4
+        return a + wb + int(np.prod(self.out_shape)) * 4
+
+    def pack_bytes(self):
+        n, c, h, w = self.shape
+        return n * c * h * w * 4 + q.packed_act_words(n, c, h, w, self.case.a_bits) * 4
+
+
+def time_kernel(fn, reps, stream):
+    """Average duration of fn's launches with HIP events on the launch stream."""
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(reps):
+        fn()
+    end.record(stream)
+    end.synchronize()
+    return start.elapsed_time(end) / 1e3 / reps
+
+
+def cpu_baseline_conv(case, mode, budget_s=12.0):
+    """The oracle (untuned) on a bounded sample of the same layer: quantize the
+    sampled images + weights, direct conv, epilogue; GOPS over that sample."""
+    import oracle
+
+    n, c, h, w = case.x.shape
+    cout, _, k, _ = case.w.shape
+    ho = q.out_size(h, k, case.stride, case.pad)
+    wo = q.out_size(w, k, case.stride, case.pad)
+    macs_per_img = cout * ho * wo * c * k * k
+
+    def run(m):
+        t0 = time.perf_counter()
+        la = oracle.quantize(case.x[:m].numpy(), case.a_bits)
+        lw, s = oracle.quantize_weights(case.w.numpy(), case.w_bits)
+        acc = oracle.qconv_acc(la, lw, case.a_bits, case.stride, case.pad)
+        if mode == q.EPI_BN_F32:
+            kk, bb = oracle.bn_fold({key: (v.numpy() if hasattr(v, "numpy") else v) for key, v in case.bn.items()})
+            oracle.epi_bn(acc, kk, bb, oracle.level_shift(case.a_bits) + oracle.level_shift(case.w_bits))
+        elif mode == q.EPI_SCALE_F32:
+            oracle.epi_scale(acc, s)
+        return time.perf_counter() - t0
+
+    t1 = run(1)
+    m = int(max(1, min(n, budget_s / max(t1, 1e-6))))
+    tm = run(m) if m > 1 else t1
+    return {"value": round(2.0 * macs_per_img * m / tm / 1e9, 3), "unit": "GOPS", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"{m} of {n} images of the same layer (quantize + direct conv + epilogue), {tm:.1f} s"}
+
+
+def cpu_baseline_net(params, forward, budget_s=12.0):
+    import oracle
+
+    n = params["x"].shape[0]
+
+    def run(m):
+        sub = dict(params)
+        sub["x"] = params["x"][:m]
+        t0 = time.perf_counter()
+        forward(sub)
+        return time.perf_counter() - t0
+
+    t1 = run(1)
+    m = int(max(1, min(n, budget_s / max(t1, 1e-6))))
+    tm = run(m) if m > 1 else t1
+    return {"value": round(m / tm, 3), "unit": "images/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"{m} of {n} images through the whole network, {tm:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="1w2a")
+    ap.add_argument("--algo", default="auto", choices=["auto", "bitplane", "mfma"])
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(images are independent, so the batch would shard across GPUs without communication)",
+              file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    algo = {"auto": q.ALGO_AUTO, "bitplane": q.ALGO_BITPLANE, "mfma": q.ALGO_MFMA_I8}[args.algo]
+    wl = args.workload
+    out = {"metric": METRIC, "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "data": "synthetic"}
+
+    if wl in ("1w1a", "1w2a") or wl.startswith("3w3a"):
+        if wl == "1w1a":
+            case, mode = synth.workload1(), q.EPI_SCALE_F32
+        elif wl == "1w2a":
+            case, mode = synth.workload2(), q.EPI_BN_F32
+        else:
+            case, mode = synth.workload5(int(wl.split("L")[1])), q.EPI_INT32
+        W = ConvWorkload(case, dev, mode, algo)
+        for _ in range(args.warmup):
+            W.step()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            W.step()
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / args.steps
+        t_conv = time_kernel(W.conv, args.steps, stream)
+        t_pack = time_kernel(W.pack, args.steps, stream)
+        gops_step = 2.0 * W.macs / dt / 1e9
+        gops_conv = 2.0 * W.macs / t_conv / 1e9
+        peak = valu_peak_gops(case.a_bits, case.w_bits)
+        n, c, h, w = W.shape
+        out.update({
+            "value": round(gops_step, 1), "unit": "GOPS", "ms_per_step": round(dt * 1e3, 4),
+            "dtype": "int32",
+            "config": {"workload": case.name, "batch": n, "cin": c, "hw": h, "cout": W.cout, "k": W.k,
+                       "a_bits": case.a_bits, "w_bits": case.w_bits,
+                       "epilogue": {q.EPI_INT32: "int32", q.EPI_SCALE_F32: "scale_f32",
+                                    q.EPI_BN_F32: "bn_f32"}[mode],
+                       "algo": args.algo, "weights": "packed once before timing"},
+            "roofline": {"bound": "alu", "kernel": "qconv_forward (bitplane)", "achieved": round(gops_conv, 1),
+                         "peak": round(peak, 1) if peak else None, "unit": "GOPS",
+                         "frac": round(gops_conv / peak, 4) if peak else None, "traffic": None,
+                         "avg_us": round(t_conv * 1e6, 2),
+                         "hbm_gbs_algorithmic": round(W.conv_bytes() / t_conv / 1e9, 1)},
+            "pack_act": {"avg_us": round(t_pack * 1e6, 2), "achieved_gbs": round(W.pack_bytes() / t_pack / 1e9, 1),
+                         "peak_gbs": HBM_PEAK_GBS},
+        })
+        if not args.no_cpu:
+            out["cpu_baseline"] = cpu_baseline_conv(case, mode)
+    elif wl in ("convnet", "resnet18"):
+        from paper_2003_04296_amd.nets import build_convnet, build_resnet18
+        import oracle
+
+        if wl == "convnet":
+            params = synth.convnet_params(seed=1003, batch=256)
+            net = build_convnet(params, dev)
+            fwd = oracle.convnet_forward
+        else:
+            params = synth.resnet18_params(seed=1004, batch=64)
+            net = build_resnet18(params, dev)
+            fwd = lambda p: oracle.resnet18_forward(p, 2, 2)  # noqa: E731
+        x = params["x"].to(dev)
+        logits = torch.empty((x.shape[0], net.out_features), dtype=torch.float32, device=dev)
+        for _ in range(args.warmup):
+            net.forward(x, logits)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            net.forward(x, logits)
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / args.steps
+        out.update({"value": round(x.shape[0] / dt, 1), "unit": "images/s", "ms_per_step": round(dt * 1e3, 4),
+                    "dtype": "int32", "roofline": None,
+                    "config": {"workload": wl + ("_1w1a_batch256_32x32" if wl == "convnet" else "_2w2a_batch64_224x224"),
+                               "batch": int(x.shape[0])}})
+        if not args.no_cpu:
+            out["cpu_baseline"] = cpu_baseline_net(params, fwd)
+    else:
+        print(f"unknown workload {wl}", file=sys.stderr)
+        sys.exit(2)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

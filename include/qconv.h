@@ -1,0 +1,242 @@
+/*
+ * qconv.h -- C ABI of the MI355X (gfx950) quantized-convolution library.
+ *
+ * The library computes the inference forward pass of MINW-Net ("M-bit
+ * Inputs and N-bit Weights Network"; Chen et al., "Propagating
+ * Asymptotic-Estimated Gradients for Low Bitwidth Quantized Neural
+ * Networks"): weights and activations quantized by the inference quantizers
+ * of Sec. III-C (Eq. 20 applying Eq. 4 sign, Eq. 21 ternary, Eq. 22
+ * power-of-two), the layer product of Algorithm 1's inference branch
+ * evaluated as XNOR/AND-popcount over channel-packed bitplanes with a
+ * shift-weighted sum over plane pairs (Sec. III-C: bitwise and shift
+ * operations replace multiplies), and the layer constructs of Sec. III-E
+ * ({QConv-pooling-BN-HardTanh}, {QConv-BN-HardTanh}) fused into the
+ * convolution's epilogue.
+ *
+ * Conventions shared by every entry point:
+ *  - Pointers named x, w, act, out, scale, bn_*, residual, logits, workspace
+ *    are DEVICE pointers owned by the caller; "host" marks host pointers.
+ *    The library never allocates device memory, never synchronises, keeps no
+ *    mutable global state, and enqueues all work on `stream` (a hipStream_t
+ *    passed as void*; NULL = the null stream).
+ *  - Every call validates its arguments synchronously and returns a negative
+ *    qconv_status WITHOUT launching anything when they are invalid.  A launch
+ *    failure returns QCONV_EHIP.  Faults inside kernels surface at the
+ *    caller's next synchronisation.
+ *  - Overlapping input and output buffers are not supported.
+ *
+ * Integer level codes (what a packed value means):
+ *   1 bit : {-1, +1}                         (Eq. 4)
+ *   2 bits: {-1, 0, +1}                      (Eq. 21)
+ *   3 bits: {0, +-1, +-2, +-4} = 4 x {0, +-1/4, +-1/2, +-1}   (Eq. 22)
+ *   Integer accumulators are in code units: the real product is
+ *   acc * 2^-(2[a_bits==3] + 2[w_bits==3]).
+ *
+ * Quantizer thresholds (the paper leaves them open; these are the defaults):
+ *   activations: 2 bits |x| <= 0.5 -> 0;  3 bits |x| <= 1/8 -> 0,
+ *                <= 3/8 -> 1/4, <= 3/4 -> 1/2, else 1 (nearest level);
+ *   weights:     the same rules with thresholds multiplied by s_c = mean|W_c|
+ *                (2 bits: 0.7 s_c; 3 bits: {1/8, 3/8, 3/4} s_c), each
+ *                threshold computed in double and rounded once to float.
+ *   sign(x) = +1 only for x > 0 (0, -0 and NaN give -1; Sec. II-A).
+ *
+ * Packed bitplane layouts (uint32 words, bit (c % 32) of word (c / 32) holds
+ * channel c; bits past the last channel are 0 in every plane):
+ *   planes P = 1 / 2 / 4 for 1 / 2 / 3 bits;
+ *   plane 0: sign, 1 <=> level > 0;
+ *   2 bits : plane 1 = level != 0;
+ *   3 bits : plane 1 = |level| == 1, plane 2 = |level| == 1/2,
+ *            plane 3 = |level| == 1/4.
+ *   activations: [n][h][w][cw][P],              cw = ceil(c / 32)
+ *   weights    : [kh][kw][cw][cout_pad][P],     cout_pad = ceil(cout / 64) * 64
+ *                (rows of padding channels are 0).
+ *   An all-zero activation word reads as level -1 for 1 bit and 0 for 2/3
+ *   bits, i.e. Q(0): the value padding taps take in the product.
+ */
+#ifndef QCONV_H
+#define QCONV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  QCONV_OK = 0,
+  QCONV_EINVAL = -1,       /* null pointer, bad size, bad enum value          */
+  QCONV_EUNSUPPORTED = -2, /* valid but not implemented (shape, bits, algo)   */
+  QCONV_EWORKSPACE = -3,   /* workspace too small                             */
+  QCONV_EOVERFLOW = -4,    /* K * max|a| * max|w| >= 2^31 (int32 accumulator) */
+  QCONV_EHIP = -5          /* a HIP launch or runtime call failed             */
+} qconv_status;
+
+/* Human-readable text for a status code (never NULL). */
+const char* qconv_error_string(int status);
+
+/* Library ABI version (major * 100 + minor). */
+int qconv_version(void);
+
+/* ------------------------------------------------------------------------ */
+/* Inference-operation rule (Sec. IV-C; Tables I and II, columns 3-4)        */
+/* ------------------------------------------------------------------------ */
+typedef enum {
+  QCONV_OP_XNOR = 1,        /* min(M, N) <= 2                               */
+  QCONV_OP_SHIFT = 2,       /* min(M, N) == 3                               */
+  QCONV_OP_XNOR_ADDER = 3,  /* one side 16-bit float, other side <= 2 bits  */
+  QCONV_OP_SHIFT_ADDER = 4, /* one side 16-bit float, other side 3 bits     */
+  QCONV_OP_MAC = 5          /* both 32-bit float                            */
+} qconv_op;
+
+/* For M-bit inputs and N-bit weights (M, N in {1, 2, 3, 16, 32}) report the
+ * inference operation (by the smaller width) and the computational precision
+ * in bits (by the larger width: 1 -> "1-bit fixed", 2 -> "2-bit fixed",
+ * 16/32 -> floating).  *op and *precision_bits are host pointers. */
+int qconv_inference_op(int m_bits, int n_bits, int* op, int* precision_bits);
+
+/* ------------------------------------------------------------------------ */
+/* Quantize + pack (Sec. III-C, Eq. 20)                                      */
+/* ------------------------------------------------------------------------ */
+
+/* Bytes of the packed activation tensor [n][h][w][ceil(c/32)][P]. */
+size_t qconv_packed_act_bytes(int n, int c, int h, int w, int bits);
+
+/* Quantize fp32 NCHW activations x[n][c][h][w] with h(.) of `bits` and pack
+ * them into out_packed.  thresholds (host, may be NULL for the defaults):
+ * 2 bits {delta}; 3 bits {t1, t2, t3} increasing; ignored for 1 bit. */
+int qconv_pack_act(const float* x, int n, int c, int h, int w, int bits,
+                   const float* thresholds, uint32_t* out_packed, void* stream);
+
+/* Bytes of the packed weight tensor [kh][kw][ceil(cin/32)][cout_pad][P]. */
+size_t qconv_packed_weight_bytes(int cout, int cin, int kh, int kw, int bits);
+
+/* Quantize fp32 OIHW weights w[cout][cin][kh][kw] (Eq. 20) and pack them.
+ * out_scale[cout] (device) receives s_c = mean |W_c| (double sum over
+ * (cin, kh, kw) in storage order, rounded once to float).  base_thresholds
+ * (host, NULL = defaults) are multiplied by s_c per channel. */
+int qconv_pack_weight(const float* w, int cout, int cin, int kh, int kw, int bits,
+                      const float* base_thresholds, uint32_t* out_packed, float* out_scale,
+                      void* stream);
+
+/* Host helper: fold batch norm (all host arrays of length c) in double,
+ * k = gamma / sqrt(var + eps), b = beta - k * mean, each rounded once. */
+int qconv_fold_bn(const float* gamma, const float* beta, const float* mean, const float* var,
+                  double eps, int c, float* k_out, float* b_out);
+
+/* ------------------------------------------------------------------------ */
+/* Quantized convolution with fused epilogue (Algorithm 1 + Sec. III-E)      */
+/* ------------------------------------------------------------------------ */
+typedef enum {
+  QCONV_ALGO_AUTO = 0,     /* library choice                                  */
+  QCONV_ALGO_BITPLANE = 1, /* VALU XNOR/AND + popcount over bitplanes         */
+  QCONV_ALGO_MFMA_I8 = 2   /* int8 matrix cores on the unpacked level codes   */
+} qconv_algo;
+
+typedef struct {
+  int n, cin, h, w;     /* input activations (packed with a_bits)         */
+  int cout, kh, kw;     /* weights (packed with w_bits)                   */
+  int stride, pad;      /* same stride / padding on both axes             */
+  int a_bits, w_bits;   /* 1..3 each                                      */
+  int algo;             /* qconv_algo                                     */
+} qconv_desc;
+
+typedef enum {
+  QCONV_EPI_INT32 = 0,     /* out: int32 [n][cout][ho][wo] accumulators (code units)    */
+  QCONV_EPI_SCALE_F32 = 1, /* out: fp32 s_c * acc_real (one rounding)                   */
+  QCONV_EPI_BN_F32 = 2,    /* out: fp32 z = fmaf(k_c, acc_real, b_c) [+ residual]       */
+  QCONV_EPI_BN_PACK = 3    /* out_packed only: Q(HardTanh(z)) packed with out_bits     */
+} qconv_epi_mode;
+
+enum {
+  QCONV_EPI_POOL2 = 1,    /* 2x2/2 max pool of the accumulators before anything else  */
+  QCONV_EPI_RESIDUAL = 2  /* BN_F32: add residual[n][cout][ho][wo] after BN (fp32 add) */
+};
+
+typedef struct {
+  int mode;                   /* qconv_epi_mode                                       */
+  int flags;                  /* QCONV_EPI_POOL2 | QCONV_EPI_RESIDUAL                  */
+  const float* scale;         /* [cout] s_c                      (SCALE_F32)          */
+  const float* bn_k;          /* [cout] folded k_c               (BN_F32, BN_PACK)    */
+  const float* bn_b;          /* [cout] folded b_c                                    */
+  const float* residual;      /* fp32 NCHW, output shape          (RESIDUAL)          */
+  int out_bits;               /* bits of out_packed (BN_PACK; BN_F32 when out_packed)  */
+  const float* out_thresholds;/* host, NULL = default activation thresholds           */
+} qconv_epilogue;
+
+/* Output spatial size of the convolution (before pooling). */
+int qconv_out_size(int in, int k, int stride, int pad);
+
+/* One quantized layer: acc = (act * W) in code units over all taps (padding
+ * taps take Q(0)), then the epilogue.  out is int32 or fp32 NCHW (may be
+ * NULL in BN_PACK mode); out_packed ([n][ho'][wo'][ceil(cout/32)][P_out],
+ * ho'/wo' after pooling) is written in BN_PACK mode and, when non-NULL, in
+ * BN_F32 mode (quantizing the fp32 result).  Requires ceil(cout/32)*32
+ * channels of room in out_packed's last word, K = cin*kh*kw with
+ * K * max|a| * max|w| < 2^31. */
+int qconv_forward(const qconv_desc* d, const uint32_t* act_packed, const uint32_t* w_packed,
+                  const qconv_epilogue* epi, void* out, uint32_t* out_packed, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Whole networks (Algorithm 1, inference branch, layer by layer)            */
+/* ------------------------------------------------------------------------ */
+
+/* A network is a list of layers over numbered tensors.  Tensor 0 is the fp32
+ * NCHW network input [batch][in_c][in_h][in_w]; every qnet_add_* call
+ * appends one layer producing one new tensor and returns its id (> 0), or a
+ * negative qconv_status.  Device pointers handed to qnet_add_* (weights,
+ * folded BN parameters) must stay valid while the network is used. */
+typedef struct qnet qnet;
+
+qnet* qnet_create(int in_c, int in_h, int in_w);
+void qnet_destroy(qnet* net);
+
+/* fp32 conv (zero padding, each output one fmaf chain over (ci, kh, kw)),
+ * then z = fmaf(k, conv, b), then ReLU if relu != 0; out_bits == 0 keeps z as
+ * fp32 NCHW, out_bits 1..3 quantizes HardTanh(z) and packs it.
+ * w: fp32 [cout][cin][k][k]. */
+int qnet_add_conv_f32(qnet* net, int src, const float* w, int cout, int k, int stride, int pad,
+                      const float* bn_k, const float* bn_b, int relu, int out_bits);
+
+/* fp32 k x k / stride max pooling with padding (padding never wins). */
+int qnet_add_maxpool_f32(qnet* net, int src, int k, int stride, int pad);
+
+/* Quantize + pack an fp32 tensor with the default activation thresholds. */
+int qnet_add_quantize(qnet* net, int src, int bits);
+
+/* Quantized conv on a packed tensor with a BN epilogue:
+ * pool2 != 0 -> 2x2 max pool of the accumulators first;
+ * out_bits 1..3 -> packed Q(HardTanh(BN)) output; out_bits 0 -> fp32 BN
+ * output, plus the fp32 tensor residual_src when residual_src > 0. */
+int qnet_add_qconv(qnet* net, int src, const uint32_t* w_packed, int cout, int k, int stride,
+                   int pad, int w_bits, int pool2, const float* bn_k, const float* bn_b,
+                   int residual_src, int out_bits);
+
+/* Global average pooling of an fp32 tensor: sum over (h, w) from +0 in
+ * storage order, one division by h*w. */
+int qnet_add_avgpool(qnet* net, int src);
+
+/* fp32 fully connected layer over the flattened (c, h, w) source, which is
+ * fp32 or a 1-bit packed tensor read as +-1.0: each output one fmaf chain in
+ * input order from +0, then + bias.  w: fp32 [out][in]; bias may be NULL. */
+int qnet_add_fc_f32(qnet* net, int src, const float* w, const float* bias, int out_features);
+
+/* Bytes of workspace qnet_forward needs for `batch` images. */
+size_t qnet_workspace_bytes(const qnet* net, int batch);
+
+/* Run the layers in order on x (device fp32 [batch][in_c][in_h][in_w]) and
+ * write the last tensor (fp32 [batch][features]) to logits. */
+int qnet_forward(const qnet* net, const float* x, int batch, float* logits, void* workspace,
+                 size_t workspace_bytes, void* stream);
+
+/* Shape of tensor `id` for `batch` images (host out-params; bits 0 = fp32),
+ * and its byte offset inside the workspace after qnet_forward (the last
+ * tensor lives in logits, offset reported as (size_t)-1). */
+int qnet_tensor_info(const qnet* net, int id, int batch, int* c, int* h, int* w, int* bits,
+                     size_t* ws_offset);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QCONV_H */

@@ -1,0 +1,261 @@
+"""Python binding of libqconv.so (the C ABI in include/qconv.h).
+
+Argument marshalling only: every step of the quantized path runs in the HIP
+kernels of the shared library.  PyTorch supplies device memory and the
+current stream.  If the library is not built, every call raises -- there is
+no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libqconv.so")
+
+QCONV_OK, QCONV_EINVAL, QCONV_EUNSUPPORTED, QCONV_EWORKSPACE, QCONV_EOVERFLOW, QCONV_EHIP = 0, -1, -2, -3, -4, -5
+ALGO_AUTO, ALGO_BITPLANE, ALGO_MFMA_I8 = 0, 1, 2
+EPI_INT32, EPI_SCALE_F32, EPI_BN_F32, EPI_BN_PACK = 0, 1, 2, 3
+EPI_POOL2, EPI_RESIDUAL = 1, 2
+OP_NAMES = {1: "XNOR", 2: "SHIFT", 3: "XNOR-ADDER", 4: "SHIFT-ADDER", 5: "MAC"}
+
+EXPORTED = (
+    "qconv_error_string", "qconv_version", "qconv_inference_op", "qconv_packed_act_bytes",
+    "qconv_pack_act", "qconv_packed_weight_bytes", "qconv_pack_weight", "qconv_fold_bn",
+    "qconv_out_size", "qconv_forward", "qnet_create", "qnet_destroy", "qnet_add_conv_f32",
+    "qnet_add_maxpool_f32", "qnet_add_quantize", "qnet_add_qconv", "qnet_add_avgpool",
+    "qnet_add_fc_f32", "qnet_workspace_bytes", "qnet_forward", "qnet_tensor_info",
+)
+
+
+class QconvError(RuntimeError):
+    def __init__(self, status: int, what: str = ""):
+        self.status = status
+        msg = _lib_or_none().qconv_error_string(status).decode() if _lib_or_none() else str(status)
+        super().__init__(f"{what}: {msg} ({status})" if what else f"{msg} ({status})")
+
+
+class qconv_desc(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_int) for name in
+                ("n", "cin", "h", "w", "cout", "kh", "kw", "stride", "pad", "a_bits", "w_bits", "algo")]
+
+
+class qconv_epilogue(ctypes.Structure):
+    _fields_ = [("mode", ctypes.c_int), ("flags", ctypes.c_int), ("scale", ctypes.c_void_p),
+                ("bn_k", ctypes.c_void_p), ("bn_b", ctypes.c_void_p), ("residual", ctypes.c_void_p),
+                ("out_bits", ctypes.c_int), ("out_thresholds", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def _lib_or_none():
+    return _lib
+
+
+def lib() -> ctypes.CDLL:
+    """Load the HIP library; raise loudly if it was not built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -c 'import __graft_entry__ as g; g.build()'`"
+                           " (the quantized path has no CPU fallback)")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+    L.qconv_error_string.restype = ctypes.c_char_p
+    L.qconv_error_string.argtypes = [i32]
+    L.qconv_version.restype = i32
+    L.qconv_inference_op.argtypes = [i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
+    L.qconv_packed_act_bytes.restype = sz
+    L.qconv_packed_act_bytes.argtypes = [i32] * 5
+    L.qconv_pack_act.argtypes = [vp, i32, i32, i32, i32, i32, vp, vp, vp]
+    L.qconv_packed_weight_bytes.restype = sz
+    L.qconv_packed_weight_bytes.argtypes = [i32] * 5
+    L.qconv_pack_weight.argtypes = [vp, i32, i32, i32, i32, i32, vp, vp, vp, vp]
+    L.qconv_fold_bn.argtypes = [vp, vp, vp, vp, ctypes.c_double, i32, vp, vp]
+    L.qconv_out_size.argtypes = [i32] * 4
+    L.qconv_forward.argtypes = [ctypes.POINTER(qconv_desc), vp, vp, ctypes.POINTER(qconv_epilogue), vp, vp, vp]
+    L.qnet_create.restype = vp
+    L.qnet_create.argtypes = [i32, i32, i32]
+    L.qnet_destroy.argtypes = [vp]
+    L.qnet_add_conv_f32.argtypes = [vp, i32, vp, i32, i32, i32, i32, vp, vp, i32, i32]
+    L.qnet_add_maxpool_f32.argtypes = [vp, i32, i32, i32, i32]
+    L.qnet_add_quantize.argtypes = [vp, i32, i32]
+    L.qnet_add_qconv.argtypes = [vp, i32, vp, i32, i32, i32, i32, i32, i32, vp, vp, i32, i32]
+    L.qnet_add_avgpool.argtypes = [vp, i32]
+    L.qnet_add_fc_f32.argtypes = [vp, i32, vp, vp, i32]
+    L.qnet_workspace_bytes.restype = sz
+    L.qnet_workspace_bytes.argtypes = [vp, i32]
+    L.qnet_forward.argtypes = [vp, vp, i32, vp, vp, sz, vp]
+    L.qnet_tensor_info.argtypes = [vp, i32, i32] + [ctypes.POINTER(i32)] * 4 + [ctypes.POINTER(sz)]
+    _lib = L
+    return L
+
+
+def _check(rc: int, what: str) -> int:
+    if rc < 0:
+        raise QconvError(rc, what)
+    return rc
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    import torch
+
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _host_f32(vals):
+    if vals is None:
+        return None
+    arr = (ctypes.c_float * len(vals))(*[float(v) for v in vals])
+    return arr
+
+
+def planes(bits: int) -> int:
+    return {1: 1, 2: 2, 3: 4}[bits]
+
+
+def out_size(n: int, k: int, stride: int, pad: int) -> int:
+    return _check(lib().qconv_out_size(n, k, stride, pad), "qconv_out_size")
+
+
+def inference_op(m_bits: int, n_bits: int):
+    op, prec = ctypes.c_int(), ctypes.c_int()
+    _check(lib().qconv_inference_op(m_bits, n_bits, ctypes.byref(op), ctypes.byref(prec)), "qconv_inference_op")
+    return OP_NAMES[op.value], prec.value
+
+
+def packed_act_words(n, c, h, w, bits) -> int:
+    return lib().qconv_packed_act_bytes(n, c, h, w, bits) // 4
+
+
+def packed_weight_words(cout, cin, kh, kw, bits) -> int:
+    return lib().qconv_packed_weight_bytes(cout, cin, kh, kw, bits) // 4
+
+
+def pack_act(x, bits: int, thresholds=None, out=None, stream=None):
+    """fp32 NCHW device tensor -> packed bitplanes [n][h][w][cw][P] (int32 view)."""
+    import torch
+
+    n, c, h, w = x.shape
+    if out is None:
+        out = torch.empty(packed_act_words(n, c, h, w, bits), dtype=torch.int32, device=x.device)
+    t = _host_f32(thresholds)
+    _check(lib().qconv_pack_act(_ptr(x), n, c, h, w, bits, t, _ptr(out), _stream(stream)), "qconv_pack_act")
+    return out
+
+
+def pack_weight(w, bits: int, base_thresholds=None, stream=None):
+    """fp32 OIHW device tensor -> (packed weights, s_c)."""
+    import torch
+
+    cout, cin, kh, kw = w.shape
+    out = torch.empty(packed_weight_words(cout, cin, kh, kw, bits), dtype=torch.int32, device=w.device)
+    scale = torch.empty(cout, dtype=torch.float32, device=w.device)
+    t = _host_f32(base_thresholds)
+    _check(lib().qconv_pack_weight(_ptr(w), cout, cin, kh, kw, bits, t, _ptr(out), _ptr(scale), _stream(stream)),
+           "qconv_pack_weight")
+    return out, scale
+
+
+def fold_bn(gamma, beta, mean, var, eps):
+    """Host fold of BN parameters (numpy/CPU arrays) -> (k, b) float32 numpy."""
+    import numpy as np
+
+    g, b, m, v = (np.ascontiguousarray(np.asarray(a, dtype=np.float32)) for a in (gamma, beta, mean, var))
+    c = g.size
+    k = np.empty(c, np.float32)
+    bb = np.empty(c, np.float32)
+    P = lambda a: a.ctypes.data_as(ctypes.c_void_p)
+    _check(lib().qconv_fold_bn(P(g), P(b), P(m), P(v), ctypes.c_double(float(eps)), c, P(k), P(bb)), "qconv_fold_bn")
+    return k, bb
+
+
+def conv(act_packed, w_packed, n, cin, h, w, cout, k, stride, pad, a_bits, w_bits, mode=EPI_INT32,
+         flags=0, scale=None, bn_k=None, bn_b=None, residual=None, out_bits=0, out=None, out_packed=None,
+         algo=ALGO_AUTO, stream=None, out_thresholds=None):
+    """qconv_forward; allocates the outputs the epilogue needs when not given."""
+    import torch
+
+    ho, wo = out_size(h, k, stride, pad), out_size(w, k, stride, pad)
+    if flags & EPI_POOL2:
+        ho, wo = ho // 2, wo // 2
+    dev = act_packed.device
+    if out is None and mode != EPI_BN_PACK:
+        dt = torch.int32 if mode == EPI_INT32 else torch.float32
+        out = torch.empty((n, cout, ho, wo), dtype=dt, device=dev)
+    if out_packed is None and mode == EPI_BN_PACK:
+        out_packed = torch.empty(packed_act_words(n, cout, ho, wo, out_bits), dtype=torch.int32, device=dev)
+    d = qconv_desc(n, cin, h, w, cout, k, k, stride, pad, a_bits, w_bits, algo)
+    thr = _host_f32(out_thresholds) if out_thresholds else None  # kept alive across the call
+    e = qconv_epilogue(mode, flags, _ptr(scale), _ptr(bn_k), _ptr(bn_b), _ptr(residual), out_bits,
+                       ctypes.cast(thr, ctypes.c_void_p) if thr is not None else None)
+    _check(lib().qconv_forward(ctypes.byref(d), _ptr(act_packed), _ptr(w_packed), ctypes.byref(e), _ptr(out),
+                               _ptr(out_packed), _stream(stream)), "qconv_forward")
+    return out, out_packed
+
+
+class Net:
+    """A qnet layer list (tensor ids as in include/qconv.h)."""
+
+    def __init__(self, in_c: int, in_h: int, in_w: int):
+        self._h = lib().qnet_create(in_c, in_h, in_w)
+        if not self._h:
+            raise QconvError(QCONV_EINVAL, "qnet_create")
+        self._keep = []  # device tensors the layers point at
+
+    def __del__(self):
+        if getattr(self, "_h", None) and _lib is not None:
+            _lib.qnet_destroy(self._h)
+            self._h = None
+
+    def _add(self, rc, what, *keep):
+        self._keep.extend(k for k in keep if k is not None)
+        return _check(rc, what)
+
+    def conv_f32(self, src, w, bn_k, bn_b, stride=1, pad=0, relu=False, out_bits=0):
+        cout, _, k, _ = w.shape
+        return self._add(lib().qnet_add_conv_f32(self._h, src, _ptr(w), cout, k, stride, pad, _ptr(bn_k), _ptr(bn_b),
+                                                 int(relu), out_bits), "qnet_add_conv_f32", w, bn_k, bn_b)
+
+    def maxpool_f32(self, src, k, stride, pad):
+        return self._add(lib().qnet_add_maxpool_f32(self._h, src, k, stride, pad), "qnet_add_maxpool_f32")
+
+    def quantize(self, src, bits):
+        return self._add(lib().qnet_add_quantize(self._h, src, bits), "qnet_add_quantize")
+
+    def qconv(self, src, w_packed, cout, k, stride, pad, w_bits, bn_k, bn_b, pool2=False, residual_src=-1,
+              out_bits=0):
+        return self._add(lib().qnet_add_qconv(self._h, src, _ptr(w_packed), cout, k, stride, pad, w_bits, int(pool2),
+                                              _ptr(bn_k), _ptr(bn_b), residual_src, out_bits),
+                         "qnet_add_qconv", w_packed, bn_k, bn_b)
+
+    def avgpool(self, src):
+        return self._add(lib().qnet_add_avgpool(self._h, src), "qnet_add_avgpool")
+
+    def fc_f32(self, src, w, bias=None):
+        return self._add(lib().qnet_add_fc_f32(self._h, src, _ptr(w), _ptr(bias), w.shape[0]), "qnet_add_fc_f32",
+                         w, bias)
+
+    def workspace_bytes(self, batch):
+        return lib().qnet_workspace_bytes(self._h, batch)
+
+    def tensor_info(self, tid, batch):
+        c, h, w, b = (ctypes.c_int() for _ in range(4))
+        off = ctypes.c_size_t()
+        _check(lib().qnet_tensor_info(self._h, tid, batch, ctypes.byref(c), ctypes.byref(h), ctypes.byref(w),
+                                      ctypes.byref(b), ctypes.byref(off)), "qnet_tensor_info")
+        return c.value, h.value, w.value, b.value, off.value
+
+    def forward(self, x, logits, workspace, stream=None):
+        nbytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+        _check(lib().qnet_forward(self._h, _ptr(x), x.shape[0], _ptr(logits), _ptr(workspace), nbytes,
+                                  _stream(stream)), "qnet_forward")
+        return logits

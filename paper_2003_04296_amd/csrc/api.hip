@@ -1,0 +1,508 @@
+// api.hip -- the C ABI declared in include/qconv.h: argument validation,
+// kernel selection and the layer loop of whole networks.  Nothing here
+// allocates device memory or synchronises; every launch goes to the
+// caller's stream.
+#include <math.h>
+#include <string.h>
+
+#include <new>
+#include <vector>
+
+#include "qconv_internal.h"
+
+using namespace qc;
+
+namespace {
+
+constexpr float kActThr2[1] = {0.5f};
+constexpr float kActThr3[3] = {0.125f, 0.375f, 0.75f};
+constexpr float kWgtThr2[1] = {0.7f};
+constexpr float kWgtThr3[3] = {0.125f, 0.375f, 0.75f};
+
+bool bits_ok(int b) { return b >= 1 && b <= 3; }
+int max_code(int bits) { return bits == 3 ? 4 : 1; }
+int code_shift(int bits) { return bits == 3 ? 2 : 0; }
+
+// Threshold set for `bits`, from a host array (validated) or the defaults.
+int act_thresholds(int bits, const float* user, Thr* t) {
+  *t = {0.0f, 0.0f, 0.0f};
+  if (bits == 1) return QCONV_OK;
+  if (bits == 2) {
+    t->t0 = user ? user[0] : kActThr2[0];
+    if (!(t->t0 >= 0.0f)) return QCONV_EINVAL;
+    return QCONV_OK;
+  }
+  const float* s = user ? user : kActThr3;
+  t->t0 = s[0];
+  t->t1 = s[1];
+  t->t2 = s[2];
+  if (!(t->t0 >= 0.0f && t->t0 <= t->t1 && t->t1 <= t->t2)) return QCONV_EINVAL;
+  return QCONV_OK;
+}
+
+size_t packed_bytes(int64_t n, int c, int64_t h, int64_t w, int bits) {
+  return (size_t)(n * h * w * ceil_div(c, 32) * planes_of(bits)) * sizeof(uint32_t);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* qconv_error_string(int status) {
+  switch (status) {
+    case QCONV_OK: return "ok";
+    case QCONV_EINVAL: return "invalid argument";
+    case QCONV_EUNSUPPORTED: return "unsupported configuration";
+    case QCONV_EWORKSPACE: return "workspace too small";
+    case QCONV_EOVERFLOW: return "int32 accumulator could overflow (K * max|a| * max|w| >= 2^31)";
+    case QCONV_EHIP: return "HIP launch or runtime error";
+    default: return "unknown status";
+  }
+}
+
+int qconv_version(void) { return 100; }
+
+int qconv_inference_op(int m, int n, int* op, int* precision_bits) {
+  auto valid = [](int b) { return b == 1 || b == 2 || b == 3 || b == 16 || b == 32; };
+  if (!op || !precision_bits || !valid(m) || !valid(n)) return QCONV_EINVAL;
+  const int lo = m < n ? m : n, hi = m < n ? n : m;
+  if (lo == 32) {
+    *op = QCONV_OP_MAC;
+    *precision_bits = 32;
+  } else if (hi >= 16) {
+    if (hi == 32) return QCONV_EUNSUPPORTED;  // not a row of the tables
+    *op = (lo == 3) ? QCONV_OP_SHIFT_ADDER : QCONV_OP_XNOR_ADDER;
+    *precision_bits = 16;
+  } else {
+    *op = (lo == 3) ? QCONV_OP_SHIFT : QCONV_OP_XNOR;
+    *precision_bits = (hi <= 2) ? 1 : 2;
+  }
+  return QCONV_OK;
+}
+
+size_t qconv_packed_act_bytes(int n, int c, int h, int w, int bits) {
+  if (n < 0 || c < 1 || h < 1 || w < 1 || !bits_ok(bits)) return 0;
+  return packed_bytes(n, c, h, w, bits);
+}
+
+int qconv_pack_act(const float* x, int n, int c, int h, int w, int bits, const float* thresholds,
+                   uint32_t* out_packed, void* stream) {
+  if (n < 0 || c < 1 || h < 1 || w < 1 || !bits_ok(bits)) return QCONV_EINVAL;
+  if (n > 0 && (!x || !out_packed)) return QCONV_EINVAL;
+  Thr t;
+  const int rc = act_thresholds(bits, thresholds, &t);
+  if (rc) return rc;
+  return launch_pack_act(x, n, c, h, w, bits, t, out_packed, (hipStream_t)stream);
+}
+
+size_t qconv_packed_weight_bytes(int cout, int cin, int kh, int kw, int bits) {
+  if (cout < 1 || cin < 1 || kh < 1 || kw < 1 || !bits_ok(bits)) return 0;
+  return (size_t)kh * kw * ceil_div(cin, 32) * cout_pad(cout) * planes_of(bits) * sizeof(uint32_t);
+}
+
+int qconv_pack_weight(const float* w, int cout, int cin, int kh, int kw, int bits,
+                      const float* base_thresholds, uint32_t* out_packed, float* out_scale,
+                      void* stream) {
+  if (!w || !out_packed || !out_scale || cout < 1 || cin < 1 || kh < 1 || kw < 1 || !bits_ok(bits))
+    return QCONV_EINVAL;
+  float base[3] = {0.0f, 0.0f, 0.0f};
+  if (bits == 2) base[0] = base_thresholds ? base_thresholds[0] : kWgtThr2[0];
+  if (bits == 3)
+    for (int j = 0; j < 3; ++j) base[j] = base_thresholds ? base_thresholds[j] : kWgtThr3[j];
+  if (bits == 2 && !(base[0] >= 0.0f)) return QCONV_EINVAL;
+  if (bits == 3 && !(base[0] >= 0.0f && base[0] <= base[1] && base[1] <= base[2])) return QCONV_EINVAL;
+  return launch_pack_weight(w, cout, cin, kh, kw, bits, base, out_packed, out_scale,
+                            (hipStream_t)stream);
+}
+
+int qconv_fold_bn(const float* gamma, const float* beta, const float* mean, const float* var,
+                  double eps, int c, float* k_out, float* b_out) {
+  if (!gamma || !beta || !mean || !var || !k_out || !b_out || c < 1 || !(eps >= 0.0))
+    return QCONV_EINVAL;
+  for (int i = 0; i < c; ++i) {
+    const double kd = (double)gamma[i] / sqrt((double)var[i] + eps);
+    k_out[i] = (float)kd;
+    b_out[i] = (float)((double)beta[i] - kd * (double)mean[i]);
+  }
+  return QCONV_OK;
+}
+
+int qconv_out_size(int in, int k, int stride, int pad) {
+  if (in < 1 || k < 1 || stride < 1 || pad < 0) return QCONV_EINVAL;
+  const int o = (in + 2 * pad - k) / stride + 1;
+  return (in + 2 * pad - k) < 0 ? QCONV_EINVAL : o;
+}
+
+int qconv_forward(const qconv_desc* d, const uint32_t* act_packed, const uint32_t* w_packed,
+                  const qconv_epilogue* epi, void* out, uint32_t* out_packed, void* stream) {
+  if (!d || !epi) return QCONV_EINVAL;
+  if (d->n < 0 || d->cin < 1 || d->h < 1 || d->w < 1 || d->cout < 1 || d->kh < 1 || d->kw < 1 ||
+      d->stride < 1 || d->pad < 0 || !bits_ok(d->a_bits) || !bits_ok(d->w_bits))
+    return QCONV_EINVAL;
+  if (d->algo < QCONV_ALGO_AUTO || d->algo > QCONV_ALGO_MFMA_I8) return QCONV_EINVAL;
+  const int ho = qconv_out_size(d->h, d->kh, d->stride, d->pad);
+  const int wo = qconv_out_size(d->w, d->kw, d->stride, d->pad);
+  if (ho < 1 || wo < 1) return QCONV_EINVAL;
+  const int64_t K = (int64_t)d->cin * d->kh * d->kw;
+  if (K * max_code(d->a_bits) * max_code(d->w_bits) >= (int64_t)1 << 31) return QCONV_EOVERFLOW;
+  if (epi->mode < QCONV_EPI_INT32 || epi->mode > QCONV_EPI_BN_PACK) return QCONV_EINVAL;
+  if (epi->flags & ~(QCONV_EPI_POOL2 | QCONV_EPI_RESIDUAL)) return QCONV_EINVAL;
+  const bool pool = (epi->flags & QCONV_EPI_POOL2) != 0;
+  const bool resid = (epi->flags & QCONV_EPI_RESIDUAL) != 0;
+  if (pool && (ho < 2 || wo < 2)) return QCONV_EINVAL;
+  if (resid && (epi->mode != QCONV_EPI_BN_F32 || !epi->residual)) return QCONV_EINVAL;
+  if (epi->mode == QCONV_EPI_SCALE_F32 && !epi->scale) return QCONV_EINVAL;
+  if ((epi->mode == QCONV_EPI_BN_F32 || epi->mode == QCONV_EPI_BN_PACK) && (!epi->bn_k || !epi->bn_b))
+    return QCONV_EINVAL;
+  const bool pack = epi->mode == QCONV_EPI_BN_PACK || (epi->mode == QCONV_EPI_BN_F32 && out_packed);
+  if (epi->mode == QCONV_EPI_BN_PACK && !out_packed) return QCONV_EINVAL;
+  if (epi->mode != QCONV_EPI_BN_PACK && !out && d->n > 0) return QCONV_EINVAL;
+  if (pack && !bits_ok(epi->out_bits)) return QCONV_EINVAL;
+  if (d->n > 0 && (!act_packed || !w_packed)) return QCONV_EINVAL;
+
+  ConvArgs a;
+  memset(&a, 0, sizeof(a));
+  a.act = act_packed;
+  a.wt = w_packed;
+  a.n = d->n;
+  a.h = d->h;
+  a.w = d->w;
+  a.cw = ceil_div(d->cin, 32);
+  a.cout = d->cout;
+  a.cop = cout_pad(d->cout);
+  a.kh = d->kh;
+  a.kw = d->kw;
+  a.stride = d->stride;
+  a.pad = d->pad;
+  a.ho = ho;
+  a.wo = wo;
+  a.oh_out = pool ? ho / 2 : ho;
+  a.ow_out = pool ? wo / 2 : wo;
+  a.kreal = (int)K;
+  a.shift = code_shift(d->a_bits) + code_shift(d->w_bits);
+  a.a_bits = d->a_bits;
+  a.w_bits = d->w_bits;
+  a.mode = epi->mode;
+  a.pool = pool ? 1 : 0;
+  a.residual_on = resid ? 1 : 0;
+  a.scale = epi->scale;
+  a.bn_k = epi->bn_k;
+  a.bn_b = epi->bn_b;
+  a.residual = epi->residual;
+  a.out = out;
+  a.out_packed = pack ? out_packed : nullptr;
+  a.out_bits = pack ? epi->out_bits : 0;
+  a.out_cw = ceil_div(d->cout, 32);
+  if (pack) {
+    const int rc = act_thresholds(epi->out_bits, epi->out_thresholds, &a.othr);
+    if (rc) return rc;
+  }
+  if (d->n == 0) return QCONV_OK;
+  hipStream_t s = (hipStream_t)stream;
+  if (d->algo == QCONV_ALGO_MFMA_I8) {
+    if (!mfma_supports(a)) return QCONV_EUNSUPPORTED;
+    return launch_conv_mfma(a, s);
+  }
+  if (d->algo == QCONV_ALGO_AUTO && mfma_supports(a)) return launch_conv_mfma(a, s);
+  return launch_conv_bitplane(a, s);
+}
+
+// ---------------------------------------------------------------------------
+// Networks
+// ---------------------------------------------------------------------------
+
+}  // extern "C"
+
+namespace {
+
+enum LayerKind { L_CONV_F32, L_MAXPOOL_F32, L_QUANTIZE, L_QCONV, L_AVGPOOL, L_FC_F32 };
+
+struct QTensor {
+  int c, h, w, bits;  // bits 0 = fp32 NCHW, else packed bitplanes
+};
+
+struct QLayer {
+  int kind = 0, src = 0, src2 = -1;
+  const float* wf = nullptr;
+  const uint32_t* wq = nullptr;
+  const float* bn_k = nullptr;
+  const float* bn_b = nullptr;
+  const float* bias = nullptr;
+  int cout = 0, k = 0, stride = 1, pad = 0, w_bits = 0, pool2 = 0, relu = 0, out_bits = 0;
+};
+
+size_t tensor_bytes(const QTensor& t, int batch) {
+  if (t.bits == 0) return (size_t)batch * t.c * t.h * t.w * sizeof(float);
+  return packed_bytes(batch, t.c, t.h, t.w, t.bits);
+}
+
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+}  // namespace
+
+struct qnet {
+  std::vector<QTensor> t;
+  std::vector<QLayer> L;
+};
+
+namespace {
+
+// Workspace plan: every tensor except the input (0) and the last one gets
+// its own 256-byte aligned region, then one region per fp32 conv for its
+// re-laid-out weights.  Returns the total; offsets[id] = (size_t)-1 if none.
+size_t plan(const qnet* net, int batch, std::vector<size_t>* toff, std::vector<size_t>* woff) {
+  size_t off = 0;
+  const int last = (int)net->t.size() - 1;
+  if (toff) toff->assign(net->t.size(), (size_t)-1);
+  for (int id = 1; id < last; ++id) {
+    if (toff) (*toff)[id] = off;
+    off = align256(off + tensor_bytes(net->t[id], batch));
+  }
+  if (woff) woff->assign(net->L.size(), (size_t)-1);
+  for (size_t i = 0; i < net->L.size(); ++i) {
+    const QLayer& l = net->L[i];
+    if (l.kind != L_CONV_F32) continue;
+    if (woff) (*woff)[i] = off;
+    const int cin = net->t[l.src].c;
+    off = align256(off + (size_t)cin * l.k * l.k * ceil_div(l.cout, 32) * 32 * sizeof(float));
+  }
+  return off;
+}
+
+int add_tensor(qnet* net, QLayer l, QTensor out) {
+  if (out.c < 1 || out.h < 1 || out.w < 1) return QCONV_EINVAL;
+  net->L.push_back(l);
+  net->t.push_back(out);
+  return (int)net->t.size() - 1;
+}
+
+bool valid_src(const qnet* net, int id) { return net && id >= 0 && id < (int)net->t.size(); }
+
+}  // namespace
+
+extern "C" {
+
+qnet* qnet_create(int in_c, int in_h, int in_w) {
+  if (in_c < 1 || in_h < 1 || in_w < 1) return nullptr;
+  qnet* net = new (std::nothrow) qnet();
+  if (!net) return nullptr;
+  net->t.push_back({in_c, in_h, in_w, 0});
+  return net;
+}
+
+void qnet_destroy(qnet* net) { delete net; }
+
+int qnet_add_conv_f32(qnet* net, int src, const float* w, int cout, int k, int stride, int pad,
+                      const float* bn_k, const float* bn_b, int relu, int out_bits) {
+  if (!valid_src(net, src) || !w || !bn_k || !bn_b || cout < 1 || k < 1 || stride < 1 || pad < 0 ||
+      out_bits < 0 || out_bits > 3)
+    return QCONV_EINVAL;
+  const QTensor& s = net->t[src];
+  if (s.bits != 0) return QCONV_EINVAL;
+  QLayer l;
+  l.kind = L_CONV_F32;
+  l.src = src;
+  l.wf = w;
+  l.bn_k = bn_k;
+  l.bn_b = bn_b;
+  l.cout = cout;
+  l.k = k;
+  l.stride = stride;
+  l.pad = pad;
+  l.relu = relu ? 1 : 0;
+  l.out_bits = out_bits;
+  const int ho = qconv_out_size(s.h, k, stride, pad), wo = qconv_out_size(s.w, k, stride, pad);
+  if (ho < 1 || wo < 1) return QCONV_EINVAL;
+  return add_tensor(net, l, {cout, ho, wo, out_bits});
+}
+
+int qnet_add_maxpool_f32(qnet* net, int src, int k, int stride, int pad) {
+  if (!valid_src(net, src) || k < 1 || stride < 1 || pad < 0 || pad >= k) return QCONV_EINVAL;
+  const QTensor& s = net->t[src];
+  if (s.bits != 0) return QCONV_EINVAL;
+  QLayer l;
+  l.kind = L_MAXPOOL_F32;
+  l.src = src;
+  l.k = k;
+  l.stride = stride;
+  l.pad = pad;
+  const int ho = qconv_out_size(s.h, k, stride, pad), wo = qconv_out_size(s.w, k, stride, pad);
+  if (ho < 1 || wo < 1) return QCONV_EINVAL;
+  return add_tensor(net, l, {s.c, ho, wo, 0});
+}
+
+int qnet_add_quantize(qnet* net, int src, int bits) {
+  if (!valid_src(net, src) || !bits_ok(bits)) return QCONV_EINVAL;
+  const QTensor s = net->t[src];
+  if (s.bits != 0) return QCONV_EINVAL;
+  QLayer l;
+  l.kind = L_QUANTIZE;
+  l.src = src;
+  l.out_bits = bits;
+  return add_tensor(net, l, {s.c, s.h, s.w, bits});
+}
+
+int qnet_add_qconv(qnet* net, int src, const uint32_t* w_packed, int cout, int k, int stride,
+                   int pad, int w_bits, int pool2, const float* bn_k, const float* bn_b,
+                   int residual_src, int out_bits) {
+  if (!valid_src(net, src) || !w_packed || !bn_k || !bn_b || cout < 1 || k < 1 || stride < 1 ||
+      pad < 0 || !bits_ok(w_bits) || out_bits < 0 || out_bits > 3)
+    return QCONV_EINVAL;
+  const QTensor s = net->t[src];
+  if (s.bits == 0) return QCONV_EINVAL;
+  int ho = qconv_out_size(s.h, k, stride, pad), wo = qconv_out_size(s.w, k, stride, pad);
+  if (ho < 1 || wo < 1) return QCONV_EINVAL;
+  if (pool2) {
+    if (ho < 2 || wo < 2) return QCONV_EINVAL;
+    ho /= 2;
+    wo /= 2;
+  }
+  if ((int64_t)s.c * k * k * max_code(s.bits) * max_code(w_bits) >= (int64_t)1 << 31)
+    return QCONV_EOVERFLOW;
+  if (residual_src > 0) {
+    if (!valid_src(net, residual_src) || out_bits != 0) return QCONV_EINVAL;
+    const QTensor& r = net->t[residual_src];
+    if (r.bits != 0 || r.c != cout || r.h != ho || r.w != wo) return QCONV_EINVAL;
+  }
+  QLayer l;
+  l.kind = L_QCONV;
+  l.src = src;
+  l.src2 = residual_src > 0 ? residual_src : -1;
+  l.wq = w_packed;
+  l.bn_k = bn_k;
+  l.bn_b = bn_b;
+  l.cout = cout;
+  l.k = k;
+  l.stride = stride;
+  l.pad = pad;
+  l.w_bits = w_bits;
+  l.pool2 = pool2 ? 1 : 0;
+  l.out_bits = out_bits;
+  return add_tensor(net, l, {cout, ho, wo, out_bits});
+}
+
+int qnet_add_avgpool(qnet* net, int src) {
+  if (!valid_src(net, src)) return QCONV_EINVAL;
+  const QTensor s = net->t[src];
+  if (s.bits != 0) return QCONV_EINVAL;
+  QLayer l;
+  l.kind = L_AVGPOOL;
+  l.src = src;
+  return add_tensor(net, l, {s.c, 1, 1, 0});
+}
+
+int qnet_add_fc_f32(qnet* net, int src, const float* w, const float* bias, int out_features) {
+  if (!valid_src(net, src) || !w || out_features < 1) return QCONV_EINVAL;
+  const QTensor s = net->t[src];
+  if (s.bits != 0 && !(s.bits == 1 && s.h == 1 && s.w == 1)) return QCONV_EUNSUPPORTED;
+  QLayer l;
+  l.kind = L_FC_F32;
+  l.src = src;
+  l.wf = w;
+  l.bias = bias;
+  l.cout = out_features;
+  return add_tensor(net, l, {out_features, 1, 1, 0});
+}
+
+size_t qnet_workspace_bytes(const qnet* net, int batch) {
+  if (!net || batch < 0) return 0;
+  return plan(net, batch, nullptr, nullptr);
+}
+
+int qnet_tensor_info(const qnet* net, int id, int batch, int* c, int* h, int* w, int* bits,
+                     size_t* ws_offset) {
+  if (!valid_src(net, id) || batch < 0) return QCONV_EINVAL;
+  const QTensor& t = net->t[id];
+  if (c) *c = t.c;
+  if (h) *h = t.h;
+  if (w) *w = t.w;
+  if (bits) *bits = t.bits;
+  if (ws_offset) {
+    std::vector<size_t> toff;
+    plan(net, batch, &toff, nullptr);
+    *ws_offset = toff[id];
+  }
+  return QCONV_OK;
+}
+
+int qnet_forward(const qnet* net, const float* x, int batch, float* logits, void* workspace,
+                 size_t workspace_bytes, void* stream) {
+  if (!net || batch < 0 || net->L.empty()) return QCONV_EINVAL;
+  if (batch == 0) return QCONV_OK;
+  if (!x || !logits) return QCONV_EINVAL;
+  const QTensor& last = net->t.back();
+  if (last.bits != 0) return QCONV_EUNSUPPORTED;
+  std::vector<size_t> toff, woff;
+  const size_t need = plan(net, batch, &toff, &woff);
+  if (workspace_bytes < need) return QCONV_EWORKSPACE;
+  if (need > 0 && !workspace) return QCONV_EINVAL;
+  char* ws = static_cast<char*>(workspace);
+  hipStream_t s = (hipStream_t)stream;
+  const int last_id = (int)net->t.size() - 1;
+  auto ptr = [&](int id) -> void* {
+    if (id == 0) return const_cast<float*>(x);
+    if (id == last_id) return logits;
+    return ws + toff[id];
+  };
+  Thr dflt[4];
+  for (int b = 1; b <= 3; ++b) act_thresholds(b, nullptr, &dflt[b]);
+  for (size_t i = 0; i < net->L.size(); ++i) {
+    const QLayer& l = net->L[i];
+    const int dst = (int)i + 1;
+    const QTensor& si = net->t[l.src];
+    const QTensor& so = net->t[dst];
+    int rc = QCONV_OK;
+    switch (l.kind) {
+      case L_CONV_F32: {
+        float* wt = reinterpret_cast<float*>(ws + woff[i]);
+        rc = launch_transpose_conv_weight(l.wf, l.cout, si.c, l.k, wt, s);
+        if (rc) return rc;
+        rc = launch_conv_f32(static_cast<const float*>(ptr(l.src)), wt, batch, si.c, si.h, si.w,
+                             l.cout, l.k, l.stride, l.pad, l.bn_k, l.bn_b, l.relu, l.out_bits,
+                             dflt[l.out_bits ? l.out_bits : 1],
+                             l.out_bits ? nullptr : static_cast<float*>(ptr(dst)),
+                             l.out_bits ? static_cast<uint32_t*>(ptr(dst)) : nullptr, s);
+        break;
+      }
+      case L_MAXPOOL_F32:
+        rc = launch_maxpool_f32(static_cast<const float*>(ptr(l.src)), batch, si.c, si.h, si.w,
+                                l.k, l.stride, l.pad, static_cast<float*>(ptr(dst)), s);
+        break;
+      case L_QUANTIZE:
+        rc = launch_pack_act(static_cast<const float*>(ptr(l.src)), batch, si.c, si.h, si.w,
+                             l.out_bits, dflt[l.out_bits], static_cast<uint32_t*>(ptr(dst)), s);
+        break;
+      case L_QCONV: {
+        qconv_desc d = {batch, si.c, si.h, si.w, l.cout, l.k, l.k, l.stride, l.pad,
+                        si.bits, l.w_bits, QCONV_ALGO_AUTO};
+        qconv_epilogue e;
+        memset(&e, 0, sizeof(e));
+        e.mode = l.out_bits ? QCONV_EPI_BN_PACK : QCONV_EPI_BN_F32;
+        e.flags = (l.pool2 ? QCONV_EPI_POOL2 : 0) | (l.src2 > 0 ? QCONV_EPI_RESIDUAL : 0);
+        e.bn_k = l.bn_k;
+        e.bn_b = l.bn_b;
+        e.residual = l.src2 > 0 ? static_cast<const float*>(ptr(l.src2)) : nullptr;
+        e.out_bits = l.out_bits;
+        rc = qconv_forward(&d, static_cast<const uint32_t*>(ptr(l.src)), l.wq, &e,
+                           l.out_bits ? nullptr : ptr(dst),
+                           l.out_bits ? static_cast<uint32_t*>(ptr(dst)) : nullptr, stream);
+        break;
+      }
+      case L_AVGPOOL:
+        rc = launch_avgpool_f32(static_cast<const float*>(ptr(l.src)), batch, si.c, si.h, si.w,
+                                static_cast<float*>(ptr(dst)), s);
+        break;
+      case L_FC_F32:
+        rc = launch_fc_f32(ptr(l.src), si.bits, batch, si.c * si.h * si.w, l.wf, l.bias, l.cout,
+                           static_cast<float*>(ptr(dst)), s);
+        break;
+      default:
+        return QCONV_EINVAL;
+    }
+    (void)so;
+    if (rc) return rc;
+  }
+  return QCONV_OK;
+}
+
+}  // extern "C"

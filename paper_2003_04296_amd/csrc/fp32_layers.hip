@@ -1,0 +1,221 @@
+// fp32_layers.hip -- full-precision support layers around the quantized
+// layers: the first convolution (its input is the image, which the paper
+// leaves unquantized, Sec. III-E), max/average pooling and the last FC.
+//
+// Every output of the first conv and of the FC is one chain of
+// single-rounding fused multiply-adds in a fixed input order, started from
+// +0, so the result does not depend on the launch configuration.  That makes
+// the binarisation after the first layer reproducible bit for bit.
+#include "qconv_internal.h"
+
+namespace qc {
+
+namespace {
+
+constexpr int CONV_TN = 32;  // output channels per wave (weights via the scalar cache)
+
+// OIHW -> [cin][k][k][cout_pad32] so that the TN weights of one tap are one
+// contiguous, wave-uniform run.
+__global__ void transpose_weight_kernel(const float* __restrict__ w, int cout, int cin, int kk,
+                                        int cop, float* __restrict__ wt) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t total = (int64_t)cin * kk * cop;
+  if (i >= total) return;
+  const int co = (int)(i % cop);
+  const int64_t tap = i / cop;  // ci * kk + (ky * k + kx)
+  wt[i] = (co < cout) ? w[(int64_t)co * cin * kk + tap] : 0.0f;
+}
+
+template <int OUT_BITS>
+__global__ __launch_bounds__(256) void conv_f32_kernel(const float* __restrict__ x,
+                                                       const float* __restrict__ wt, int n, int cin,
+                                                       int h, int w, int cout, int cop, int k,
+                                                       int stride, int pad, int ho, int wo,
+                                                       const float* __restrict__ bn_k,
+                                                       const float* __restrict__ bn_b, int relu,
+                                                       Thr othr, float* __restrict__ out,
+                                                       uint32_t* __restrict__ out_packed) {
+  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t total = (int64_t)n * ho * wo;
+  if (g >= total) return;
+  const int co0 = blockIdx.y * CONV_TN;
+  const int ow = (int)(g % wo);
+  const int64_t r = g / wo;
+  const int oh = (int)(r % ho);
+  const int b = (int)(r / ho);
+  float acc[CONV_TN];
+#pragma unroll
+  for (int j = 0; j < CONV_TN; ++j) acc[j] = 0.0f;
+  const float* xb = x + (int64_t)b * cin * h * w;
+  for (int ci = 0; ci < cin; ++ci) {
+    for (int ky = 0; ky < k; ++ky) {
+      const int ih = oh * stride - pad + ky;
+      if (ih < 0 || ih >= h) continue;
+      for (int kx = 0; kx < k; ++kx) {
+        const int iw = ow * stride - pad + kx;
+        if (iw < 0 || iw >= w) continue;
+        const float xv = xb[((int64_t)ci * h + ih) * w + iw];
+        const float* wp = wt + ((int64_t)(ci * k + ky) * k + kx) * cop + co0;
+#pragma unroll
+        for (int j = 0; j < CONV_TN; ++j) acc[j] = fmaf(xv, wp[j], acc[j]);
+      }
+    }
+  }
+  const int64_t plane = (int64_t)ho * wo;
+  uint32_t words[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int j = 0; j < CONV_TN; ++j) {
+    const int co = co0 + j;
+    if (co >= cout) break;
+    float z = fmaf(bn_k[co], acc[j], bn_b[co]);
+    if (relu) z = (z > 0.0f) ? z : 0.0f;
+    if constexpr (OUT_BITS == 0) {
+      out[((int64_t)b * cout + co) * plane + (int64_t)oh * wo + ow] = z;
+    } else {
+      const uint32_t pl = quant_planes<OUT_BITS>(hardtanh(z), othr);
+#pragma unroll
+      for (int p = 0; p < 4; ++p) words[p] |= ((pl >> p) & 1u) << j;
+    }
+  }
+  if constexpr (OUT_BITS != 0) {
+    constexpr int P = planes_of(OUT_BITS);
+    const int cwn = ceil_div(cout, 32);
+    uint32_t* dst = out_packed + ((((int64_t)b * ho + oh) * wo + ow) * cwn + (co0 >> 5)) * P;
+#pragma unroll
+    for (int p = 0; p < P; ++p) dst[p] = words[p];
+  }
+}
+
+__global__ __launch_bounds__(256) void maxpool_f32_kernel(const float* __restrict__ x, int n,
+                                                          int c, int h, int w, int k, int stride,
+                                                          int pad, int ho, int wo,
+                                                          float* __restrict__ y) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t total = (int64_t)n * c * ho * wo;
+  if (i >= total) return;
+  const int ow = (int)(i % wo);
+  const int64_t r = i / wo;
+  const int oh = (int)(r % ho);
+  const int64_t bc = r / ho;
+  const float* p = x + bc * h * w;
+  float m = -INFINITY;
+  for (int dy = 0; dy < k; ++dy) {
+    const int ih = oh * stride - pad + dy;
+    if (ih < 0 || ih >= h) continue;
+    for (int dx = 0; dx < k; ++dx) {
+      const int iw = ow * stride - pad + dx;
+      if (iw < 0 || iw >= w) continue;
+      const float v = p[(int64_t)ih * w + iw];
+      if (v > m) m = v;
+    }
+  }
+  y[i] = m;
+}
+
+__global__ __launch_bounds__(256) void avgpool_f32_kernel(const float* __restrict__ x,
+                                                          int64_t nc, int hw,
+                                                          float* __restrict__ y) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= nc) return;
+  const float* p = x + i * hw;
+  float s = 0.0f;
+  for (int j = 0; j < hw; ++j) s += p[j];
+  y[i] = s / (float)hw;
+}
+
+constexpr int FC_TN = 16;  // outputs per lane; lanes = images
+
+template <int X_BITS>
+__global__ __launch_bounds__(64) void fc_f32_kernel(const void* __restrict__ xin, int n, int in,
+                                                    const float* __restrict__ w,
+                                                    const float* __restrict__ bias, int out,
+                                                    float* __restrict__ y) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= n) return;
+  const int o0 = blockIdx.y * FC_TN;
+  float acc[FC_TN];
+#pragma unroll
+  for (int j = 0; j < FC_TN; ++j) acc[j] = 0.0f;
+  const int cwn = (in + 31) >> 5;
+  for (int i = 0; i < in; ++i) {
+    float xv;
+    if constexpr (X_BITS == 0) {
+      xv = static_cast<const float*>(xin)[(int64_t)b * in + i];
+    } else {
+      const uint32_t word = static_cast<const uint32_t*>(xin)[(int64_t)b * cwn + (i >> 5)];
+      xv = ((word >> (i & 31)) & 1u) ? 1.0f : -1.0f;
+    }
+#pragma unroll
+    for (int j = 0; j < FC_TN; ++j) {
+      const int o = min(o0 + j, out - 1);
+      acc[j] = fmaf(xv, w[(int64_t)o * in + i], acc[j]);
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < FC_TN; ++j) {
+    const int o = o0 + j;
+    if (o < out) y[(int64_t)b * out + o] = acc[j] + (bias ? bias[o] : 0.0f);
+  }
+}
+
+}  // namespace
+
+int launch_transpose_conv_weight(const float* w, int cout, int cin, int k, float* wt,
+                                 hipStream_t s) {
+  const int cop = ceil_div(cout, CONV_TN) * CONV_TN;
+  const int64_t total = (int64_t)cin * k * k * cop;
+  transpose_weight_kernel<<<(unsigned)((total + 255) / 256), 256, 0, s>>>(w, cout, cin, k * k, cop,
+                                                                           wt);
+  return hip_status();
+}
+
+int launch_conv_f32(const float* x, const float* wt, int n, int cin, int h, int w, int cout, int k,
+                    int stride, int pad, const float* bn_k, const float* bn_b, int relu,
+                    int out_bits, Thr othr, float* out_f32, uint32_t* out_packed, hipStream_t s) {
+  const int ho = (h + 2 * pad - k) / stride + 1, wo = (w + 2 * pad - k) / stride + 1;
+  const int cop = ceil_div(cout, CONV_TN) * CONV_TN;
+  const int64_t total = (int64_t)n * ho * wo;
+  if (total == 0) return QCONV_OK;
+  const dim3 grid((unsigned)((total + 255) / 256), (unsigned)(cop / CONV_TN));
+#define QC_F32(B)                                                                              \
+  conv_f32_kernel<B><<<grid, 256, 0, s>>>(x, wt, n, cin, h, w, cout, cop, k, stride, pad, ho, \
+                                          wo, bn_k, bn_b, relu, othr, out_f32, out_packed)
+  switch (out_bits) {
+    case 0: QC_F32(0); break;
+    case 1: QC_F32(1); break;
+    case 2: QC_F32(2); break;
+    default: QC_F32(3); break;
+  }
+#undef QC_F32
+  return hip_status();
+}
+
+int launch_maxpool_f32(const float* x, int n, int c, int h, int w, int k, int stride, int pad,
+                       float* y, hipStream_t s) {
+  const int ho = (h + 2 * pad - k) / stride + 1, wo = (w + 2 * pad - k) / stride + 1;
+  const int64_t total = (int64_t)n * c * ho * wo;
+  if (total == 0) return QCONV_OK;
+  maxpool_f32_kernel<<<(unsigned)((total + 255) / 256), 256, 0, s>>>(x, n, c, h, w, k, stride,
+                                                                     pad, ho, wo, y);
+  return hip_status();
+}
+
+int launch_avgpool_f32(const float* x, int n, int c, int h, int w, float* y, hipStream_t s) {
+  const int64_t nc = (int64_t)n * c;
+  if (nc == 0) return QCONV_OK;
+  avgpool_f32_kernel<<<(unsigned)((nc + 255) / 256), 256, 0, s>>>(x, nc, h * w, y);
+  return hip_status();
+}
+
+int launch_fc_f32(const void* x, int x_bits, int n, int in, const float* w, const float* bias,
+                  int out, float* y, hipStream_t s) {
+  if (n == 0) return QCONV_OK;
+  const dim3 grid((unsigned)ceil_div(n, 64), (unsigned)ceil_div(out, FC_TN));
+  if (x_bits == 0)
+    fc_f32_kernel<0><<<grid, 64, 0, s>>>(x, n, in, w, bias, out, y);
+  else
+    fc_f32_kernel<1><<<grid, 64, 0, s>>>(x, n, in, w, bias, out, y);
+  return hip_status();
+}
+
+}  // namespace qc

@@ -1,0 +1,139 @@
+// pack.hip -- quantize-and-pack kernels (Sec. III-C, Eq. 20 with the
+// quantizers of Eqs. 4, 21, 22).
+//
+// Activations: fp32 NCHW -> bitplanes [n][h][w][cw][P].  One thread owns one
+// (image, 32-channel word, pixel); consecutive lanes take consecutive pixels,
+// so each of the 32 channel reads of a wave is one contiguous 256-byte run
+// (HBM-bound: 4 bytes read per channel, P/8 bytes written).
+//
+// Weights: fp32 OIHW -> per-channel scale s_c = mean|W_c| (double, storage
+// order) -> thresholds scaled by s_c -> bitplanes [kh][kw][cw][cout_pad][P].
+#include "qconv_internal.h"
+
+namespace qc {
+
+namespace {
+
+template <int BITS>
+__global__ __launch_bounds__(256) void pack_act_kernel(const float* __restrict__ x, int c,
+                                                       int hw, int cwn, int64_t total, Thr t,
+                                                       uint32_t* __restrict__ out) {
+  constexpr int P = planes_of(BITS);
+  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (tid >= total) return;
+  const int pix = (int)(tid % hw);
+  const int64_t r = tid / hw;
+  const int cw = (int)(r % cwn);
+  const int64_t b = r / cwn;
+  const int c0 = cw * 32;
+  const int nch = min(32, c - c0);
+  const float* src = x + (b * c + c0) * (int64_t)hw + pix;
+  uint32_t word[P];
+#pragma unroll
+  for (int p = 0; p < P; ++p) word[p] = 0u;
+  if (nch == 32) {
+#pragma unroll 8
+    for (int j = 0; j < 32; ++j) {
+      const uint32_t pl = quant_planes<BITS>(src[(int64_t)j * hw], t);
+#pragma unroll
+      for (int p = 0; p < P; ++p) word[p] |= ((pl >> p) & 1u) << j;
+    }
+  } else {
+    for (int j = 0; j < nch; ++j) {
+      const uint32_t pl = quant_planes<BITS>(src[(int64_t)j * hw], t);
+#pragma unroll
+      for (int p = 0; p < P; ++p) word[p] |= ((pl >> p) & 1u) << j;
+    }
+  }
+  uint32_t* dst = out + ((b * hw + pix) * cwn + cw) * P;
+#pragma unroll
+  for (int p = 0; p < P; ++p) dst[p] = word[p];
+}
+
+// s_c = (float)(sum_k |W_ck| / K), the sum in double in storage order.
+__global__ void weight_scale_kernel(const float* __restrict__ w, int cout, int k,
+                                    float* __restrict__ scale) {
+  const int co = blockIdx.x * blockDim.x + threadIdx.x;
+  if (co >= cout) return;
+  const float* p = w + (int64_t)co * k;
+  double sum = 0.0;
+  for (int i = 0; i < k; ++i) sum += fabs((double)p[i]);
+  scale[co] = (float)(sum / (double)k);
+}
+
+template <int BITS>
+__global__ __launch_bounds__(256) void pack_weight_kernel(const float* __restrict__ w, int cout,
+                                                          int cin, int kh, int kw, int cwn,
+                                                          int cop, Thr base,
+                                                          const float* __restrict__ scale,
+                                                          uint32_t* __restrict__ out) {
+  constexpr int P = planes_of(BITS);
+  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t total = (int64_t)kh * kw * cwn * cop;
+  if (tid >= total) return;
+  const int co = (int)(tid % cop);
+  int64_t r = tid / cop;
+  const int cw = (int)(r % cwn);
+  r /= cwn;
+  const int x = (int)(r % kw);
+  const int y = (int)(r / kw);
+  uint32_t word[P];
+#pragma unroll
+  for (int p = 0; p < P; ++p) word[p] = 0u;
+  if (co < cout) {
+    Thr t = {0.0f, 0.0f, 0.0f};
+    if constexpr (BITS > 1) {
+      const double s = (double)scale[co];
+      t.t0 = (float)((double)base.t0 * s);
+      t.t1 = (float)((double)base.t1 * s);
+      t.t2 = (float)((double)base.t2 * s);
+    }
+    const int c0 = cw * 32;
+    const int nch = min(32, cin - c0);
+    for (int j = 0; j < nch; ++j) {
+      const float v = w[(((int64_t)co * cin + c0 + j) * kh + y) * kw + x];
+      const uint32_t pl = quant_planes<BITS>(v, t);
+#pragma unroll
+      for (int p = 0; p < P; ++p) word[p] |= ((pl >> p) & 1u) << j;
+    }
+  }
+  uint32_t* dst = out + tid * P;
+#pragma unroll
+  for (int p = 0; p < P; ++p) dst[p] = word[p];
+}
+
+}  // namespace
+
+int launch_pack_act(const float* x, int n, int c, int h, int w, int bits, Thr t, uint32_t* out,
+                    hipStream_t s) {
+  const int hw = h * w;
+  const int cwn = ceil_div(c, 32);
+  const int64_t total = (int64_t)n * cwn * hw;
+  if (total == 0) return QCONV_OK;
+  const dim3 grid((unsigned)((total + 255) / 256));
+  switch (bits) {
+    case 1: pack_act_kernel<1><<<grid, 256, 0, s>>>(x, c, hw, cwn, total, t, out); break;
+    case 2: pack_act_kernel<2><<<grid, 256, 0, s>>>(x, c, hw, cwn, total, t, out); break;
+    default: pack_act_kernel<3><<<grid, 256, 0, s>>>(x, c, hw, cwn, total, t, out); break;
+  }
+  return hip_status();
+}
+
+int launch_pack_weight(const float* w, int cout, int cin, int kh, int kw, int bits,
+                       const float* base_thr, uint32_t* out, float* scale, hipStream_t s) {
+  const int k = cin * kh * kw;
+  weight_scale_kernel<<<ceil_div(cout, 64), 64, 0, s>>>(w, cout, k, scale);
+  const int cwn = ceil_div(cin, 32);
+  const int cop = cout_pad(cout);
+  const int64_t total = (int64_t)kh * kw * cwn * cop;
+  const dim3 grid((unsigned)((total + 255) / 256));
+  Thr b = {base_thr[0], base_thr[1], base_thr[2]};
+  switch (bits) {
+    case 1: pack_weight_kernel<1><<<grid, 256, 0, s>>>(w, cout, cin, kh, kw, cwn, cop, b, scale, out); break;
+    case 2: pack_weight_kernel<2><<<grid, 256, 0, s>>>(w, cout, cin, kh, kw, cwn, cop, b, scale, out); break;
+    default: pack_weight_kernel<3><<<grid, 256, 0, s>>>(w, cout, cin, kh, kw, cwn, cop, b, scale, out); break;
+  }
+  return hip_status();
+}
+
+}  // namespace qc

@@ -1,0 +1,178 @@
+"""Host-side tests of the C ABI (CPU only, no kernel is launched): the
+library loads and exports every function include/qconv.h declares, status
+strings, the inference-operation rule against Table I, size queries, BN
+folding against the oracle, and argument validation that must reject bad
+input before any launch."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2003_04296_amd as q
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "qconv.h")
+GOLDEN = os.path.join(ROOT, "tests", "golden", "dispatch_table1.txt")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"\b((?:qconv|qnet)_[a-z0-9_]+)\s*\(", text)
+    return sorted(set(names))
+
+
+def test_library_exports_every_declared_function():
+    L = q.lib()
+    declared = _declared_functions()
+    assert len(declared) >= 20
+    missing = [n for n in declared if not hasattr(L, n)]
+    assert not missing, missing
+    assert set(declared) == set(q.EXPORTED)
+
+
+def test_error_strings():
+    L = q.lib()
+    for code in (0, -1, -2, -3, -4, -5):
+        s = L.qconv_error_string(code).decode()
+        assert s and s != "unknown status"
+    assert L.qconv_error_string(-99).decode() == "unknown status"
+
+
+def test_inference_op_matches_table1():
+    rows = [ln.split() for ln in open(GOLDEN) if ln.strip() and not ln.startswith("#")]
+    assert len(rows) == 16
+    for m, n, op, prec in rows:
+        got_op, got_bits = q.inference_op(int(m), int(n))
+        assert got_op == op, (m, n)
+        want_bits = int(prec.split("-")[0])
+        assert got_bits == want_bits, (m, n)
+
+
+def test_inference_op_rejects_other_widths():
+    op, prec = ctypes.c_int(), ctypes.c_int()
+    assert q.lib().qconv_inference_op(4, 1, ctypes.byref(op), ctypes.byref(prec)) == q.QCONV_EINVAL
+
+
+@pytest.mark.parametrize("n,c,h,w,bits", [(1, 1, 1, 1, 1), (2, 33, 5, 7, 2), (256, 128, 32, 32, 2), (3, 64, 4, 4, 3)])
+def test_packed_act_size(n, c, h, w, bits):
+    want = n * h * w * ((c + 31) // 32) * {1: 1, 2: 2, 3: 4}[bits] * 4
+    assert q.lib().qconv_packed_act_bytes(n, c, h, w, bits) == want
+
+
+@pytest.mark.parametrize("cout,cin,k,bits", [(128, 128, 3, 1), (10, 33, 1, 2), (512, 256, 3, 3)])
+def test_packed_weight_size(cout, cin, k, bits):
+    want = k * k * ((cin + 31) // 32) * ((cout + 63) // 64 * 64) * {1: 1, 2: 2, 3: 4}[bits] * 4
+    assert q.lib().qconv_packed_weight_bytes(cout, cin, k, k, bits) == want
+
+
+def test_size_queries_reject_bad_input():
+    L = q.lib()
+    assert L.qconv_packed_act_bytes(1, 0, 1, 1, 1) == 0
+    assert L.qconv_packed_act_bytes(1, 1, 1, 1, 4) == 0
+    assert L.qconv_packed_weight_bytes(0, 1, 1, 1, 1) == 0
+
+
+def test_out_size():
+    assert q.out_size(32, 3, 1, 1) == 32
+    assert q.out_size(224, 7, 2, 3) == 112
+    assert q.out_size(56, 1, 2, 0) == 28
+    assert q.lib().qconv_out_size(2, 5, 1, 0) == q.QCONV_EINVAL
+
+
+def test_fold_bn_matches_oracle(oracle_mod):
+    rng = np.random.default_rng(0)
+    c = 64
+    bn = {"gamma": rng.uniform(0.5, 1.5, c).astype(np.float32), "beta": rng.normal(0, 0.3, c).astype(np.float32),
+          "mean": rng.normal(0, 1, c).astype(np.float32), "var": rng.uniform(1, 2000, c).astype(np.float32),
+          "eps": 1e-5}
+    k, b = q.fold_bn(bn["gamma"], bn["beta"], bn["mean"], bn["var"], bn["eps"])
+    ko, bo = oracle_mod.bn_fold(bn)
+    np.testing.assert_array_equal(k, ko)
+    np.testing.assert_array_equal(b, bo)
+
+
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails validation first
+
+
+def _desc(**kw):
+    base = dict(n=1, cin=32, h=8, w=8, cout=32, kh=3, kw=3, stride=1, pad=1, a_bits=1, w_bits=1, algo=0)
+    base.update(kw)
+    return q.qconv_desc(*[base[f] for f, _ in q.qconv_desc._fields_])
+
+
+def _fwd(d, e, out=FAKE, out_packed=None):
+    return q.lib().qconv_forward(ctypes.byref(d), FAKE, FAKE, ctypes.byref(e), out, out_packed, None)
+
+
+@pytest.mark.parametrize("bad", [dict(a_bits=0), dict(w_bits=4), dict(cin=0), dict(kh=0), dict(stride=0),
+                                 dict(pad=-1), dict(h=1, pad=0), dict(algo=7), dict(n=-1)])
+def test_forward_rejects_bad_desc(bad):
+    e = q.qconv_epilogue(q.EPI_INT32, 0, None, None, None, None, 0, None)
+    assert _fwd(_desc(**bad), e) == q.QCONV_EINVAL
+
+
+def test_forward_rejects_overflowing_k():
+    e = q.qconv_epilogue(q.EPI_INT32, 0, None, None, None, None, 0, None)
+    # K = 134218000 * 1 * 1 with 3-bit codes (max 4*4) exceeds 2^31
+    assert _fwd(_desc(cin=134218000, kh=1, kw=1, pad=0, a_bits=3, w_bits=3), e) == q.QCONV_EOVERFLOW
+
+
+def test_forward_rejects_bad_epilogue():
+    d = _desc()
+    assert _fwd(d, q.qconv_epilogue(9, 0, None, None, None, None, 0, None)) == q.QCONV_EINVAL
+    assert _fwd(d, q.qconv_epilogue(q.EPI_SCALE_F32, 0, None, None, None, None, 0, None)) == q.QCONV_EINVAL
+    assert _fwd(d, q.qconv_epilogue(q.EPI_BN_F32, 0, None, FAKE, None, None, 0, None)) == q.QCONV_EINVAL
+    assert _fwd(d, q.qconv_epilogue(q.EPI_BN_PACK, 0, None, FAKE, FAKE, None, 1, None), out_packed=None) == q.QCONV_EINVAL
+    assert _fwd(d, q.qconv_epilogue(q.EPI_BN_PACK, 0, None, FAKE, FAKE, None, 5, None), out_packed=FAKE) == q.QCONV_EINVAL
+    assert _fwd(d, q.qconv_epilogue(q.EPI_INT32, 0x10, None, None, None, None, 0, None)) == q.QCONV_EINVAL
+    assert _fwd(d, q.qconv_epilogue(q.EPI_INT32, q.EPI_RESIDUAL, None, None, None, FAKE, 0, None)) == q.QCONV_EINVAL
+    d1 = _desc(h=1, w=1, pad=0, kh=1, kw=1)
+    assert _fwd(d1, q.qconv_epilogue(q.EPI_INT32, q.EPI_POOL2, None, None, None, None, 0, None)) == q.QCONV_EINVAL
+    bad_thr = (ctypes.c_float * 3)(0.5, 0.25, 0.75)
+    e = q.qconv_epilogue(q.EPI_BN_PACK, 0, None, FAKE, FAKE, None, 3, ctypes.cast(bad_thr, ctypes.c_void_p))
+    assert _fwd(d, e, out_packed=FAKE) == q.QCONV_EINVAL
+
+
+def test_pack_calls_reject_bad_input():
+    L = q.lib()
+    assert L.qconv_pack_act(FAKE, 1, 1, 1, 1, 0, None, FAKE, None) == q.QCONV_EINVAL
+    assert L.qconv_pack_act(None, 1, 1, 1, 1, 1, None, FAKE, None) == q.QCONV_EINVAL
+    neg = (ctypes.c_float * 1)(-0.5)
+    assert L.qconv_pack_act(FAKE, 1, 1, 1, 1, 2, neg, FAKE, None) == q.QCONV_EINVAL
+    assert L.qconv_pack_weight(FAKE, 1, 1, 1, 1, 2, None, FAKE, None, None) == q.QCONV_EINVAL
+    dec = (ctypes.c_float * 3)(0.3, 0.2, 0.9)
+    assert L.qconv_pack_weight(FAKE, 1, 1, 1, 1, 3, dec, FAKE, FAKE, None) == q.QCONV_EINVAL
+
+
+def test_qnet_validation_and_workspace():
+    L = q.lib()
+    assert not L.qnet_create(0, 32, 32)
+    net = q.Net(3, 32, 32)
+    h = net._h
+    assert L.qnet_add_qconv(h, 0, FAKE, 16, 3, 1, 1, 1, 0, FAKE, FAKE, -1, 1) == q.QCONV_EINVAL  # fp32 source
+    assert L.qnet_add_conv_f32(h, 5, FAKE, 16, 3, 1, 1, FAKE, FAKE, 0, 1) == q.QCONV_EINVAL  # no tensor 5
+    t1 = L.qnet_add_conv_f32(h, 0, FAKE, 16, 3, 1, 1, FAKE, FAKE, 0, 1)
+    assert t1 == 1
+    assert L.qnet_add_maxpool_f32(h, t1, 2, 2, 0) == q.QCONV_EINVAL  # packed source
+    t2 = L.qnet_add_qconv(h, t1, FAKE, 16, 3, 1, 1, 1, 1, FAKE, FAKE, -1, 0)
+    assert t2 == 2
+    assert net.tensor_info(t2, 4)[:4] == (16, 16, 16, 0)
+    t3 = L.qnet_add_avgpool(h, t2)
+    t4 = L.qnet_add_fc_f32(h, t3, FAKE, None, 10)
+    assert t4 == 4
+    need = net.workspace_bytes(4)
+    # packed conv1 output + fp32 conv2 output + avgpool + transposed conv1 weights
+    assert need >= 4 * 32 * 32 * 4 + 4 * 16 * 16 * 16 * 4 + 4 * 16 * 4
+    rc = L.qnet_forward(h, FAKE, 4, FAKE, FAKE, need - 1, None)
+    assert rc == q.QCONV_EWORKSPACE
+    assert L.qnet_forward(h, None, 4, FAKE, FAKE, need, None) == q.QCONV_EINVAL
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(q, "_lib", None)
+    monkeypatch.setattr(q, "LIB_PATH", str(tmp_path / "absent.so"))
+    with pytest.raises(RuntimeError, match="no CPU fallback"):
+        q.lib()

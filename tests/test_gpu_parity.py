@@ -1,0 +1,362 @@
+"""GPU parity of the HIP path against the CPU oracle (run with -m gpu).
+
+Integer results (packed levels, accumulators) must match bit for bit.  The
+fp32 epilogues are single-rounding fmaf / multiply / add in both
+implementations and must match bit for bit as well (the 1e-3 relative bar is
+the floor; exact equality is what is asserted).  Inputs come from the seeded
+generators; the oracle quantizes them itself and never sees GPU output."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2003_04296_amd as q
+from paper_2003_04296_amd import synth
+from helpers import tail_bits_zero, unpack_act, unpack_weight
+
+pytestmark = pytest.mark.gpu
+
+BIT_PAIRS = [(1, 1), (2, 1), (1, 2), (2, 2), (3, 3), (3, 1), (1, 3), (3, 2), (2, 3)]  # (a_bits, w_bits)
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    oracle.lib()
+    q.lib()
+    return torch.device("cuda:0")
+
+
+def _inputs(seed, n, cin, h, w, cout, k, special=True):
+    g = synth.generator(seed)
+    x = synth.normal(g, (n, cin, h, w), 1.0)
+    wt = synth.normal(g, (cout, cin, k, k), 2.0 / (cin * k * k))
+    if special and x.numel() > 16:
+        flat = x.view(-1)
+        vals = torch.tensor([0.0, -0.0, float("nan"), 0.5, -0.5, 0.125, 0.375, 0.75, -0.75, 1e-40, -1e-40, 3.0])
+        flat[:vals.numel()] = vals
+    return x, wt
+
+
+def _bn(seed, cout):
+    g = synth.generator(seed + 7)
+    k = synth.uniform(g, (cout,), 0.001, 0.05)
+    b = synth.normal(g, (cout,), 0.1)
+    return k, b
+
+
+# ---------------------------------------------------------------------------
+# quantize + pack
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("bits", [1, 2, 3])
+@pytest.mark.parametrize("shape", [(1, 1, 1, 1), (2, 40, 9, 7), (3, 64, 5, 5), (2, 100, 3, 3), (1, 32, 17, 31)])
+def test_pack_act_matches_oracle_levels(dev, bits, shape):
+    n, c, h, w = shape
+    x, _ = _inputs(11, n, c, h, w, 1, 1)
+    words = q.pack_act(x.to(dev), bits)
+    torch.cuda.synchronize()
+    got = unpack_act(words.cpu().numpy(), n, c, h, w, bits)
+    np.testing.assert_array_equal(got, oracle.quantize(x.numpy(), bits))
+    assert tail_bits_zero(words.cpu().numpy(), c, bits)
+
+
+@pytest.mark.parametrize("bits", [1, 2, 3])
+@pytest.mark.parametrize("shape", [(1, 1, 1, 1), (70, 40, 3, 3), (128, 128, 3, 3), (33, 64, 1, 1), (16, 512, 4, 4)])
+def test_pack_weight_matches_oracle(dev, bits, shape):
+    cout, cin, kh, kw = shape
+    _, w = _inputs(12, 1, cin, 1, 1, cout, kh, special=False)
+    words, scale = q.pack_weight(w.to(dev), bits)
+    torch.cuda.synchronize()
+    lv, s = oracle.quantize_weights(w.numpy(), bits)
+    np.testing.assert_array_equal(scale.cpu().numpy(), s)
+    np.testing.assert_array_equal(unpack_weight(words.cpu().numpy(), cout, cin, kh, kw, bits), lv)
+    # padding rows of the weight layout are zero
+    cop = (cout + 63) // 64 * 64
+    wd = words.cpu().numpy().view(np.uint32).reshape(kh, kw, (cin + 31) // 32, cop, -1)
+    assert np.all(wd[:, :, :, cout:, :] == 0)
+
+
+# ---------------------------------------------------------------------------
+# the quantized product, element by element
+# ---------------------------------------------------------------------------
+
+CONV_CASES = [
+    # n, cin, h, w, cout, k, stride, pad
+    (2, 32, 8, 8, 32, 3, 1, 1),
+    (3, 40, 9, 7, 70, 3, 1, 1),     # ragged cin and cout
+    (2, 64, 13, 13, 96, 3, 2, 1),   # stride 2
+    (1, 33, 7, 7, 40, 1, 2, 0),     # 1x1 stride 2 (ResNet shortcut)
+    (2, 96, 6, 6, 33, 4, 1, 0),     # kernel covering a 4x4 map (FC as conv)
+    (1, 7, 11, 11, 17, 7, 2, 3),    # 7x7 / 2 pad 3
+    (2, 31, 20, 20, 64, 3, 1, 1),   # 800 pixels: several 256-pixel blocks + ragged tail
+    (1, 160, 1, 1, 100, 1, 1, 0),   # 1x1 map (FC)
+]
+
+
+def _gpu_conv(dev, x, w, a_bits, w_bits, stride, pad, algo=q.ALGO_AUTO, **epi):
+    n, cin, h, ww = x.shape
+    cout, _, k, _ = w.shape
+    act = q.pack_act(x.to(dev), a_bits)
+    wq, scale = q.pack_weight(w.to(dev), w_bits)
+    out, outp = q.conv(act, wq, n, cin, h, ww, cout, k, stride, pad, a_bits, w_bits, algo=algo, **epi)
+    torch.cuda.synchronize()
+    return out, outp, scale
+
+
+def _oracle_acc(x, w, a_bits, w_bits, stride, pad):
+    la = oracle.quantize(x.numpy(), a_bits)
+    lw, s = oracle.quantize_weights(w.numpy(), w_bits)
+    return oracle.qconv_acc(la, lw, a_bits, stride, pad), s
+
+
+@pytest.mark.parametrize("bits", BIT_PAIRS)
+@pytest.mark.parametrize("case", CONV_CASES)
+def test_conv_int32_bit_exact(dev, bits, case):
+    n, cin, h, w, cout, k, s, p = case
+    ab, wb = bits
+    x, wt = _inputs(100 + sum(case), n, cin, h, w, cout, k)
+    out, _, _ = _gpu_conv(dev, x, wt, ab, wb, s, p, algo=q.ALGO_BITPLANE)
+    want, _ = _oracle_acc(x, wt, ab, wb, s, p)
+    np.testing.assert_array_equal(out.cpu().numpy(), want)
+
+
+def _scale_epi_conv(dev, x, wt, ab, wb):
+    n, cin, h, w = x.shape
+    cout, _, k, _ = wt.shape
+    act = q.pack_act(x.to(dev), ab)
+    wq, scale = q.pack_weight(wt.to(dev), wb)
+    out, _ = q.conv(act, wq, n, cin, h, w, cout, k, 1, 1, ab, wb, mode=q.EPI_SCALE_F32, scale=scale)
+    torch.cuda.synchronize()
+    return out
+
+
+@pytest.mark.parametrize("bits", [(1, 1), (3, 3)])
+def test_scale_epilogue_uses_mean_abs_weight(dev, bits):
+    ab, wb = bits
+    x, wt = _inputs(6, 2, 40, 9, 9, 70, 3)
+    out = _scale_epi_conv(dev, x, wt, ab, wb)
+    acc, s = _oracle_acc(x, wt, ab, wb, 1, 1)
+    shift = oracle.level_shift(ab) + oracle.level_shift(wb)
+    np.testing.assert_array_equal(out.cpu().numpy(), oracle.epi_scale(acc, s, shift))
+
+
+@pytest.mark.parametrize("bits", BIT_PAIRS)
+@pytest.mark.parametrize("pool", [False, True])
+@pytest.mark.parametrize("out_bits", [0, 1, 2, 3])
+def test_bn_epilogues(dev, bits, pool, out_bits):
+    """{QConv-[pool]-BN-HardTanh} -> fp32 output, or requantized + packed output."""
+    ab, wb = bits
+    n, cin, h, w, cout = 2, 40, 10, 9, 70
+    x, wt = _inputs(7, n, cin, h, w, cout, 3)
+    k, b = _bn(7, cout)
+    flags = q.EPI_POOL2 if pool else 0
+    mode = q.EPI_BN_PACK if out_bits else q.EPI_BN_F32
+    out, outp, _ = _gpu_conv(dev, x, wt, ab, wb, 1, 1, mode=mode, flags=flags, bn_k=k.to(dev), bn_b=b.to(dev),
+                             out_bits=out_bits)
+    acc, _ = _oracle_acc(x, wt, ab, wb, 1, 1)
+    if pool:
+        acc = oracle.maxpool2_int(acc)
+    shift = oracle.level_shift(ab) + oracle.level_shift(wb)
+    z = oracle.epi_bn(acc, k.numpy(), b.numpy(), shift)
+    if out_bits == 0:
+        np.testing.assert_array_equal(out.cpu().numpy(), z)
+    else:
+        want = oracle.quantize(oracle.hardtanh(z), out_bits)
+        got = unpack_act(outp.cpu().numpy(), n, cout, acc.shape[2], acc.shape[3], out_bits)
+        np.testing.assert_array_equal(got, want)
+        assert tail_bits_zero(outp.cpu().numpy(), cout, out_bits)
+
+
+@pytest.mark.parametrize("bits", [(2, 2), (1, 1), (3, 3)])
+def test_bn_residual_and_repack(dev, bits):
+    ab, wb = bits
+    n, cin, h, w, cout = 2, 64, 8, 8, 64
+    x, wt = _inputs(8, n, cin, h, w, cout, 3)
+    k, b = _bn(8, cout)
+    g = synth.generator(99)
+    res = synth.normal(g, (n, cout, h, w), 1.0)
+    act = q.pack_act(x.to(dev), ab)
+    wq, _ = q.pack_weight(wt.to(dev), wb)
+    outp = torch.empty(q.packed_act_words(n, cout, h, w, ab), dtype=torch.int32, device=dev)
+    out, _ = q.conv(act, wq, n, cin, h, w, cout, 3, 1, 1, ab, wb, mode=q.EPI_BN_F32, flags=q.EPI_RESIDUAL,
+                    bn_k=k.to(dev), bn_b=b.to(dev), residual=res.to(dev), out_bits=ab, out_packed=outp)
+    torch.cuda.synchronize()
+    acc, _ = _oracle_acc(x, wt, ab, wb, 1, 1)
+    shift = oracle.level_shift(ab) + oracle.level_shift(wb)
+    zz = oracle.add(oracle.epi_bn(acc, k.numpy(), b.numpy(), shift), res.numpy())
+    np.testing.assert_array_equal(out.cpu().numpy(), zz)
+    np.testing.assert_array_equal(unpack_act(outp.cpu().numpy(), n, cout, h, w, ab),
+                                  oracle.quantize(oracle.hardtanh(zz), ab))
+
+
+def test_empty_batch_is_a_no_op(dev):
+    x = torch.zeros((0, 32, 4, 4), device=dev)
+    act = q.pack_act(x, 1)
+    wq, _ = q.pack_weight(torch.ones((32, 32, 3, 3), device=dev), 1)
+    out, _ = q.conv(act, wq, 0, 32, 4, 4, 32, 3, 1, 1, 1, 1)
+    torch.cuda.synchronize()
+    assert out.numel() == 0
+
+
+def test_deterministic_rerun(dev):
+    x, wt = _inputs(9, 4, 128, 16, 16, 128, 3)
+    a1, _, _ = _gpu_conv(dev, x, wt, 2, 1, 1, 1)
+    a2, _, _ = _gpu_conv(dev, x, wt, 2, 1, 1, 1)
+    assert torch.equal(a1, a2)
+
+
+# ---------------------------------------------------------------------------
+# full-size workloads: sampled outputs + properties that hold at any size
+# ---------------------------------------------------------------------------
+
+def _sample_idx(shape, count, seed):
+    n, c, h, w = shape
+    rng = np.random.default_rng(seed)
+    idx = rng.choice(n * c * h * w, count, replace=False)
+    corners = []
+    for b in (0, n - 1):
+        for co in (0, c - 1):
+            for (yy, xx) in ((0, 0), (0, w - 1), (h - 1, 0), (h - 1, w - 1), (h // 2, 0)):
+                corners.append(((b * c + co) * h + yy) * w + xx)
+    return np.unique(np.concatenate([idx, np.array(corners, dtype=np.int64)]))
+
+
+def _check_sampled(case, out_int, seed, count=4096):
+    la = oracle.quantize(case.x.numpy(), case.a_bits)
+    lw, s = oracle.quantize_weights(case.w.numpy(), case.w_bits)
+    idx = _sample_idx(out_int.shape, count, seed)
+    want = oracle.conv_levels_at(la, lw, idx, case.stride, case.pad, oracle.pad_level(case.a_bits))
+    got = out_int.reshape(-1)[torch.from_numpy(idx).to(out_int.device)].cpu().numpy()
+    np.testing.assert_array_equal(got, want)
+    return idx, want, s
+
+
+def test_workload1_full(dev):
+    """1W1A, batch 4 x 128 x 32 x 32, 128 out, pad -1: int32 and s_c * acc, every output."""
+    case = synth.workload1()
+    n, c, h, w = case.x.shape
+    act = q.pack_act(case.x.to(dev), 1)
+    wq, scale = q.pack_weight(case.w.to(dev), 1)
+    acc, _ = q.conv(act, wq, n, c, h, w, 128, 3, 1, 1, 1, 1)
+    y, _ = q.conv(act, wq, n, c, h, w, 128, 3, 1, 1, 1, 1, mode=q.EPI_SCALE_F32, scale=scale)
+    torch.cuda.synchronize()
+    want, s = _oracle_acc(case.x, case.w, 1, 1, 1, 1)
+    np.testing.assert_array_equal(acc.cpu().numpy(), want)
+    np.testing.assert_array_equal(y.cpu().numpy(), oracle.epi_scale(want, s))
+
+
+def test_workload2_full_sampled(dev):
+    """1W2A, batch 256 x 128 x 32 x 32, BN epilogue, in the launch the benchmark times."""
+    case = synth.workload2()
+    n, c, h, w = case.x.shape
+    xd = case.x.to(dev)
+    act = q.pack_act(xd, 2)
+    wq, _ = q.pack_weight(case.w.to(dev), 1)
+    k, b = q.fold_bn(*(case.bn[kk].numpy() for kk in ("gamma", "beta", "mean", "var")), case.bn["eps"])
+    kd, bd = torch.from_numpy(k).to(dev), torch.from_numpy(b).to(dev)
+    z, _ = q.conv(act, wq, n, c, h, w, 128, 3, 1, 1, 2, 1, mode=q.EPI_BN_F32, bn_k=kd, bn_b=bd)
+    acc, _ = q.conv(act, wq, n, c, h, w, 128, 3, 1, 1, 2, 1, algo=q.ALGO_BITPLANE)
+    torch.cuda.synchronize()
+    idx, want, _ = _check_sampled(case, acc, 2002)
+    # BN output at the sampled positions: fmaf(k_c, acc, b_c) of the oracle's accumulator
+    co = (idx // (h * w)) % 128
+    ok, ob = oracle.bn_fold({kk: (v.numpy() if hasattr(v, "numpy") else v) for kk, v in case.bn.items()})
+    zw = oracle.epi_bn(want.reshape(1, -1, 1, 1), ok[co], ob[co]).reshape(-1)
+    got = z.reshape(-1)[torch.from_numpy(idx).to(dev)].cpu().numpy()
+    np.testing.assert_array_equal(got, zw)
+    # property at full size: every BN output equals fmaf(k_c, acc, b_c) of the int32 output
+    zz = torch.addcmul(bd.view(1, -1, 1, 1).double(), kd.view(1, -1, 1, 1).double(), acc.double()).float()
+    assert torch.equal(z, zz)
+    # activations bounded by the receptive field
+    assert int(acc.abs().max()) <= c * 9
+
+
+@pytest.mark.parametrize("layer", [0, 1, 2, 3])
+def test_workload5_full_sampled(dev, layer):
+    """3W3A ResNet-18 3x3 layers at batch 256: int32 accumulators (16 x the real dot)."""
+    case = synth.workload5(layer)
+    n, c, h, w = case.x.shape
+    act = q.pack_act(case.x.to(dev), 3)
+    wq, _ = q.pack_weight(case.w.to(dev), 3)
+    acc, _ = q.conv(act, wq, n, c, h, w, c, 3, 1, 1, 3, 3)
+    torch.cuda.synchronize()
+    _check_sampled(case, acc, 5000 + layer, 2048)
+    assert int(acc.abs().max()) <= c * 9 * 16
+
+
+# ---------------------------------------------------------------------------
+# networks
+# ---------------------------------------------------------------------------
+
+def _levels_of(words, shape, bits):
+    n, c, h, w = shape
+    return unpack_act(words.cpu().numpy(), n, c, h, w, bits)
+
+
+def test_convnet_layers_and_logits(dev):
+    """ConvNet (Model A widths), batch 4: every binary layer's packed output and the
+    logits equal the oracle's."""
+    from paper_2003_04296_amd.nets import build_convnet
+
+    p = synth.convnet_params(seed=1003, batch=4)
+    net = build_convnet(p, dev)
+    logits = net.forward(p["x"].to(dev))
+    torch.cuda.synchronize()
+    want, levels = oracle.convnet_forward(p, return_levels=True)
+    names = ["conv1", "conv2", "conv3", "conv4", "conv5", "conv6", "fc1", "fc2"]
+    for name, lv in zip(names, levels):
+        tid = net.ids[name]
+        words, bits = net.tensor(tid, 4)
+        shape = lv.shape if lv.ndim == 4 else (lv.shape[0], lv.shape[1], 1, 1)
+        np.testing.assert_array_equal(_levels_of(words, shape, bits).reshape(lv.shape), lv, err_msg=name)
+    np.testing.assert_array_equal(logits.cpu().numpy(), want)
+
+
+def test_convnet_full_batch_rows(dev):
+    """Batch 256 on the GPU; images are independent, so oracle rows 0, 137, 255 must match."""
+    from paper_2003_04296_amd.nets import build_convnet
+
+    p = synth.convnet_params(seed=1003, batch=256)
+    net = build_convnet(p, dev)
+    logits = net.forward(p["x"].to(dev)).cpu().numpy()
+    rows = [0, 137, 255]
+    sub = dict(p)
+    sub["x"] = p["x"][rows]
+    want = oracle.convnet_forward(sub)
+    np.testing.assert_array_equal(logits[rows], want)
+    np.testing.assert_allclose(logits[rows], want, rtol=1e-3, atol=1e-3)
+
+
+def test_resnet18_blocks_and_logits(dev):
+    """ResNet-18 2W2A at 224x224, batch 2: the fp32 residual stream after the stem
+    and every block, and the logits, equal the oracle's."""
+    from paper_2003_04296_amd.nets import build_resnet18
+
+    p = synth.resnet18_params(seed=1004, batch=2)
+    net = build_resnet18(p, dev)
+    logits = net.forward(p["x"].to(dev))
+    torch.cuda.synchronize()
+    want, acts = oracle.resnet18_forward(p, 2, 2, return_acts=True)
+    got_stem, _ = net.tensor(net.ids["stem"], 2)
+    np.testing.assert_array_equal(got_stem.cpu().numpy(), acts[0])
+    for i in range(8):
+        if net.ids[f"block{i}"] == net.ids["logits"]:
+            continue
+        got, _ = net.tensor(net.ids[f"block{i}"], 2)
+        np.testing.assert_array_equal(got.cpu().numpy(), acts[i + 1], err_msg=f"block{i}")
+    np.testing.assert_array_equal(logits.cpu().numpy(), want)
+
+
+def test_resnet18_full_batch_rows(dev):
+    from paper_2003_04296_amd.nets import build_resnet18
+
+    p = synth.resnet18_params(seed=1004, batch=64)
+    net = build_resnet18(p, dev)
+    logits = net.forward(p["x"].to(dev)).cpu().numpy()
+    rows = [0, 63]
+    sub = dict(p)
+    sub["x"] = p["x"][rows]
+    want = oracle.resnet18_forward(sub, 2, 2)
+    np.testing.assert_array_equal(logits[rows], want)
