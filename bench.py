@@ -109,6 +109,25 @@ class ConvWorkload:
         return n * c * h * w * 4 + q.packed_act_words(n, c, h, w, self.case.a_bits) * 4
 
 
+def measured_traffic(kernel: str):
+    """HBM bytes per launch from the committed rocprofv3 counter runs, or None
+    when the kernel's sources changed since the counters were taken."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path)).get(kernel)
+    if not rec:
+        return None
+    h = hashlib.sha256()
+    for src in rec["sources"]:
+        h.update(open(os.path.join(ROOT, src), "rb").read())
+    if h.hexdigest() != rec["sources_sha256"]:
+        return None
+    return rec["fetch_bytes"] + rec["write_bytes"]
+
+
 def time_kernel(fn, reps, stream):
     """Average duration of fn's launches with HIP events on the launch stream."""
     start = torch.cuda.Event(enable_timing=True)
@@ -179,6 +198,8 @@ def main():
     ap.add_argument("--workload", default="1w2a")
     ap.add_argument("--algo", default="auto", choices=["auto", "bitplane", "mfma"])
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--copy-ref-mib", type=int, default=0,
+                    help="after timing, run one device copy of this many MiB (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -216,6 +237,8 @@ def main():
         gops_step = 2.0 * W.macs / dt / 1e9
         gops_conv = 2.0 * W.macs / t_conv / 1e9
         peak = valu_peak_gops(case.a_bits, case.w_bits)
+        kname = f"conv_bitplane_kernel<{q.planes(case.a_bits)}, {q.planes(case.w_bits)}, " \
+                f"{32 if max(case.a_bits, case.w_bits) < 3 else (8 if case.a_bits == case.w_bits else 16)}, false>"
         n, c, h, w = W.shape
         out.update({
             "value": round(gops_step, 1), "unit": "GOPS", "ms_per_step": round(dt * 1e3, 4),
@@ -227,7 +250,8 @@ def main():
                        "algo": args.algo, "weights": "packed once before timing"},
             "roofline": {"bound": "alu", "kernel": "qconv_forward (bitplane)", "achieved": round(gops_conv, 1),
                          "peak": round(peak, 1) if peak else None, "unit": "GOPS",
-                         "frac": round(gops_conv / peak, 4) if peak else None, "traffic": None,
+                         "frac": round(gops_conv / peak, 4) if peak else None,
+                         "traffic": measured_traffic(kname), "traffic_unit": "bytes per launch (HBM)",
                          "avg_us": round(t_conv * 1e6, 2),
                          "hbm_gbs_algorithmic": round(W.conv_bytes() / t_conv / 1e9, 1)},
             "pack_act": {"avg_us": round(t_pack * 1e6, 2), "achieved_gbs": round(W.pack_bytes() / t_pack / 1e9, 1),
@@ -266,6 +290,13 @@ def main():
     else:
         print(f"unknown workload {wl}", file=sys.stderr)
         sys.exit(2)
+    if args.copy_ref_mib:
+        src = torch.empty(args.copy_ref_mib * (1 << 20) // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        out["copy_ref_bytes"] = src.numel() * 4
     print(json.dumps(out), flush=True)
 
 

@@ -18,6 +18,8 @@
 // (L1/L2 cached; neighbouring taps and channel tiles re-read the same lines).
 // The epilogue ({QConv-pool-BN-HardTanh} / {QConv-BN-HardTanh}, Sec. III-E)
 // runs in registers before the only store.
+#include <type_traits>
+
 #include "qconv_internal.h"
 
 namespace qc {
@@ -216,12 +218,19 @@ __global__ __launch_bounds__(256) void conv_bitplane_kernel(const ConvArgs a) {
     if constexpr (TN == 32) {
       uint32_t* dst = a.out_packed + wbase_o * pout;
       for (int p = 0; p < pout; ++p) dst[p] = ow_words[p];
-    } else if constexpr (TN == 16) {
-      uint16_t* dst = reinterpret_cast<uint16_t*>(a.out_packed + wbase_o * pout) + ((co0 & 31) >> 4);
-      for (int p = 0; p < pout; ++p) dst[2 * p] = (uint16_t)ow_words[p];
     } else {
-      uint8_t* dst = reinterpret_cast<uint8_t*>(a.out_packed + wbase_o * pout) + ((co0 & 31) >> 3);
-      for (int p = 0; p < pout; ++p) dst[4 * p] = (uint8_t)ow_words[p];
+      // Sub-word store of this tile's TN channels.  The tile holding the last
+      // channel also clears the rest of that word (no tile covers those
+      // channels, and bits past the last channel must read 0).
+      constexpr int SUBS = 32 / TN;
+      const int sub = (co0 & 31) / TN;
+      const int last_sub = (co0 + TN >= a.cout) ? SUBS - 1 : sub;
+      using sub_t = typename std::conditional<TN == 16, uint16_t, uint8_t>::type;
+      sub_t* dst = reinterpret_cast<sub_t*>(a.out_packed + wbase_o * pout);
+      for (int p = 0; p < pout; ++p) {
+        dst[SUBS * p + sub] = (sub_t)ow_words[p];
+        for (int s2 = sub + 1; s2 <= last_sub; ++s2) dst[SUBS * p + s2] = (sub_t)0;
+      }
     }
   }
 }
