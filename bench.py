@@ -36,7 +36,8 @@ METRIC = "quantized-conv GOPS (1W1A, 2W2A, 3W3A) + images/sec fwd; % of roofline
 # MI355X figures: 256 CUs x 64 lanes x 2.4 GHz of 32-bit VALU issue.
 VALU_LANE_OPS = 256 * 64 * 2.4e9
 HBM_PEAK_GBS = 8000.0
-MFMA_I8_PEAK_TOPS = 5000.0
+# dense matrix-core peaks (ops = 2 per MAC), in G: int8 5.0 POP/s, fp4 10.1 PFLOP/s
+MFMA_PEAK_GOPS = {"mfma_i8": 5.0e6, "mfma_fp4": 10.1e6}
 # Minimal VALU recipe (lane-ops per 32-channel word pair) of the bitplane
 # product on gfx950, where v_bitop3_b32 fuses any 3-input bit function:
 #   1W1A: xor, bcnt                         -> 2
@@ -196,7 +197,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="1w2a")
-    ap.add_argument("--algo", default="auto", choices=["auto", "bitplane", "mfma"])
+    ap.add_argument("--algo", default="auto", choices=["auto", "bitplane", "mfma_i8", "mfma_fp4"])
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--copy-ref-mib", type=int, default=0,
                     help="after timing, run one device copy of this many MiB (HBM counter calibration)")
@@ -211,7 +212,8 @@ def main():
         sys.exit(2)
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
-    algo = {"auto": q.ALGO_AUTO, "bitplane": q.ALGO_BITPLANE, "mfma": q.ALGO_MFMA_I8}[args.algo]
+    algo = {"auto": q.ALGO_AUTO, "bitplane": q.ALGO_BITPLANE, "mfma_i8": q.ALGO_MFMA_I8,
+            "mfma_fp4": q.ALGO_MFMA_FP4}[args.algo]
     wl = args.workload
     out = {"metric": METRIC, "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "higher_is_better": True,
            "scaling": "weak", "vs_baseline": None, "data": "synthetic"}
@@ -236,9 +238,20 @@ def main():
         t_pack = time_kernel(W.pack, args.steps, stream)
         gops_step = 2.0 * W.macs / dt / 1e9
         gops_conv = 2.0 * W.macs / t_conv / 1e9
-        peak = valu_peak_gops(case.a_bits, case.w_bits)
-        kname = f"conv_bitplane_kernel<{q.planes(case.a_bits)}, {q.planes(case.w_bits)}, " \
-                f"{32 if max(case.a_bits, case.w_bits) < 3 else (8 if case.a_bits == case.w_bits else 16)}, false>"
+        n, c, h, w = W.shape
+        used = q.ALGO_NAMES[q.resolve_algo(n, c, h, w, W.cout, W.k, case.stride, case.pad, case.a_bits,
+                                           case.w_bits, mode, 0, 0, algo)]
+        if used == "bitplane":
+            peak, cbound = valu_peak_gops(case.a_bits, case.w_bits), "alu"
+            kname = f"conv_bitplane_kernel<{q.planes(case.a_bits)}, {q.planes(case.w_bits)}, " \
+                    f"{32 if max(case.a_bits, case.w_bits) < 3 else (8 if case.a_bits == case.w_bits else 16)}, false>"
+        else:
+            peak, cbound = MFMA_PEAK_GOPS[used], "mfma"
+            kname = f"conv_mfma_kernel<{1 if used == 'mfma_fp4' else 0}, {q.planes(case.a_bits)}, " \
+                    f"{2 if W.cout > 64 else 1}>"
+        hbm_gbs = W.conv_bytes() / t_conv / 1e9
+        frac_c = gops_conv / peak if peak else 0.0
+        frac_h = hbm_gbs / HBM_PEAK_GBS
         n, c, h, w = W.shape
         out.update({
             "value": round(gops_step, 1), "unit": "GOPS", "ms_per_step": round(dt * 1e3, 4),
@@ -247,13 +260,21 @@ def main():
                        "a_bits": case.a_bits, "w_bits": case.w_bits,
                        "epilogue": {q.EPI_INT32: "int32", q.EPI_SCALE_F32: "scale_f32",
                                     q.EPI_BN_F32: "bn_f32"}[mode],
-                       "algo": args.algo, "weights": "packed once before timing"},
-            "roofline": {"bound": "alu", "kernel": "qconv_forward (bitplane)", "achieved": round(gops_conv, 1),
-                         "peak": round(peak, 1) if peak else None, "unit": "GOPS",
-                         "frac": round(gops_conv / peak, 4) if peak else None,
-                         "traffic": measured_traffic(kname), "traffic_unit": "bytes per launch (HBM)",
-                         "avg_us": round(t_conv * 1e6, 2),
-                         "hbm_gbs_algorithmic": round(W.conv_bytes() / t_conv / 1e9, 1)},
+                       "algo": used, "weights": "packed once before timing"},
+            "roofline": ({"bound": "hbm", "kernel": kname, "achieved": round(hbm_gbs, 1), "peak": HBM_PEAK_GBS,
+                          "unit": "GB/s", "frac": round(frac_h, 4),
+                          "compute": {"bound": cbound, "achieved_gops": round(gops_conv, 1),
+                                      "peak_gops": round(peak, 1), "frac": round(frac_c, 4)}}
+                         if frac_h > frac_c else
+                         {"bound": cbound, "kernel": kname, "achieved": round(gops_conv, 1),
+                          "peak": round(peak, 1), "unit": "GOPS", "frac": round(frac_c, 4),
+                          "hbm": {"achieved_gbs": round(hbm_gbs, 1), "peak_gbs": HBM_PEAK_GBS,
+                                  "frac": round(frac_h, 4)}}),
+        })
+        out["roofline"].update({
+            "traffic": measured_traffic(kname), "traffic_unit": "HBM bytes per launch",
+            "algorithmic_bytes": W.conv_bytes(), "avg_us": round(t_conv * 1e6, 2)})
+        out.update({
             "pack_act": {"avg_us": round(t_pack * 1e6, 2), "achieved_gbs": round(W.pack_bytes() / t_pack / 1e9, 1),
                          "peak_gbs": HBM_PEAK_GBS},
         })

@@ -48,8 +48,14 @@
  *   3 bits : plane 1 = |level| == 1, plane 2 = |level| == 1/2,
  *            plane 3 = |level| == 1/4.
  *   activations: [n][h][w][cw][P],              cw = ceil(c / 32)
- *   weights    : [kh][kw][cw][cout_pad][P],     cout_pad = ceil(cout / 64) * 64
- *                (rows of padding channels are 0).
+ *   weights    : [kh][kw][cw][cout_pad][P],     cout_pad = ceil(cout / 128) * 128
+ *                (rows of padding channels are 0), followed in the same
+ *                buffer by two matrix-core operand copies of the same levels,
+ *                expanded from those bitplanes (channels past cin are 0):
+ *                int8 codes [kh][kw][cw][cout_pad][32 B] and E2M1 (fp4)
+ *                codes [kh][kw][ceil(cw/2)][cout_pad][32 B] (64 channels,
+ *                two per byte, low nibble first; the codes 0, +-1, +-2, +-4
+ *                are exact in both formats).
  *   An all-zero activation word reads as level -1 for 1 bit and 0 for 2/3
  *   bits, i.e. Q(0): the value padding taps take in the product.
  */
@@ -108,7 +114,8 @@ size_t qconv_packed_act_bytes(int n, int c, int h, int w, int bits);
 int qconv_pack_act(const float* x, int n, int c, int h, int w, int bits,
                    const float* thresholds, uint32_t* out_packed, void* stream);
 
-/* Bytes of the packed weight tensor [kh][kw][ceil(cin/32)][cout_pad][P]. */
+/* Bytes of the packed weight buffer: the bitplanes [kh][kw][ceil(cin/32)][cout_pad][P]
+ * plus the int8 and fp4 operand copies described above. */
 size_t qconv_packed_weight_bytes(int cout, int cin, int kh, int kw, int bits);
 
 /* Quantize fp32 OIHW weights w[cout][cin][kh][kw] (Eq. 20) and pack them.
@@ -128,9 +135,10 @@ int qconv_fold_bn(const float* gamma, const float* beta, const float* mean, cons
 /* Quantized convolution with fused epilogue (Algorithm 1 + Sec. III-E)      */
 /* ------------------------------------------------------------------------ */
 typedef enum {
-  QCONV_ALGO_AUTO = 0,     /* library choice                                  */
+  QCONV_ALGO_AUTO = 0,     /* library choice (matrix cores where supported)   */
   QCONV_ALGO_BITPLANE = 1, /* VALU XNOR/AND + popcount over bitplanes         */
-  QCONV_ALGO_MFMA_I8 = 2   /* int8 matrix cores on the unpacked level codes   */
+  QCONV_ALGO_MFMA_I8 = 2,  /* int8 matrix cores on the expanded level codes   */
+  QCONV_ALGO_MFMA_FP4 = 3  /* fp4 (E2M1) matrix cores on the same codes        */
 } qconv_algo;
 
 typedef struct {
@@ -173,9 +181,18 @@ int qconv_out_size(int in, int k, int stride, int pad);
  * ho'/wo' after pooling) is written in BN_PACK mode and, when non-NULL, in
  * BN_F32 mode (quantizing the fp32 result).  Requires ceil(cout/32)*32
  * channels of room in out_packed's last word, K = cin*kh*kw with
- * K * max|a| * max|w| < 2^31. */
+ * K * max|a| * max|w| < 2^31.  The matrix-core algorithms support stride 1
+ * or 2 without pooling and an input tile that fits their staging buffer;
+ * asked for explicitly otherwise they return QCONV_EUNSUPPORTED, and AUTO
+ * falls back to the bitplane kernels.  Every algorithm returns the same
+ * bits. */
 int qconv_forward(const qconv_desc* d, const uint32_t* act_packed, const uint32_t* w_packed,
                   const qconv_epilogue* epi, void* out, uint32_t* out_packed, void* stream);
+
+/* The concrete algorithm (QCONV_ALGO_BITPLANE / _MFMA_I8 / _MFMA_FP4) that
+ * qconv_forward would run for d and epi (d->algo may be AUTO), or a negative
+ * status if the call would be rejected.  Launches nothing. */
+int qconv_resolve_algo(const qconv_desc* d, const qconv_epilogue* epi);
 
 /* ------------------------------------------------------------------------ */
 /* Whole networks (Algorithm 1, inference branch, layer by layer)            */

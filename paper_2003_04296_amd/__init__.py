@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libqconv.so")
 
 QCONV_OK, QCONV_EINVAL, QCONV_EUNSUPPORTED, QCONV_EWORKSPACE, QCONV_EOVERFLOW, QCONV_EHIP = 0, -1, -2, -3, -4, -5
-ALGO_AUTO, ALGO_BITPLANE, ALGO_MFMA_I8 = 0, 1, 2
+ALGO_AUTO, ALGO_BITPLANE, ALGO_MFMA_I8, ALGO_MFMA_FP4 = 0, 1, 2, 3
 EPI_INT32, EPI_SCALE_F32, EPI_BN_F32, EPI_BN_PACK = 0, 1, 2, 3
 EPI_POOL2, EPI_RESIDUAL = 1, 2
 OP_NAMES = {1: "XNOR", 2: "SHIFT", 3: "XNOR-ADDER", 4: "SHIFT-ADDER", 5: "MAC"}
@@ -24,7 +24,7 @@ EXPORTED = (
     "qconv_pack_act", "qconv_packed_weight_bytes", "qconv_pack_weight", "qconv_fold_bn",
     "qconv_out_size", "qconv_forward", "qnet_create", "qnet_destroy", "qnet_add_conv_f32",
     "qnet_add_maxpool_f32", "qnet_add_quantize", "qnet_add_qconv", "qnet_add_avgpool",
-    "qnet_add_fc_f32", "qnet_workspace_bytes", "qnet_forward", "qnet_tensor_info",
+    "qnet_add_fc_f32", "qnet_workspace_bytes", "qnet_forward", "qnet_tensor_info", "qconv_resolve_algo",
 )
 
 
@@ -76,6 +76,7 @@ def lib() -> ctypes.CDLL:
     L.qconv_fold_bn.argtypes = [vp, vp, vp, vp, ctypes.c_double, i32, vp, vp]
     L.qconv_out_size.argtypes = [i32] * 4
     L.qconv_forward.argtypes = [ctypes.POINTER(qconv_desc), vp, vp, ctypes.POINTER(qconv_epilogue), vp, vp, vp]
+    L.qconv_resolve_algo.argtypes = [ctypes.POINTER(qconv_desc), ctypes.POINTER(qconv_epilogue)]
     L.qnet_create.restype = vp
     L.qnet_create.argtypes = [i32, i32, i32]
     L.qnet_destroy.argtypes = [vp]
@@ -200,6 +201,17 @@ def conv(act_packed, w_packed, n, cin, h, w, cout, k, stride, pad, a_bits, w_bit
     _check(lib().qconv_forward(ctypes.byref(d), _ptr(act_packed), _ptr(w_packed), ctypes.byref(e), _ptr(out),
                                _ptr(out_packed), _stream(stream)), "qconv_forward")
     return out, out_packed
+
+
+ALGO_NAMES = {ALGO_BITPLANE: "bitplane", ALGO_MFMA_I8: "mfma_i8", ALGO_MFMA_FP4: "mfma_fp4"}
+
+
+def resolve_algo(n, cin, h, w, cout, k, stride, pad, a_bits, w_bits, mode=EPI_INT32, flags=0, out_bits=0,
+                 algo=ALGO_AUTO) -> int:
+    """The concrete algorithm qconv_forward would run (launches nothing)."""
+    d = qconv_desc(n, cin, h, w, cout, k, k, stride, pad, a_bits, w_bits, algo)
+    e = qconv_epilogue(mode, flags, None, None, None, None, out_bits, None)
+    return _check(lib().qconv_resolve_algo(ctypes.byref(d), ctypes.byref(e)), "qconv_resolve_algo")
 
 
 class Net:

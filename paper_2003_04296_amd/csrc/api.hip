@@ -97,7 +97,8 @@ int qconv_pack_act(const float* x, int n, int c, int h, int w, int bits, const f
 
 size_t qconv_packed_weight_bytes(int cout, int cin, int kh, int kw, int bits) {
   if (cout < 1 || cin < 1 || kh < 1 || kw < 1 || !bits_ok(bits)) return 0;
-  return (size_t)kh * kw * ceil_div(cin, 32) * cout_pad(cout) * planes_of(bits) * sizeof(uint32_t);
+  return wbytes_planes(cout, cin, kh, kw, bits) + wbytes_i8(cout, cin, kh, kw) +
+         wbytes_fp4(cout, cin, kh, kw);
 }
 
 int qconv_pack_weight(const float* w, int cout, int cin, int kh, int kw, int bits,
@@ -133,13 +134,20 @@ int qconv_out_size(int in, int k, int stride, int pad) {
   return (in + 2 * pad - k) < 0 ? QCONV_EINVAL : o;
 }
 
-int qconv_forward(const qconv_desc* d, const uint32_t* act_packed, const uint32_t* w_packed,
-                  const qconv_epilogue* epi, void* out, uint32_t* out_packed, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Validates a qconv_forward call and fills the kernel arguments; returns the
+// concrete algorithm to run (> 0) or a negative status.
+int prepare_conv(const qconv_desc* d, const uint32_t* act_packed, const uint32_t* w_packed,
+                 const qconv_epilogue* epi, void* out, uint32_t* out_packed, bool check_ptrs,
+                 ConvArgs* args) {
   if (!d || !epi) return QCONV_EINVAL;
   if (d->n < 0 || d->cin < 1 || d->h < 1 || d->w < 1 || d->cout < 1 || d->kh < 1 || d->kw < 1 ||
       d->stride < 1 || d->pad < 0 || !bits_ok(d->a_bits) || !bits_ok(d->w_bits))
     return QCONV_EINVAL;
-  if (d->algo < QCONV_ALGO_AUTO || d->algo > QCONV_ALGO_MFMA_I8) return QCONV_EINVAL;
+  if (d->algo < QCONV_ALGO_AUTO || d->algo > QCONV_ALGO_MFMA_FP4) return QCONV_EINVAL;
   const int ho = qconv_out_size(d->h, d->kh, d->stride, d->pad);
   const int wo = qconv_out_size(d->w, d->kw, d->stride, d->pad);
   if (ho < 1 || wo < 1) return QCONV_EINVAL;
@@ -150,17 +158,20 @@ int qconv_forward(const qconv_desc* d, const uint32_t* act_packed, const uint32_
   const bool pool = (epi->flags & QCONV_EPI_POOL2) != 0;
   const bool resid = (epi->flags & QCONV_EPI_RESIDUAL) != 0;
   if (pool && (ho < 2 || wo < 2)) return QCONV_EINVAL;
-  if (resid && (epi->mode != QCONV_EPI_BN_F32 || !epi->residual)) return QCONV_EINVAL;
-  if (epi->mode == QCONV_EPI_SCALE_F32 && !epi->scale) return QCONV_EINVAL;
-  if ((epi->mode == QCONV_EPI_BN_F32 || epi->mode == QCONV_EPI_BN_PACK) && (!epi->bn_k || !epi->bn_b))
-    return QCONV_EINVAL;
+  if (resid && epi->mode != QCONV_EPI_BN_F32) return QCONV_EINVAL;
+  if (check_ptrs) {
+    if (resid && !epi->residual) return QCONV_EINVAL;
+    if (epi->mode == QCONV_EPI_SCALE_F32 && !epi->scale) return QCONV_EINVAL;
+    if ((epi->mode == QCONV_EPI_BN_F32 || epi->mode == QCONV_EPI_BN_PACK) && (!epi->bn_k || !epi->bn_b))
+      return QCONV_EINVAL;
+  }
   const bool pack = epi->mode == QCONV_EPI_BN_PACK || (epi->mode == QCONV_EPI_BN_F32 && out_packed);
-  if (epi->mode == QCONV_EPI_BN_PACK && !out_packed) return QCONV_EINVAL;
-  if (epi->mode != QCONV_EPI_BN_PACK && !out && d->n > 0) return QCONV_EINVAL;
+  if (check_ptrs && epi->mode == QCONV_EPI_BN_PACK && !out_packed) return QCONV_EINVAL;
+  if (check_ptrs && epi->mode != QCONV_EPI_BN_PACK && !out && d->n > 0) return QCONV_EINVAL;
   if (pack && !bits_ok(epi->out_bits)) return QCONV_EINVAL;
-  if (d->n > 0 && (!act_packed || !w_packed)) return QCONV_EINVAL;
+  if (check_ptrs && d->n > 0 && (!act_packed || !w_packed)) return QCONV_EINVAL;
 
-  ConvArgs a;
+  ConvArgs& a = *args;
   memset(&a, 0, sizeof(a));
   a.act = act_packed;
   a.wt = w_packed;
@@ -197,14 +208,42 @@ int qconv_forward(const qconv_desc* d, const uint32_t* act_packed, const uint32_
     const int rc = act_thresholds(epi->out_bits, epi->out_thresholds, &a.othr);
     if (rc) return rc;
   }
+  a.cin = d->cin;
+  {
+    const uint8_t* wb = reinterpret_cast<const uint8_t*>(w_packed);
+    a.w_i8 = wb ? wb + wbytes_planes(d->cout, d->cin, d->kh, d->kw, d->w_bits) : nullptr;
+    a.w_fp4 = wb ? a.w_i8 + wbytes_i8(d->cout, d->cin, d->kh, d->kw) : nullptr;
+  }
+  if (d->algo == QCONV_ALGO_MFMA_I8 || d->algo == QCONV_ALGO_MFMA_FP4) {
+    a.mfma_fp4 = d->algo == QCONV_ALGO_MFMA_FP4 ? 1 : 0;
+    if (d->n > 0 && !mfma_supports(a)) return QCONV_EUNSUPPORTED;
+    return d->algo;
+  }
+  if (d->algo == QCONV_ALGO_AUTO && d->n > 0) {
+    a.mfma_fp4 = 1;
+    if (mfma_supports(a)) return QCONV_ALGO_MFMA_FP4;
+  }
+  return QCONV_ALGO_BITPLANE;
+}
+
+}  // namespace
+
+extern "C" {
+
+int qconv_resolve_algo(const qconv_desc* d, const qconv_epilogue* epi) {
+  ConvArgs a;
+  return prepare_conv(d, nullptr, nullptr, epi, nullptr, nullptr, false, &a);
+}
+
+int qconv_forward(const qconv_desc* d, const uint32_t* act_packed, const uint32_t* w_packed,
+                  const qconv_epilogue* epi, void* out, uint32_t* out_packed, void* stream) {
+  ConvArgs a;
+  const int algo = prepare_conv(d, act_packed, w_packed, epi, out, out_packed, true, &a);
+  if (algo < 0) return algo;
   if (d->n == 0) return QCONV_OK;
   hipStream_t s = (hipStream_t)stream;
-  if (d->algo == QCONV_ALGO_MFMA_I8) {
-    if (!mfma_supports(a)) return QCONV_EUNSUPPORTED;
-    return launch_conv_mfma(a, s);
-  }
-  if (d->algo == QCONV_ALGO_AUTO && mfma_supports(a)) return launch_conv_mfma(a, s);
-  return launch_conv_bitplane(a, s);
+  if (algo == QCONV_ALGO_BITPLANE) return launch_conv_bitplane(a, s);
+  return launch_conv_mfma(a, s);
 }
 
 // ---------------------------------------------------------------------------

@@ -102,6 +102,63 @@ __global__ __launch_bounds__(256) void pack_weight_kernel(const float* __restric
   for (int p = 0; p < P; ++p) dst[p] = word[p];
 }
 
+// Matrix-core operand copies of packed weights: one thread per
+// (tap, word, output channel) for int8 (32 bytes), per (tap, word pair,
+// output channel) for fp4 (32 bytes = 64 nibbles).
+template <int P>
+__global__ __launch_bounds__(256) void expand_weight_kernel(const uint32_t* __restrict__ planes,
+                                                            int taps, int cwn, int cop, int cin,
+                                                            uint8_t* __restrict__ w_i8,
+                                                            uint8_t* __restrict__ w_fp4) {
+  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int cwp = (cwn + 1) / 2;
+  const int64_t n_i8 = (int64_t)taps * cwn * cop;
+  const int64_t n_fp4 = (int64_t)taps * cwp * cop;
+  if (tid < n_i8) {
+    const int co = (int)(tid % cop);
+    const int64_t r = tid / cop;
+    const int cw = (int)(r % cwn);
+    const int tap = (int)(r / cwn);
+    const uint32_t* src = planes + (((int64_t)tap * cwn + cw) * cop + co) * P;
+    const int nvalid = min(32, cin - cw * 32);
+    const uint32_t valid = nvalid >= 32 ? 0xFFFFFFFFu : ((1u << nvalid) - 1u);
+    uint32_t pl[P];
+#pragma unroll
+    for (int p = 0; p < P; ++p) pl[p] = src[p];
+    uint32_t o[8];
+    expand_i8_word<P>(pl, valid, o);
+    uint4* dst = reinterpret_cast<uint4*>(w_i8 + tid * 32);
+    dst[0] = make_uint4(o[0], o[1], o[2], o[3]);
+    dst[1] = make_uint4(o[4], o[5], o[6], o[7]);
+  } else if (tid < n_i8 + n_fp4) {
+    const int64_t u = tid - n_i8;
+    const int co = (int)(u % cop);
+    const int64_t r = u / cop;
+    const int kp = (int)(r % cwp);
+    const int tap = (int)(r / cwp);
+    uint32_t o[8];
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      const int cw = 2 * kp + half;
+      uint32_t pl[P];
+      uint32_t valid = 0u;
+#pragma unroll
+      for (int p = 0; p < P; ++p) pl[p] = 0u;
+      if (cw < cwn) {
+        const uint32_t* src = planes + (((int64_t)tap * cwn + cw) * cop + co) * P;
+#pragma unroll
+        for (int p = 0; p < P; ++p) pl[p] = src[p];
+        const int nvalid = min(32, cin - cw * 32);
+        valid = nvalid >= 32 ? 0xFFFFFFFFu : ((1u << nvalid) - 1u);
+      }
+      expand_fp4_word<P>(pl, valid, o + 4 * half);
+    }
+    uint4* dst = reinterpret_cast<uint4*>(w_fp4 + u * 32);
+    dst[0] = make_uint4(o[0], o[1], o[2], o[3]);
+    dst[1] = make_uint4(o[4], o[5], o[6], o[7]);
+  }
+}
+
 }  // namespace
 
 int launch_pack_act(const float* x, int n, int c, int h, int w, int bits, Thr t, uint32_t* out,
@@ -132,6 +189,16 @@ int launch_pack_weight(const float* w, int cout, int cin, int kh, int kw, int bi
     case 1: pack_weight_kernel<1><<<grid, 256, 0, s>>>(w, cout, cin, kh, kw, cwn, cop, b, scale, out); break;
     case 2: pack_weight_kernel<2><<<grid, 256, 0, s>>>(w, cout, cin, kh, kw, cwn, cop, b, scale, out); break;
     default: pack_weight_kernel<3><<<grid, 256, 0, s>>>(w, cout, cin, kh, kw, cwn, cop, b, scale, out); break;
+  }
+  uint8_t* w_i8 = reinterpret_cast<uint8_t*>(out) + wbytes_planes(cout, cin, kh, kw, bits);
+  uint8_t* w_fp4 = w_i8 + wbytes_i8(cout, cin, kh, kw);
+  const int taps = kh * kw;
+  const int64_t items = (int64_t)taps * cwn * cop + (int64_t)taps * ((cwn + 1) / 2) * cop;
+  const dim3 g2((unsigned)((items + 255) / 256));
+  switch (bits) {
+    case 1: expand_weight_kernel<1><<<g2, 256, 0, s>>>(out, taps, cwn, cop, cin, w_i8, w_fp4); break;
+    case 2: expand_weight_kernel<2><<<g2, 256, 0, s>>>(out, taps, cwn, cop, cin, w_i8, w_fp4); break;
+    default: expand_weight_kernel<4><<<g2, 256, 0, s>>>(out, taps, cwn, cop, cin, w_i8, w_fp4); break;
   }
   return hip_status();
 }

@@ -50,7 +50,86 @@ __device__ __forceinline__ float hardtanh(float v) {
 }
 
 __host__ __device__ inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
-inline int cout_pad(int cout) { return ceil_div(cout, 64) * 64; }
+inline int cout_pad(int cout) { return ceil_div(cout, 128) * 128; }
+
+// ---------------------------------------------------------------------------
+// Bitplanes -> matrix-core operands.  One 32-channel word of `P` planes is
+// turned into the level codes of its channels.  `valid` marks the channels
+// that exist (bits past cin give 0; only needed for 1-bit operands, whose
+// sign plane alone cannot express 0).
+// ---------------------------------------------------------------------------
+
+// Nibble -> one bit per byte: bit j of `nib` (j < 4) lands in bit 0 of byte j.
+// The four shifted copies of the nibble (offsets 0, 7, 14, 21) never overlap,
+// so the product has no carries.
+__device__ __forceinline__ uint32_t spread4(uint32_t nib) {
+  return __umul24(nib, 0x00204081u) & 0x01010101u;
+}
+
+// int8 codes of channels [4q, 4q+4) as 4 bytes, by a byte lookup (v_perm_b32)
+// with index = S + 2*M for 1/2-bit operands (M = nonzero mask) and
+// index = B0 + 2*B1 + 4*S for 3-bit ones (B0 = |l| in {1,4}, B1 = |l| in {2,4}).
+template <int P>
+__device__ __forceinline__ void expand_i8_word(const uint32_t* pl, uint32_t valid, uint32_t out[8]) {
+  if constexpr (P <= 2) {
+    const uint32_t S = pl[0];
+    const uint32_t M = (P == 1) ? valid : pl[1];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const uint32_t idx = spread4((S >> (4 * q)) & 0xFu) | (spread4((M >> (4 * q)) & 0xFu) << 1);
+      // idx 0/1 -> 0, 2 -> -1, 3 -> +1
+      out[q] = __builtin_amdgcn_perm(0u, 0x01FF0000u, idx);
+    }
+  } else {
+    const uint32_t S = pl[0], E1 = pl[1], E2 = pl[2], E3 = pl[3];
+    const uint32_t B0 = E1 | E3, B1 = E1 | E2;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const uint32_t idx = spread4((B0 >> (4 * q)) & 0xFu) | (spread4((B1 >> (4 * q)) & 0xFu) << 1) |
+                           (spread4((S >> (4 * q)) & 0xFu) << 2);
+      // idx 0..3 -> 0, -1, -2, -4 ; idx 4..7 -> 0, +1, +2, +4
+      out[q] = __builtin_amdgcn_perm(0x04020100u, 0xFCFEFF00u, idx);
+    }
+  }
+}
+
+// Byte -> eight nibble slots: channel i of the byte goes to nibble 2i (i < 4)
+// or nibble 2(i-4)+1 (i >= 4).  Any fixed channel order works for the
+// product as long as both operands use it; this one costs two spreads.
+__device__ __forceinline__ uint32_t spread8(uint32_t b) {
+  return spread4(b & 0xFu) | (spread4((b >> 4) & 0xFu) << 4);
+}
+
+// E2M1 (fp4) codes of 32 channels as 4 words: +1 = 0x2, +2 = 0x4, +4 = 0x6,
+// sign bit 0x8, zero = 0x0.
+template <int P>
+__device__ __forceinline__ void expand_fp4_word(const uint32_t* pl, uint32_t valid, uint32_t out[4]) {
+  if constexpr (P <= 2) {
+    const uint32_t M = (P == 1) ? valid : pl[1];
+    const uint32_t N = M & ~pl[0];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      out[q] = (spread8((M >> (8 * q)) & 0xFFu) << 1) | (spread8((N >> (8 * q)) & 0xFFu) << 3);
+  } else {
+    const uint32_t E1 = pl[1], E2 = pl[2], E3 = pl[3];
+    const uint32_t B1 = E1 | E3, B2 = E1 | E2, N = (E1 | E2 | E3) & ~pl[0];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      out[q] = (spread8((B1 >> (8 * q)) & 0xFFu) << 1) | (spread8((B2 >> (8 * q)) & 0xFFu) << 2) |
+               (spread8((N >> (8 * q)) & 0xFFu) << 3);
+  }
+}
+
+// Byte sizes / offsets of the three parts of a packed weight buffer.
+inline size_t wbytes_planes(int cout, int cin, int kh, int kw, int bits) {
+  return (size_t)kh * kw * ceil_div(cin, 32) * cout_pad(cout) * planes_of(bits) * 4;
+}
+inline size_t wbytes_i8(int cout, int cin, int kh, int kw) {
+  return (size_t)kh * kw * ceil_div(cin, 32) * cout_pad(cout) * 32;
+}
+inline size_t wbytes_fp4(int cout, int cin, int kh, int kw) {
+  return (size_t)kh * kw * ceil_div(ceil_div(cin, 32), 2) * cout_pad(cout) * 32;
+}
 
 // ---------------------------------------------------------------------------
 // Launchers (each returns a qconv_status; inputs already validated).
@@ -81,6 +160,11 @@ struct ConvArgs {
   uint32_t* out_packed;
   int out_bits, out_cw;
   Thr othr;
+  // matrix-core operand copies of the weights (parts of the packed buffer)
+  int cin;
+  const uint8_t* w_i8;
+  const uint8_t* w_fp4;
+  int mfma_fp4;  // 1: fp4 operands, 0: int8
 };
 int launch_conv_bitplane(const ConvArgs& a, hipStream_t s);
 int launch_conv_mfma(const ConvArgs& a, hipStream_t s);

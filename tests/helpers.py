@@ -29,8 +29,8 @@ def unpack_weight(words, cout, cin, kh, kw, bits) -> np.ndarray:
     """[kh][kw][cw][cout_pad][P] -> int8 levels [cout][cin][kh][kw]."""
     P = PLANES[bits]
     cw = (cin + 31) // 32
-    cop = (cout + 63) // 64 * 64
-    wd = np.asarray(words).view(np.uint32).reshape(kh, kw, cw, cop, P)
+    cop = (cout + 127) // 128 * 128
+    wd = np.asarray(words).view(np.uint32)[:kh * kw * cw * cop * P].reshape(kh, kw, cw, cop, P)
     bitidx = np.arange(32, dtype=np.uint32)
     b = ((wd[..., None] >> bitidx) & 1).astype(np.int8)  # kh,kw,cw,cop,P,32
     b = np.moveaxis(b, 2, 4)  # kh,kw,cop,P,cw,32
@@ -54,3 +54,33 @@ def tail_bits_zero(words, c, bits) -> bool:
     wd = np.asarray(words).view(np.uint32).reshape(-1, cw, P)
     mask = np.uint32((0xFFFFFFFF << (c % 32)) & 0xFFFFFFFF)
     return bool(np.all((wd[:, cw - 1, :] & mask) == 0))
+
+
+def weight_copies(words, cout, cin, kh, kw, bits):
+    """Decode the int8 and fp4 operand copies that follow the bitplanes in a
+    packed weight buffer -> two int8 level arrays [cout][cin][kh][kw]."""
+    P = PLANES[bits]
+    cw = (cin + 31) // 32
+    cwp = (cw + 1) // 2
+    cop = (cout + 127) // 128 * 128
+    raw = np.asarray(words).view(np.uint8)
+    off = kh * kw * cw * cop * P * 4
+    i8 = raw[off:off + kh * kw * cw * cop * 32].view(np.int8).reshape(kh, kw, cw, cop, 32)
+    off += kh * kw * cw * cop * 32
+    f4 = raw[off:off + kh * kw * cwp * cop * 32].reshape(kh, kw, cwp, cop, 2, 4, 4)  # pair, word, u32 q, byte
+    # levels from int8: channel cw*32 + c at byte c
+    lv8 = np.moveaxis(i8, 2, 3).reshape(kh, kw, cop, cw * 32)[:, :, :cout, :cin]
+    # fp4: u32 q of a word holds channels 8q..8q+7; nibble 2i <- channel 8q+i, nibble 2i+1 <- 8q+4+i
+    u32 = f4.copy().view(np.uint32).reshape(kh, kw, cwp, cop, 2, 4)
+    nib = np.stack([(u32 >> (4 * k)) & 0xF for k in range(8)], axis=-1)  # ..., q, nibble k
+    order = np.empty(8, np.int64)
+    for i in range(4):
+        order[i] = 2 * i
+        order[4 + i] = 2 * i + 1
+    nib = nib[..., order]  # channel-ordered within the byte group
+    mag = np.array([0, 0, 1, 0, 2, 0, 4, 0] * 2, np.int64)[nib]
+    sgn = np.where(nib & 8, -1, 1)
+    val = (mag * sgn).reshape(kh, kw, cwp, cop, 2 * 32)  # pair, 64 channels
+    lv4 = np.moveaxis(val, 2, 3).reshape(kh, kw, cop, cwp * 64)[:, :, :cout, :cin]
+    to_oihw = lambda a: np.ascontiguousarray(np.transpose(a, (2, 3, 0, 1))).astype(np.int8)
+    return to_oihw(lv8), to_oihw(lv4)

@@ -64,8 +64,11 @@ def test_packed_act_size(n, c, h, w, bits):
 
 @pytest.mark.parametrize("cout,cin,k,bits", [(128, 128, 3, 1), (10, 33, 1, 2), (512, 256, 3, 3)])
 def test_packed_weight_size(cout, cin, k, bits):
-    want = k * k * ((cin + 31) // 32) * ((cout + 63) // 64 * 64) * {1: 1, 2: 2, 3: 4}[bits] * 4
-    assert q.lib().qconv_packed_weight_bytes(cout, cin, k, k, bits) == want
+    cw, cop = (cin + 31) // 32, (cout + 127) // 128 * 128
+    planes = k * k * cw * cop * {1: 1, 2: 2, 3: 4}[bits] * 4
+    i8 = k * k * cw * cop * 32
+    fp4 = k * k * ((cw + 1) // 2) * cop * 32
+    assert q.lib().qconv_packed_weight_bytes(cout, cin, k, k, bits) == planes + i8 + fp4
 
 
 def test_size_queries_reject_bad_input():

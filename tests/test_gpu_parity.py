@@ -12,7 +12,7 @@ import torch
 import oracle
 import paper_2003_04296_amd as q
 from paper_2003_04296_amd import synth
-from helpers import tail_bits_zero, unpack_act, unpack_weight
+from helpers import tail_bits_zero, unpack_act, unpack_weight, weight_copies
 
 pytestmark = pytest.mark.gpu
 
@@ -73,9 +73,15 @@ def test_pack_weight_matches_oracle(dev, bits, shape):
     np.testing.assert_array_equal(scale.cpu().numpy(), s)
     np.testing.assert_array_equal(unpack_weight(words.cpu().numpy(), cout, cin, kh, kw, bits), lv)
     # padding rows of the weight layout are zero
-    cop = (cout + 63) // 64 * 64
-    wd = words.cpu().numpy().view(np.uint32).reshape(kh, kw, (cin + 31) // 32, cop, -1)
+    cop = (cout + 127) // 128 * 128
+    P = {1: 1, 2: 2, 3: 4}[bits]
+    wd = words.cpu().numpy().view(np.uint32)[:kh * kw * ((cin + 31) // 32) * cop * P]
+    wd = wd.reshape(kh, kw, (cin + 31) // 32, cop, P)
     assert np.all(wd[:, :, :, cout:, :] == 0)
+    # the matrix-core operand copies hold the same levels (0 past cin)
+    lv8, lv4 = weight_copies(words.cpu().numpy(), cout, cin, kh, kw, bits)
+    np.testing.assert_array_equal(lv8, lv)
+    np.testing.assert_array_equal(lv4, lv)
 
 
 # ---------------------------------------------------------------------------
@@ -92,7 +98,23 @@ CONV_CASES = [
     (1, 7, 11, 11, 17, 7, 2, 3),    # 7x7 / 2 pad 3
     (2, 31, 20, 20, 64, 3, 1, 1),   # 800 pixels: several 256-pixel blocks + ragged tail
     (1, 160, 1, 1, 100, 1, 1, 0),   # 1x1 map (FC)
+    # shapes aimed at the matrix-core tiling
+    (3, 64, 7, 7, 64, 3, 1, 1),     # several whole images per block, ho*wo % 4 != 0
+    (6, 256, 14, 14, 130, 3, 1, 1), # two channel chunks, cout padded to 256
+    (2, 96, 30, 30, 64, 3, 2, 1),   # stride 2, odd output size
+    (2, 64, 56, 56, 64, 3, 1, 1),   # image spans many blocks, blocks span rows
 ]
+
+ALGOS = {"bitplane": q.ALGO_BITPLANE, "mfma_i8": q.ALGO_MFMA_I8, "mfma_fp4": q.ALGO_MFMA_FP4}
+
+
+def _run_or_skip(fn):
+    try:
+        return fn()
+    except q.QconvError as e:
+        if e.status == q.QCONV_EUNSUPPORTED:
+            pytest.skip("configuration not supported by this algorithm")
+        raise
 
 
 def _gpu_conv(dev, x, w, a_bits, w_bits, stride, pad, algo=q.ALGO_AUTO, **epi):
@@ -111,41 +133,44 @@ def _oracle_acc(x, w, a_bits, w_bits, stride, pad):
     return oracle.qconv_acc(la, lw, a_bits, stride, pad), s
 
 
+@pytest.mark.parametrize("algo", list(ALGOS))
 @pytest.mark.parametrize("bits", BIT_PAIRS)
 @pytest.mark.parametrize("case", CONV_CASES)
-def test_conv_int32_bit_exact(dev, bits, case):
+def test_conv_int32_bit_exact(dev, bits, case, algo):
     n, cin, h, w, cout, k, s, p = case
     ab, wb = bits
     x, wt = _inputs(100 + sum(case), n, cin, h, w, cout, k)
-    out, _, _ = _gpu_conv(dev, x, wt, ab, wb, s, p, algo=q.ALGO_BITPLANE)
+    out, _, _ = _run_or_skip(lambda: _gpu_conv(dev, x, wt, ab, wb, s, p, algo=ALGOS[algo]))
     want, _ = _oracle_acc(x, wt, ab, wb, s, p)
     np.testing.assert_array_equal(out.cpu().numpy(), want)
 
 
-def _scale_epi_conv(dev, x, wt, ab, wb):
+def _scale_epi_conv(dev, x, wt, ab, wb, algo):
     n, cin, h, w = x.shape
     cout, _, k, _ = wt.shape
     act = q.pack_act(x.to(dev), ab)
     wq, scale = q.pack_weight(wt.to(dev), wb)
-    out, _ = q.conv(act, wq, n, cin, h, w, cout, k, 1, 1, ab, wb, mode=q.EPI_SCALE_F32, scale=scale)
+    out, _ = q.conv(act, wq, n, cin, h, w, cout, k, 1, 1, ab, wb, mode=q.EPI_SCALE_F32, scale=scale, algo=algo)
     torch.cuda.synchronize()
     return out
 
 
+@pytest.mark.parametrize("algo", list(ALGOS))
 @pytest.mark.parametrize("bits", [(1, 1), (3, 3)])
-def test_scale_epilogue_uses_mean_abs_weight(dev, bits):
+def test_scale_epilogue_uses_mean_abs_weight(dev, bits, algo):
     ab, wb = bits
     x, wt = _inputs(6, 2, 40, 9, 9, 70, 3)
-    out = _scale_epi_conv(dev, x, wt, ab, wb)
+    out = _run_or_skip(lambda: _scale_epi_conv(dev, x, wt, ab, wb, ALGOS[algo]))
     acc, s = _oracle_acc(x, wt, ab, wb, 1, 1)
     shift = oracle.level_shift(ab) + oracle.level_shift(wb)
     np.testing.assert_array_equal(out.cpu().numpy(), oracle.epi_scale(acc, s, shift))
 
 
+@pytest.mark.parametrize("algo", list(ALGOS))
 @pytest.mark.parametrize("bits", BIT_PAIRS)
 @pytest.mark.parametrize("pool", [False, True])
 @pytest.mark.parametrize("out_bits", [0, 1, 2, 3])
-def test_bn_epilogues(dev, bits, pool, out_bits):
+def test_bn_epilogues(dev, bits, pool, out_bits, algo):
     """{QConv-[pool]-BN-HardTanh} -> fp32 output, or requantized + packed output."""
     ab, wb = bits
     n, cin, h, w, cout = 2, 40, 10, 9, 70
@@ -153,8 +178,8 @@ def test_bn_epilogues(dev, bits, pool, out_bits):
     k, b = _bn(7, cout)
     flags = q.EPI_POOL2 if pool else 0
     mode = q.EPI_BN_PACK if out_bits else q.EPI_BN_F32
-    out, outp, _ = _gpu_conv(dev, x, wt, ab, wb, 1, 1, mode=mode, flags=flags, bn_k=k.to(dev), bn_b=b.to(dev),
-                             out_bits=out_bits)
+    out, outp, _ = _run_or_skip(lambda: _gpu_conv(dev, x, wt, ab, wb, 1, 1, algo=ALGOS[algo], mode=mode, flags=flags,
+                                                  bn_k=k.to(dev), bn_b=b.to(dev), out_bits=out_bits))
     acc, _ = _oracle_acc(x, wt, ab, wb, 1, 1)
     if pool:
         acc = oracle.maxpool2_int(acc)
@@ -169,10 +194,12 @@ def test_bn_epilogues(dev, bits, pool, out_bits):
         assert tail_bits_zero(outp.cpu().numpy(), cout, out_bits)
 
 
+@pytest.mark.parametrize("algo", list(ALGOS))
 @pytest.mark.parametrize("bits", [(2, 2), (1, 1), (3, 3)])
-def test_bn_residual_and_repack(dev, bits):
+@pytest.mark.parametrize("hw", [8, 7])
+def test_bn_residual_and_repack(dev, bits, algo, hw):
     ab, wb = bits
-    n, cin, h, w, cout = 2, 64, 8, 8, 64
+    n, cin, h, w, cout = 3, 64, hw, hw, 64
     x, wt = _inputs(8, n, cin, h, w, cout, 3)
     k, b = _bn(8, cout)
     g = synth.generator(99)
@@ -180,8 +207,9 @@ def test_bn_residual_and_repack(dev, bits):
     act = q.pack_act(x.to(dev), ab)
     wq, _ = q.pack_weight(wt.to(dev), wb)
     outp = torch.empty(q.packed_act_words(n, cout, h, w, ab), dtype=torch.int32, device=dev)
-    out, _ = q.conv(act, wq, n, cin, h, w, cout, 3, 1, 1, ab, wb, mode=q.EPI_BN_F32, flags=q.EPI_RESIDUAL,
-                    bn_k=k.to(dev), bn_b=b.to(dev), residual=res.to(dev), out_bits=ab, out_packed=outp)
+    out, _ = _run_or_skip(lambda: q.conv(act, wq, n, cin, h, w, cout, 3, 1, 1, ab, wb, mode=q.EPI_BN_F32,
+                                         flags=q.EPI_RESIDUAL, bn_k=k.to(dev), bn_b=b.to(dev), residual=res.to(dev),
+                                         out_bits=ab, out_packed=outp, algo=ALGOS[algo]))
     torch.cuda.synchronize()
     acc, _ = _oracle_acc(x, wt, ab, wb, 1, 1)
     shift = oracle.level_shift(ab) + oracle.level_shift(wb)
@@ -258,6 +286,9 @@ def test_workload2_full_sampled(dev):
     kd, bd = torch.from_numpy(k).to(dev), torch.from_numpy(b).to(dev)
     z, _ = q.conv(act, wq, n, c, h, w, 128, 3, 1, 1, 2, 1, mode=q.EPI_BN_F32, bn_k=kd, bn_b=bd)
     acc, _ = q.conv(act, wq, n, c, h, w, 128, 3, 1, 1, 2, 1, algo=q.ALGO_BITPLANE)
+    for algo in (q.ALGO_MFMA_I8, q.ALGO_MFMA_FP4):
+        other, _ = q.conv(act, wq, n, c, h, w, 128, 3, 1, 1, 2, 1, algo=algo)
+        assert torch.equal(other, acc), algo
     torch.cuda.synchronize()
     idx, want, _ = _check_sampled(case, acc, 2002)
     # BN output at the sampled positions: fmaf(k_c, acc, b_c) of the oracle's accumulator
@@ -283,6 +314,9 @@ def test_workload5_full_sampled(dev, layer):
     acc, _ = q.conv(act, wq, n, c, h, w, c, 3, 1, 1, 3, 3)
     torch.cuda.synchronize()
     _check_sampled(case, acc, 5000 + layer, 2048)
+    for algo in (q.ALGO_BITPLANE, q.ALGO_MFMA_I8):
+        other, _ = q.conv(act, wq, n, c, h, w, c, 3, 1, 1, 3, 3, algo=algo)
+        assert torch.equal(other, acc), algo
     assert int(acc.abs().max()) <= c * 9 * 16
 
 
