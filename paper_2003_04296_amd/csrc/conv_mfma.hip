@@ -44,10 +44,7 @@ constexpr int BLOCK_PIX = 2 * MTW * 32;  // 2 waves along M
 #define QC_MFMA_WPE 3
 #endif
 constexpr int MAX_LDS = 64 * 1024;
-#ifndef QC_MFMA_UNROLL
-#define QC_MFMA_UNROLL 2
-#endif
-constexpr int KUNR = QC_MFMA_UNROLL;  // k-steps whose loads are issued together
+
 
 template <int FP4>
 struct OpT;
@@ -69,6 +66,7 @@ struct OpT<1> {
 struct MfmaArgs {
   ConvArgs c;
   const uint8_t* wx;    // expanded weights in the chosen operand format
+  int wx_bytes;         // size of that operand copy (bounds of the B buffer reads)
   int ipb;              // whole images per block (1: the block is a pixel range of one image)
   int blocks_per_img;   // ipb == 1: blocks per image
   int hr, hc;           // halo rows / cols per image slot
@@ -77,6 +75,9 @@ struct MfmaArgs {
   int ksteps;           // k-steps per tap over all words (int8: cw, fp4: ceil(cw/2))
   int nchunks;
   int vec_store;        // ho*wo % 4 == 0: 4 consecutive pixels are one aligned 16-byte run
+  int tiles_px;         // pixel tiles (blocks of BLOCK_PIX pixels or ipb images)
+  int tiles_co;         // output-channel tiles (64 * NTW channels)
+  int halo_bytes;       // LDS bytes of the halo tile (reused as the output stage)
 };
 
 __device__ __forceinline__ v16i mfma(v4i a, v4i b, v16i c) {
@@ -270,153 +271,172 @@ __global__ __launch_bounds__(256, QC_MFMA_WPE) void conv_mfma_kernel(const MfmaA
   const int g = lane >> 5, r32 = lane & 31;
   const int hwo = a.ho * a.wo;
 
-  // ---- which pixels this block owns ----
-  int img0, p0;
-  if (m.ipb == 1) {
-    img0 = blockIdx.x / m.blocks_per_img;
-    p0 = (blockIdx.x % m.blocks_per_img) * BLOCK_PIX;
-  } else {
-    img0 = blockIdx.x * m.ipb;
-    p0 = 0;
-  }
-  const int oy0 = p0 / a.wo;
-  const int iy0 = oy0 * a.stride - a.pad;
-  const int co_blk = blockIdx.y * (64 * NTW);
   const int slot_pix = m.hr * m.hc;
-
-  // LDS byte offset of each of the wave's M-tile rows at tap (0, 0), plus
-  // this lane's 16-byte half of the k-step.
-  int abase[MTW];
-#pragma unroll
-  for (int i = 0; i < MTW; ++i) {
-    const int t = 32 * (wm * MTW + i) + r32;
-    int slot, pp;
-    if (m.ipb == 1) {
-      slot = 0;
-      pp = p0 + t;
-    } else {
-      slot = t / hwo;
-      pp = t - slot * hwo;
-    }
-    bool ok = (m.ipb == 1) ? (pp < hwo) : (slot < m.ipb);
-    if (!ok) {  // a row past the end: read any valid LDS pixel, its result is dropped
-      slot = 0;
-      pp = p0;
-    }
-    const int oy = pp / a.wo, ox = pp - (pp / a.wo) * a.wo;
-    const int hp = slot * slot_pix + (oy - oy0) * a.stride * m.hc + ox * a.stride;
-    abase[i] = hp * m.pix_bytes + g * 16;
-  }
-
-  acc_t acc[MTW][NTW];
-#pragma unroll
-  for (int i = 0; i < MTW; ++i)
-#pragma unroll
-    for (int j = 0; j < NTW; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0;
-
   const int apix = a.cw * PA;
   const int n_slots = (m.ipb == 1) ? 1 : m.ipb;
   const int items_per_chunk = n_slots * slot_pix * m.chunk_words;
   const int taps = a.kh * a.kw;
   const int steps_per_chunk = m.chunk_words / O::WORDS_PER_STEP;
+  // B fragments are read through a buffer resource: the per-lane part of
+  // the address is a vector offset, the per-step part a scalar offset, and
+  // reads past the operand copy return 0.
+  const __amdgpu_buffer_rsrc_t brsrc =
+      __builtin_amdgcn_make_buffer_rsrc((void*)m.wx, (short)0, m.wx_bytes, 0x00020000);
+  const int bstride = a.cop * 32;  // bytes between consecutive k-steps
+  // one (pixel tile, channel tile) per block
+  {
+    const int pb = blockIdx.x;
+    const int co_blk = blockIdx.y * (64 * NTW);
+    int img0, p0;
+    if (m.ipb == 1) {
+      img0 = pb / m.blocks_per_img;
+      p0 = (pb % m.blocks_per_img) * BLOCK_PIX;
+    } else {
+      img0 = pb * m.ipb;
+      p0 = 0;
+    }
+    const int oy0 = p0 / a.wo;
+    const int iy0 = oy0 * a.stride - a.pad;
 
-  // per-lane B fragment pointers (tap 0, k-step 0) of the wave's N-tiles
-  const uint8_t* bbase[NTW];
+    // LDS byte offset of each of the wave's M-tile rows at tap (0, 0), plus
+    // this lane's 16-byte half of the k-step.
+    int abase[MTW];
 #pragma unroll
-  for (int j = 0; j < NTW; ++j)
-    bbase[j] = m.wx + ((int64_t)(co_blk + 32 * (wn * NTW + j) + r32)) * 32 + g * 16;
-  const int64_t bstride = (int64_t)a.cop * 32;  // bytes between consecutive k-steps
+    for (int i = 0; i < MTW; ++i) {
+      const int t = 32 * (wm * MTW + i) + r32;
+      int slot, pp;
+      if (m.ipb == 1) {
+        slot = 0;
+        pp = p0 + t;
+      } else {
+        slot = t / hwo;
+        pp = t - slot * hwo;
+      }
+      bool ok = (m.ipb == 1) ? (pp < hwo) : (slot < m.ipb);
+      if (!ok) {  // a row past the end: read any valid LDS pixel, its result is dropped
+        slot = 0;
+        pp = p0;
+      }
+      const int oy = pp / a.wo, ox = pp - (pp / a.wo) * a.wo;
+      const int hp = slot * slot_pix + (oy - oy0) * a.stride * m.hc + ox * a.stride;
+      abase[i] = hp * m.pix_bytes + g * 16;
+    }
 
-  for (int chunk = 0; chunk < m.nchunks; ++chunk) {
-    __syncthreads();
-    // ---- expand the halo tile of this channel chunk into LDS ----
-    // loads of up to 4 items are issued together before any is expanded
-    for (int it0 = 0; it0 < items_per_chunk; it0 += 4 * 256) {
-      uint32_t pl[4][PA];
-      int dst[4];
+    acc_t acc[MTW][NTW];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int it = it0 + u * 256 + tid;
-        dst[u] = -1;
+    for (int i = 0; i < MTW; ++i)
 #pragma unroll
-        for (int p = 0; p < PA; ++p) pl[u][p] = 0u;
-        if (it < items_per_chunk) {
-          const int cwl = it % m.chunk_words;
-          const int hp = it / m.chunk_words;
-          const int slot = hp / slot_pix;
-          const int rem = hp - slot * slot_pix;
-          const int hrow = rem / m.hc, hcol = rem - (rem / m.hc) * m.hc;
-          const int img = img0 + slot;
-          const int iy = iy0 + hrow, ix = hcol - a.pad;
-          const int cw = chunk * m.chunk_words + cwl;
-          dst[u] = hp * m.pix_bytes + cwl * O::WORD_BYTES;
-          if (img < a.n && iy >= 0 && iy < a.h && ix >= 0 && ix < a.w && cw < a.cw) {
-            const uint32_t* src = a.act + (((int64_t)img * a.h + iy) * a.w + ix) * apix + cw * PA;
+      for (int j = 0; j < NTW; ++j)
 #pragma unroll
-            for (int p = 0; p < PA; ++p) pl[u][p] = src[p];
+        for (int v = 0; v < 16; ++v) acc[i][j][v] = 0;
+
+    int bvoff[NTW];
+#pragma unroll
+    for (int j = 0; j < NTW; ++j) bvoff[j] = (co_blk + 32 * (wn * NTW + j) + r32) * 32 + g * 16;
+
+    for (int chunk = 0; chunk < m.nchunks; ++chunk) {
+      __syncthreads();
+      // ---- expand the halo tile of this channel chunk into LDS ----
+      // loads of up to 4 items are issued together before any is expanded
+      for (int it0 = 0; it0 < items_per_chunk; it0 += 4 * 256) {
+        uint32_t pl[4][PA];
+        int dst[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int it = it0 + u * 256 + tid;
+          dst[u] = -1;
+#pragma unroll
+          for (int p = 0; p < PA; ++p) pl[u][p] = 0u;
+          if (it < items_per_chunk) {
+            const int cwl = it % m.chunk_words;
+            const int hp = it / m.chunk_words;
+            const int slot = hp / slot_pix;
+            const int rem = hp - slot * slot_pix;
+            const int hrow = rem / m.hc, hcol = rem - (rem / m.hc) * m.hc;
+            const int img = img0 + slot;
+            const int iy = iy0 + hrow, ix = hcol - a.pad;
+            const int cw = chunk * m.chunk_words + cwl;
+            dst[u] = hp * m.pix_bytes + cwl * O::WORD_BYTES;
+            if (img < a.n && iy >= 0 && iy < a.h && ix >= 0 && ix < a.w && cw < a.cw) {
+              const uint32_t* src = a.act + (((int64_t)img * a.h + iy) * a.w + ix) * apix + cw * PA;
+#pragma unroll
+              for (int p = 0; p < PA; ++p) pl[u][p] = src[p];
+            }
           }
         }
-      }
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-        if (dst[u] >= 0) expand_to_lds<FP4, PA>(pl[u], lds + dst[u]);
-    }
-    __syncthreads();
+        for (int u = 0; u < 4; ++u)
+          if (dst[u] >= 0) expand_to_lds<FP4, PA>(pl[u], lds + dst[u]);
+      }
+      __syncthreads();
 
-    // ---- MFMA over (tap, k-step) of this chunk ----
-    // KUNR k-steps per iteration: the fragment loads of all of them are
-    // issued first, so later steps' loads are in flight while the first
-    // step's MFMAs run.  (tap, k-step) advance incrementally.
-    const int ks0 = chunk * steps_per_chunk;
-    const int spc = min(m.ksteps, ks0 + steps_per_chunk) - ks0;  // k-steps per tap in this chunk
-    const int nsteps = taps * spc;
-    int tap = 0, ksl = 0, ky = 0, kx = 0;
-    auto advance = [&]() {
-      if (++ksl == spc) {
-        ksl = 0;
-        ++tap;
-        if (++kx == a.kw) {
-          kx = 0;
-          ++ky;
+      // ---- MFMA over (tap, k-step) of this chunk ----
+      // B fragments come from a ring of three register sets, each loaded two
+      // k-steps before its MFMAs (buffer loads, so the compiler keeps them
+      // where they are issued).  A fragments are read from LDS in the step
+      // that uses them.  Steps advance (tap, k-step) incrementally.
+      const int ks0 = chunk * steps_per_chunk;
+      const int spc = min(m.ksteps, ks0 + steps_per_chunk) - ks0;  // k-steps per tap in this chunk
+      const int nsteps = taps * spc;
+      // load stream (runs two steps ahead of the compute stream)
+      int l_tap = 0, l_ksl = 0, l_count = 0;
+      auto bload = [&](v4i (&dst)[NTW]) {
+        const int so = (l_tap * m.ksteps + ks0 + l_ksl) * bstride;
+#pragma unroll
+        for (int j = 0; j < NTW; ++j)
+          dst[j] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(brsrc, bvoff[j], so, 0));
+        if (l_count + 1 < nsteps) {  // the last step is reloaded past the end (never used)
+          ++l_count;
+          if (++l_ksl == spc) {
+            l_ksl = 0;
+            ++l_tap;
+          }
         }
-      }
-    };
-    for (int st = 0; st < nsteps; st += KUNR) {
-      const int nu = min(KUNR, nsteps - st);  // uniform
-      v4i bf[KUNR][NTW], af[KUNR][MTW];
+      };
+      // compute stream
+      int c_ksl = 0, c_ky = 0, c_kx = 0;
+      auto step = [&](const v4i (&bf)[NTW]) {
+        const int lo = (c_ky * m.hc + c_kx) * m.pix_bytes + c_ksl * 32;
+        v4i af[MTW];
 #pragma unroll
-      for (int u = 0; u < KUNR; ++u) {
-        if (u >= nu) break;
-        const int64_t bo = ((int64_t)tap * m.ksteps + ks0 + ksl) * bstride;
-        const int lo = (ky * m.hc + kx) * m.pix_bytes + ksl * 32;
-#pragma unroll
-        for (int j = 0; j < NTW; ++j) bf[u][j] = *reinterpret_cast<const v4i*>(bbase[j] + bo);
-#pragma unroll
-        for (int i = 0; i < MTW; ++i) af[u][i] = *reinterpret_cast<const v4i*>(lds + abase[i] + lo);
-        advance();
-      }
-#pragma unroll
-      for (int u = 0; u < KUNR; ++u) {
-        if (u >= nu) break;
+        for (int i = 0; i < MTW; ++i) af[i] = *reinterpret_cast<const v4i*>(lds + abase[i] + lo);
 #pragma unroll
         for (int i = 0; i < MTW; ++i)
 #pragma unroll
-          for (int j = 0; j < NTW; ++j) acc[i][j] = mfma(af[u][i], bf[u][j], acc[i][j]);
+          for (int j = 0; j < NTW; ++j) acc[i][j] = mfma(af[i], bf[j], acc[i][j]);
+        if (++c_ksl == spc) {
+          c_ksl = 0;
+          if (++c_kx == a.kw) {
+            c_kx = 0;
+            ++c_ky;
+          }
+        }
+      };
+      v4i B0[NTW], B1[NTW], B2[NTW];
+      bload(B0);
+      bload(B1);
+      for (int st = 0; st < nsteps; st += 3) {
+        bload(B2);
+        step(B0);
+        if (st + 1 >= nsteps) break;
+        bload(B0);
+        step(B1);
+        if (st + 2 >= nsteps) break;
+        bload(B1);
+        step(B2);
       }
     }
-  }
 
-  // ---- epilogue ----
-  __syncthreads();  // every wave is done with the halo tile; LDS becomes the output stage
-  const EpiCtx x = {img0, p0, co_blk, hwo, lane};
-  float* stage = reinterpret_cast<float*>(lds + wave * STAGE_BYTES);
-  Unroll<0, MTW>::run([&](auto I) {
-    Unroll<0, NTW>::run([&](auto J) {
-      store_tile(m, x, acc[I][J], wm * MTW + I, co_blk + 32 * (wn * NTW + J), stage);
+    // ---- epilogue ----
+    __syncthreads();  // every wave is done with the halo tile; LDS becomes the output stage
+    float* stage = reinterpret_cast<float*>(lds + wave * STAGE_BYTES);
+    const EpiCtx x = {img0, p0, co_blk, hwo, lane};
+    Unroll<0, MTW>::run([&](auto I) {
+      Unroll<0, NTW>::run([&](auto J) {
+        store_tile(m, x, acc[I][J], wm * MTW + I, co_blk + 32 * (wn * NTW + J), stage);
+      });
     });
-  });
+  }
 }
 
 bool plan(const ConvArgs& a, MfmaArgs* m) {
@@ -429,6 +449,7 @@ bool plan(const ConvArgs& a, MfmaArgs* m) {
   const int cw_round = ceil_div(a.cw, wpstep) * wpstep;
   m->ksteps = ceil_div(a.cw, wpstep);
   m->wx = fp4 ? a.w_fp4 : a.w_i8;
+  m->wx_bytes = (int)(a.kh * a.kw * m->ksteps * a.cop * 32);
   const int hwo = a.ho * a.wo;
   m->hc = (a.wo - 1) * a.stride + a.kw;
   m->vec_store = (hwo % 4 == 0) ? 1 : 0;
@@ -468,22 +489,21 @@ bool plan(const ConvArgs& a, MfmaArgs* m) {
   if (best_pix < 0) return false;
   *m = best;
   if (m->ipb == 1 && m->blocks_per_img == 0) m->blocks_per_img = 1;
+  m->tiles_px = (m->ipb == 1) ? a.n * m->blocks_per_img : ceil_div(a.n, m->ipb);
+  m->tiles_co = (a.cout > 64) ? ceil_div(a.cout, 128) : 1;
+  m->halo_bytes = m->hr * m->hc * m->pix_bytes * (m->ipb == 1 ? 1 : m->ipb);
   return true;
 }
 
 template <int FP4, int PA>
 int launch_fp(const MfmaArgs& m, hipStream_t s) {
   const ConvArgs& a = m.c;
-  const unsigned gx = (m.ipb == 1) ? (unsigned)(a.n * m.blocks_per_img) : (unsigned)ceil_div(a.n, m.ipb);
-  const size_t halo = (size_t)m.hr * m.hc * m.pix_bytes * (m.ipb == 1 ? 1 : m.ipb);
-  const size_t lds = halo > (size_t)(4 * STAGE_BYTES) ? halo : (size_t)(4 * STAGE_BYTES);
-  if (a.cout > 64) {
-    const dim3 grid(gx, (unsigned)ceil_div(a.cout, 128));
+  const size_t lds = max((size_t)m.halo_bytes, (size_t)(4 * STAGE_BYTES));
+  const dim3 grid((unsigned)m.tiles_px, (unsigned)m.tiles_co);
+  if (a.cout > 64)
     conv_mfma_kernel<FP4, PA, 2><<<grid, 256, lds, s>>>(m);
-  } else {
-    const dim3 grid(gx, 1);
+  else
     conv_mfma_kernel<FP4, PA, 1><<<grid, 256, lds, s>>>(m);
-  }
   return hip_status();
 }
 
