@@ -78,6 +78,8 @@ struct MfmaArgs {
   int tiles_px;         // pixel tiles (blocks of BLOCK_PIX pixels or ipb images)
   int tiles_co;         // output-channel tiles (64 * NTW channels)
   int halo_bytes;       // LDS bytes of the halo tile (reused as the output stage)
+  int pool_wo;          // 2x2 max pooling: the conv output width (8, 16, 32 or 64), else 0
+  int mt_interleave;    // wave wm owns M-tiles wm, wm + 2, ... instead of a contiguous run
 };
 
 __device__ __forceinline__ v16i mfma(v4i a, v4i b, v16i c) {
@@ -260,6 +262,78 @@ __device__ __forceinline__ void store_tile(const MfmaArgs& m, const EpiCtx& x, c
   }
 }
 
+// Pooled epilogue (2x2 max over the integer accumulator, before BN) of one
+// wave's two M-tiles for output channels [c32, c32 + 32).  The block starts
+// at an even conv row and the M-tiles are assigned so that all four pixels of
+// every window sit in the same lane:
+//   wo = 32: the two tiles are rows 2r and 2r+1 (same register);
+//   wo = 64: the tiles are the same half of rows 2r and 2r+1 (interleaved tiles);
+//   wo = 16: one tile is two rows, the lower pixel is register v + 8;
+//   wo =  8: one tile is four rows, the lower pixel is register v + 4;
+// and the horizontal neighbour of an even pixel (even v) is register v + 1.
+// Lane (g, r32) ends with 8 pooled pixels of channel c32 + r32.
+template <int WO, class AccT>
+__device__ __forceinline__ void store_pool_tiles(const MfmaArgs& m, const EpiCtx& x, const AccT& a0,
+                                                 const AccT& a1, int mt0, int mt1, int c32) {
+  const ConvArgs& a = m.c;
+  const int g = x.lane >> 5, r32 = x.lane & 31;
+  const float inv = 1.0f / (float)(1 << a.shift);
+  const bool pack = a.out_packed != nullptr && c32 < a.cout;  // uniform
+  const int co = c32 + r32;
+  const bool co_ok = co < a.cout;
+  const int cs = min(co, a.cout - 1);
+  float kk = 0.0f, bb = 0.0f, ss = 0.0f;
+  if (a.mode == QCONV_EPI_BN_F32 || a.mode == QCONV_EPI_BN_PACK) {
+    kk = a.bn_k[cs];
+    bb = a.bn_b[cs];
+  } else if (a.mode == QCONV_EPI_SCALE_F32) {
+    ss = a.scale[cs];
+  }
+  const int64_t plane = (int64_t)a.oh_out * a.ow_out;
+  const int pout = pack ? planes_of(a.out_bits) : 0;
+  const int cword = c32 >> 5;
+  Unroll<0, 8>::run([&](auto S) {
+    constexpr int s = decltype(S)::value;
+    constexpr bool pair_tiles = WO >= 32;
+    constexpr int ti = pair_tiles ? 0 : s / 4;  // tile holding the window's upper row
+    constexpr int u = pair_tiles ? s : s % 4;
+    constexpr int v = (WO == 8) ? (u & 1) * 2 + (u >> 1) * 8 : 2 * u;
+    constexpr int dv = pair_tiles ? 0 : (WO == 16 ? 8 : 4);
+    const AccT& top = (ti == 0) ? a0 : a1;
+    const AccT& bot = pair_tiles ? a1 : top;
+    const int best = max(max(acc_value(top, v), acc_value(top, v + 1)),
+                         max(acc_value(bot, v + dv), acc_value(bot, v + dv + 1)));
+    const int t = 32 * ((ti == 0) ? mt0 : mt1) + 8 * (v / 4) + 4 * g + (v % 4);
+    int img = 0, pp = 0;
+    bool ok = block_pixel(m, x, t, &img, &pp);
+    const int oy = pp / a.wo, ox = pp - (pp / a.wo) * a.wo;
+    const int py = oy >> 1, px = ox >> 1;
+    ok = ok && py < a.oh_out;  // an odd last conv row has no pooled row
+    const float ar = (float)best * inv;
+    float z = (a.mode == QCONV_EPI_SCALE_F32) ? ss * ar : fmaf(kk, ar, bb);
+    const int64_t oi = ((int64_t)img * a.cout + cs) * plane + (int64_t)py * a.ow_out + px;
+    if (a.mode != QCONV_EPI_BN_PACK && co_ok && ok) {
+      if (a.mode == QCONV_EPI_INT32) {
+        static_cast<int32_t*>(a.out)[oi] = best;
+      } else {
+        if (a.residual_on) z = z + a.residual[oi];
+        static_cast<float*>(a.out)[oi] = z;
+      }
+    }
+    if (pack) {
+      const uint32_t pl = (co_ok && ok) ? quant_rt(hardtanh(z), a.out_bits, a.othr) : 0u;
+      for (int p = 0; p < pout; ++p) {
+        const uint64_t bal = __ballot((pl >> p) & 1u);
+        if (r32 == 0 && ok) {
+          const uint32_t word = g ? (uint32_t)(bal >> 32) : (uint32_t)bal;
+          a.out_packed[((((int64_t)img * a.oh_out + py) * a.ow_out + px) * a.out_cw + cword) * pout + p] =
+              word;
+        }
+      }
+    }
+  });
+}
+
 template <int FP4, int PA, int NTW>
 __global__ __launch_bounds__(256, QC_MFMA_WPE) void conv_mfma_kernel(const MfmaArgs m) {
   using O = OpT<FP4>;
@@ -303,7 +377,7 @@ __global__ __launch_bounds__(256, QC_MFMA_WPE) void conv_mfma_kernel(const MfmaA
     int abase[MTW];
 #pragma unroll
     for (int i = 0; i < MTW; ++i) {
-      const int t = 32 * (wm * MTW + i) + r32;
+      const int t = 32 * (m.mt_interleave ? wm + 2 * i : wm * MTW + i) + r32;
       int slot, pp;
       if (m.ipb == 1) {
         slot = 0;
@@ -431,6 +505,22 @@ __global__ __launch_bounds__(256, QC_MFMA_WPE) void conv_mfma_kernel(const MfmaA
     __syncthreads();  // every wave is done with the halo tile; LDS becomes the output stage
     float* stage = reinterpret_cast<float*>(lds + wave * STAGE_BYTES);
     const EpiCtx x = {img0, p0, co_blk, hwo, lane};
+    if constexpr (MTW == 2) {
+      if (m.pool_wo) {
+        const int mt0 = m.mt_interleave ? wm : 2 * wm;
+        const int mt1 = m.mt_interleave ? wm + 2 : 2 * wm + 1;
+        Unroll<0, NTW>::run([&](auto J) {
+          const int c32 = co_blk + 32 * (wn * NTW + J);
+          switch (m.pool_wo) {
+            case 8: store_pool_tiles<8>(m, x, acc[0][J], acc[1][J], mt0, mt1, c32); break;
+            case 16: store_pool_tiles<16>(m, x, acc[0][J], acc[1][J], mt0, mt1, c32); break;
+            case 32: store_pool_tiles<32>(m, x, acc[0][J], acc[1][J], mt0, mt1, c32); break;
+            default: store_pool_tiles<64>(m, x, acc[0][J], acc[1][J], mt0, mt1, c32); break;
+          }
+        });
+        return;
+      }
+    }
     Unroll<0, MTW>::run([&](auto I) {
       Unroll<0, NTW>::run([&](auto J) {
         store_tile(m, x, acc[I][J], wm * MTW + I, co_blk + 32 * (wn * NTW + J), stage);
@@ -488,6 +578,13 @@ bool plan(const ConvArgs& a, MfmaArgs* m) {
   }
   if (best_pix < 0) return false;
   *m = best;
+  if (a.pool) {
+    // every 2x2 window must fall in one lane of one wave (see store_pool_tiles)
+    if (MTW != 2 || !(a.wo == 8 || a.wo == 16 || a.wo == 32 || a.wo == 64)) return false;
+    if (m->ipb > 1 && a.ho % 2 != 0) return false;
+    m->pool_wo = a.wo;
+    m->mt_interleave = (a.wo == 64) ? 1 : 0;
+  }
   if (m->ipb == 1 && m->blocks_per_img == 0) m->blocks_per_img = 1;
   m->tiles_px = (m->ipb == 1) ? a.n * m->blocks_per_img : ceil_div(a.n, m->ipb);
   m->tiles_co = (a.cout > 64) ? ceil_div(a.cout, 128) : 1;
@@ -510,7 +607,7 @@ int launch_fp(const MfmaArgs& m, hipStream_t s) {
 }  // namespace
 
 bool mfma_supports(const ConvArgs& a) {
-  if (a.pool || a.stride > 2 || a.n == 0) return false;
+  if (a.stride > 2 || a.n == 0) return false;
   MfmaArgs m;
   return plan(a, &m);
 }

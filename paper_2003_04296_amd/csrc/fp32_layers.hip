@@ -123,39 +123,112 @@ __global__ __launch_bounds__(256) void avgpool_f32_kernel(const float* __restric
   y[i] = s / (float)hw;
 }
 
-constexpr int FC_TN = 16;  // outputs per lane; lanes = images
+// Last FC.  Each output of each image is one sequential fmaf chain over the
+// inputs, so the run time is set by the chain length, not by the flops: a
+// wave owns ONE output for 64 images (lane = image) and a block of 4 waves
+// owns 4 consecutive outputs.  Per chunk of inputs the block stages, with
+// all of its loads in flight at once, the 64 images' inputs and the 4 weight
+// rows in LDS; lanes then read their own input row (16-byte reads, padded
+// rows) and the wave's weight row as a broadcast.
+//
+// x_bits = 0: x is fp32 [n][in].  x_bits = 1: x is the packed sign plane
+// [n][ceil(in/32)] of {-1,+1} inputs (a 1x1 map), and fmaf(+-1, w, acc) is
+// computed as the single-rounding add acc + (+-w).
+constexpr int FC_CI_F32 = 192;           // fp32 inputs per chunk
+constexpr int FC_XLD = FC_CI_F32 + 4;    // padded LDS row (floats)
+constexpr int FC_CW_BIN = 32;            // packed words per chunk (1024 inputs)
+constexpr int FC_XLD_BIN = FC_CW_BIN + 1;
 
 template <int X_BITS>
-__global__ __launch_bounds__(64) void fc_f32_kernel(const void* __restrict__ xin, int n, int in,
+__global__ __launch_bounds__(256) void fc_f32_kernel(const void* __restrict__ xin, int n, int in,
                                                     const float* __restrict__ w,
                                                     const float* __restrict__ bias, int out,
                                                     float* __restrict__ y) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= n) return;
-  const int o0 = blockIdx.y * FC_TN;
-  float acc[FC_TN];
+  constexpr int CI = X_BITS ? FC_CW_BIN * 32 : FC_CI_F32;
+  constexpr int XWORDS = X_BITS ? 64 * FC_XLD_BIN : 64 * FC_XLD;
+  __shared__ __attribute__((aligned(16))) float ws[4 * CI];
+  __shared__ __attribute__((aligned(16))) uint32_t xs[XWORDS];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int b0 = blockIdx.x * 64;
+  const int nb = min(64, n - b0);
+  const int o = blockIdx.y * 4 + wave;
+  const int oc = min(o, out - 1);
+  const int ob = blockIdx.y * 4;
+  float acc = 0.0f;
+  for (int c0 = 0; c0 < in; c0 += CI) {
+    const int L = min(CI, in - c0);  // inputs in this chunk
+    __syncthreads();
+    // Every load of the chunk is issued before the first LDS store.  Indices
+    // are clamped into the chunk (and the batch), so no load is guarded;
+    // values staged past L (or past the batch) are never read.
+    // Weights: thread -> row tid / 64 (rows past out repeat the last one),
+    // columns tid % 64 + 64 u.  Inputs: thread -> row tid / 4, columns
+    // tid % 4 + 4 u.
+    constexpr int WU = CI / 64;
+    constexpr int XCOLS = X_BITS ? FC_CW_BIN : CI;
+    constexpr int XU = XCOLS / 4;
+    constexpr int XLD = X_BITS ? FC_XLD_BIN : FC_XLD;
+    const int xl = X_BITS ? ((L + 31) >> 5) : L;  // valid columns of the input tile
+    float wv[WU];
+    uint32_t xv[XU];
+    {
+      const float* wrow = w + (int64_t)min(ob + (tid >> 6), out - 1) * in + c0;
 #pragma unroll
-  for (int j = 0; j < FC_TN; ++j) acc[j] = 0.0f;
-  const int cwn = (in + 31) >> 5;
-  for (int i = 0; i < in; ++i) {
-    float xv;
+      for (int u = 0; u < WU; ++u) wv[u] = wrow[min((tid & 63) + 64 * u, L - 1)];
+      const int r = min(tid >> 2, nb - 1);
+      const uint32_t* xrow;
+      if constexpr (X_BITS == 0)
+        xrow = static_cast<const uint32_t*>(xin) + (int64_t)(b0 + r) * in + c0;
+      else
+        xrow = static_cast<const uint32_t*>(xin) + (int64_t)(b0 + r) * ((in + 31) >> 5) + (c0 >> 5);
+#pragma unroll
+      for (int u = 0; u < XU; ++u) xv[u] = xrow[min((tid & 3) + 4 * u, xl - 1)];
+    }
+#pragma unroll
+    for (int u = 0; u < WU; ++u) ws[(tid >> 6) * CI + (tid & 63) + 64 * u] = wv[u];
+#pragma unroll
+    for (int u = 0; u < XU; ++u) xs[(tid >> 2) * XLD + (tid & 3) + 4 * u] = xv[u];
+    __syncthreads();
+    const float* wr = ws + wave * CI;
     if constexpr (X_BITS == 0) {
-      xv = static_cast<const float*>(xin)[(int64_t)b * in + i];
+      const float* xr = reinterpret_cast<const float*>(xs) + lane * FC_XLD;
+      const int L4 = L & ~3;
+#pragma unroll 4
+      for (int k = 0; k < L4; k += 4) {
+        const float4 xv = *reinterpret_cast<const float4*>(xr + k);
+        const float4 wv = *reinterpret_cast<const float4*>(wr + k);
+        acc = fmaf(xv.x, wv.x, acc);
+        acc = fmaf(xv.y, wv.y, acc);
+        acc = fmaf(xv.z, wv.z, acc);
+        acc = fmaf(xv.w, wv.w, acc);
+      }
+      for (int k = L4; k < L; ++k) acc = fmaf(xr[k], wr[k], acc);
     } else {
-      const uint32_t word = static_cast<const uint32_t*>(xin)[(int64_t)b * cwn + (i >> 5)];
-      xv = ((word >> (i & 31)) & 1u) ? 1.0f : -1.0f;
-    }
+      const uint32_t* xr = xs + lane * FC_XLD_BIN;
+      const int full = L >> 5;
+      for (int c = 0; c < full; ++c) {
+        const uint32_t neg = ~xr[c];  // bit set <=> input -1
 #pragma unroll
-    for (int j = 0; j < FC_TN; ++j) {
-      const int o = min(o0 + j, out - 1);
-      acc[j] = fmaf(xv, w[(int64_t)o * in + i], acc[j]);
+        for (int k0 = 0; k0 < 32; k0 += 4) {
+          const float4 wv = *reinterpret_cast<const float4*>(wr + 32 * c + k0);
+          const float wk[4] = {wv.x, wv.y, wv.z, wv.w};
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const uint32_t sgn = (neg << (31 - k0 - k)) & 0x80000000u;
+            acc = acc + __uint_as_float(__float_as_uint(wk[k]) ^ sgn);
+          }
+        }
+      }
+      if (L & 31) {
+        const uint32_t neg = ~xr[full];
+        for (int k = 0; k < (L & 31); ++k) {
+          const uint32_t sgn = (neg << (31 - k)) & 0x80000000u;
+          acc = acc + __uint_as_float(__float_as_uint(wr[32 * full + k]) ^ sgn);
+        }
+      }
     }
   }
-#pragma unroll
-  for (int j = 0; j < FC_TN; ++j) {
-    const int o = o0 + j;
-    if (o < out) y[(int64_t)b * out + o] = acc[j] + (bias ? bias[o] : 0.0f);
-  }
+  if (o < out && lane < nb) y[(int64_t)(b0 + lane) * out + o] = acc + (bias ? bias[oc] : 0.0f);
 }
 
 }  // namespace
@@ -210,11 +283,11 @@ int launch_avgpool_f32(const float* x, int n, int c, int h, int w, float* y, hip
 int launch_fc_f32(const void* x, int x_bits, int n, int in, const float* w, const float* bias,
                   int out, float* y, hipStream_t s) {
   if (n == 0) return QCONV_OK;
-  const dim3 grid((unsigned)ceil_div(n, 64), (unsigned)ceil_div(out, FC_TN));
+  const dim3 grid((unsigned)ceil_div(n, 64), (unsigned)ceil_div(out, 4));
   if (x_bits == 0)
-    fc_f32_kernel<0><<<grid, 64, 0, s>>>(x, n, in, w, bias, out, y);
+    fc_f32_kernel<0><<<grid, 256, 0, s>>>(x, n, in, w, bias, out, y);
   else
-    fc_f32_kernel<1><<<grid, 64, 0, s>>>(x, n, in, w, bias, out, y);
+    fc_f32_kernel<1><<<grid, 256, 0, s>>>(x, n, in, w, bias, out, y);
   return hip_status();
 }
 

@@ -97,6 +97,15 @@ def test_fold_bn_matches_oracle(oracle_mod):
     np.testing.assert_array_equal(b, bo)
 
 
+def test_pooled_resolution():
+    """AUTO takes the matrix cores for pooled layers whose windows fit one lane."""
+    fp4 = q.ALGO_MFMA_FP4
+    assert q.resolve_algo(2, 128, 32, 32, 128, 3, 1, 1, 1, 1, flags=q.EPI_POOL2) == fp4
+    assert q.resolve_algo(2, 128, 8, 8, 128, 3, 1, 1, 1, 1, flags=q.EPI_POOL2) == fp4
+    assert q.resolve_algo(2, 128, 9, 9, 128, 3, 1, 1, 1, 1, flags=q.EPI_POOL2) == q.ALGO_BITPLANE
+    assert q.resolve_algo(2, 128, 8, 128, 128, 3, 1, 1, 1, 1, flags=q.EPI_POOL2) == q.ALGO_BITPLANE
+
+
 FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails validation first
 
 

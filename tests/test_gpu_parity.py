@@ -219,6 +219,72 @@ def test_bn_residual_and_repack(dev, bits, algo, hw):
                                   oracle.quantize(oracle.hardtanh(zz), ab))
 
 
+POOL_CASES = [
+    # n, cin, h, w, cout, k, stride, pad -- conv output widths 8, 16, 32, 64
+    (3, 40, 8, 8, 70, 3, 1, 1),     # wo 8, two whole images per block, last block half empty
+    (1, 32, 9, 8, 33, 3, 1, 1),     # wo 8, odd conv rows: the last one has no pooled row
+    (2, 32, 10, 8, 32, 3, 1, 1),    # wo 8, 80-pixel images (one block each)
+    (2, 33, 4, 16, 40, 3, 1, 1),    # wo 16, 64-pixel images, two per block
+    (2, 64, 16, 16, 96, 3, 1, 1),   # wo 16, two blocks per image
+    (1, 64, 32, 32, 128, 3, 1, 1),  # wo 32
+    (2, 32, 7, 32, 64, 3, 1, 1),    # wo 32, odd conv rows
+    (3, 64, 2, 32, 64, 3, 1, 1),    # wo 32, 2-row images, two per block
+    (2, 64, 64, 64, 64, 3, 2, 1),   # wo 32 after stride 2
+    (1, 32, 6, 64, 33, 3, 1, 1),    # wo 64: interleaved M-tiles
+    (2, 32, 7, 8, 32, 3, 1, 1),     # wo 8 with odd rows and two images per block: bit-serial only
+    (2, 40, 10, 9, 70, 3, 1, 1),    # odd width: bit-serial only
+]
+POOL_ALGOS = dict(ALGOS, auto=q.ALGO_AUTO)
+
+
+@pytest.mark.parametrize("algo", list(POOL_ALGOS))
+@pytest.mark.parametrize("case", POOL_CASES)
+def test_pooled_conv_int32(dev, case, algo):
+    """2x2 max pooling of the integer accumulator, every pairing of the M-tiles."""
+    n, cin, h, w, cout, k, s, p = case
+    for ab, wb in [(1, 1), (2, 2), (3, 1)]:
+        x, wt = _inputs(300 + sum(case) + ab, n, cin, h, w, cout, k)
+        out, _, _ = _run_or_skip(lambda: _gpu_conv(dev, x, wt, ab, wb, s, p, algo=POOL_ALGOS[algo],
+                                                   flags=q.EPI_POOL2))
+        acc, _ = _oracle_acc(x, wt, ab, wb, s, p)
+        np.testing.assert_array_equal(out.cpu().numpy(), oracle.maxpool2_int(acc), err_msg=str((ab, wb)))
+
+
+@pytest.mark.parametrize("algo", list(POOL_ALGOS))
+@pytest.mark.parametrize("case", POOL_CASES)
+def test_pooled_conv_bn_pack_and_residual(dev, case, algo):
+    """{QConv-pool-BN-HardTanh-quantize} packed; and pool-BN + residual -> fp32 + repack."""
+    n, cin, h, w, cout, k, s, p = case
+    ab, wb = 1, 2
+    x, wt = _inputs(400 + sum(case), n, cin, h, w, cout, k)
+    kk, bb = _bn(400 + sum(case), cout)
+    acc, _ = _oracle_acc(x, wt, ab, wb, s, p)
+    acc = oracle.maxpool2_int(acc)
+    ho, wo = acc.shape[2], acc.shape[3]
+    shift = oracle.level_shift(ab) + oracle.level_shift(wb)
+    z = oracle.epi_bn(acc, kk.numpy(), bb.numpy(), shift)
+    for out_bits in (1, 2):
+        _, outp, _ = _run_or_skip(lambda: _gpu_conv(dev, x, wt, ab, wb, s, p, algo=POOL_ALGOS[algo],
+                                                    mode=q.EPI_BN_PACK, flags=q.EPI_POOL2, bn_k=kk.to(dev),
+                                                    bn_b=bb.to(dev), out_bits=out_bits))
+        got = unpack_act(outp.cpu().numpy(), n, cout, ho, wo, out_bits)
+        np.testing.assert_array_equal(got, oracle.quantize(oracle.hardtanh(z), out_bits))
+        assert tail_bits_zero(outp.cpu().numpy(), cout, out_bits)
+    res = synth.normal(synth.generator(401), (n, cout, ho, wo), 1.0)
+    act = q.pack_act(x.to(dev), ab)
+    wq, _ = q.pack_weight(wt.to(dev), wb)
+    outp = torch.empty(q.packed_act_words(n, cout, ho, wo, 2), dtype=torch.int32, device=dev)
+    out, _ = _run_or_skip(lambda: q.conv(act, wq, n, cin, h, w, cout, k, s, p, ab, wb, mode=q.EPI_BN_F32,
+                                         flags=q.EPI_POOL2 | q.EPI_RESIDUAL, bn_k=kk.to(dev), bn_b=bb.to(dev),
+                                         residual=res.to(dev), out_bits=2, out_packed=outp,
+                                         algo=POOL_ALGOS[algo]))
+    torch.cuda.synchronize()
+    zz = oracle.add(z, res.numpy())
+    np.testing.assert_array_equal(out.cpu().numpy(), zz)
+    np.testing.assert_array_equal(unpack_act(outp.cpu().numpy(), n, cout, ho, wo, 2),
+                                  oracle.quantize(oracle.hardtanh(zz), 2))
+
+
 def test_empty_batch_is_a_no_op(dev):
     x = torch.zeros((0, 32, 4, 4), device=dev)
     act = q.pack_act(x, 1)
@@ -394,3 +460,80 @@ def test_resnet18_full_batch_rows(dev):
     sub["x"] = p["x"][rows]
     want = oracle.resnet18_forward(sub, 2, 2)
     np.testing.assert_array_equal(logits[rows], want)
+
+
+# ---------------------------------------------------------------------------
+# fp32 support layers through small qnet graphs
+# ---------------------------------------------------------------------------
+
+def _run_net(dev, net, x, out_features):
+    ws = torch.empty(max(net.workspace_bytes(x.shape[0]), 1), dtype=torch.uint8, device=dev)
+    logits = torch.empty((x.shape[0], out_features), dtype=torch.float32, device=dev)
+    net.forward(x.to(dev), logits, ws)
+    torch.cuda.synchronize()
+    return logits.cpu().numpy()
+
+
+@pytest.mark.parametrize("n,c,h,w,out,bias", [
+    (1, 5, 1, 1, 1, True),        # single image, tiny
+    (3, 7, 3, 3, 10, False),      # in = 63 (not a multiple of 4), no bias
+    (70, 512, 1, 1, 1000, True),  # ResNet head: two image groups, ragged last group
+    (65, 200, 1, 1, 13, True),    # in spans two chunks with a ragged one
+    (2, 100, 2, 2, 5, True),      # in = 400: two full chunks + 16
+])
+def test_fc_f32_fp32_input(dev, n, c, h, w, out, bias):
+    g = synth.generator(500 + n + c + out)
+    x = synth.normal(g, (n, c, h, w), 1.0)
+    wt = synth.normal(g, (out, c * h * w), 2.0 / (c * h * w))
+    b = synth.normal(g, (out,), 0.1) if bias else None
+    net = q.Net(c, h, w)
+    net.fc_f32(0, wt.to(dev), b.to(dev) if bias else None)
+    got = _run_net(dev, net, x, out)
+    want = oracle.fc_f32(x.numpy().reshape(n, -1), wt.numpy(), b.numpy() if bias else None)
+    np.testing.assert_array_equal(got, want)
+
+
+@pytest.mark.parametrize("n,c,out", [(256, 1024, 10), (3, 33, 7), (64, 2049, 5), (1, 32, 1), (130, 64, 9)])
+def test_fc_f32_binary_input(dev, n, c, out):
+    """FC over a packed {-1,+1} vector (ConvNet head); inputs span whole and ragged words and chunks."""
+    g = synth.generator(600 + n + c + out)
+    x = synth.normal(g, (n, c, 1, 1), 1.0)
+    wt = synth.normal(g, (out, c), 2.0 / c)
+    b = synth.normal(g, (out,), 0.1)
+    net = q.Net(c, 1, 1)
+    t = net.quantize(0, 1)
+    net.fc_f32(t, wt.to(dev), b.to(dev))
+    got = _run_net(dev, net, x, out)
+    lv = oracle.quantize(x.numpy(), 1).astype(np.float32).reshape(n, c)
+    np.testing.assert_array_equal(got, oracle.fc_f32(lv, wt.numpy(), b.numpy()))
+
+
+@pytest.mark.parametrize("n,cin,hw,cout,k,s,p", [(2, 3, 32, 128, 3, 1, 1), (1, 3, 37, 64, 7, 2, 3), (3, 5, 9, 40, 3, 2, 0)])
+def test_conv_f32_pools_and_head(dev, n, cin, hw, cout, k, s, p):
+    """fp32 conv -> BN -> ReLU -> max pool 3x3/2 -> avg pool -> FC, layer by layer."""
+    g = synth.generator(700 + hw + cout)
+    x = synth.normal(g, (n, cin, hw, hw), 1.0)
+    wt = synth.normal(g, (cout, cin, k, k), 2.0 / (cin * k * k))
+    kk, bb = _bn(700 + hw, cout)
+    fw = synth.normal(g, (11, cout), 2.0 / cout)
+    net = q.Net(cin, hw, hw)
+    t1 = net.conv_f32(0, wt.to(dev), kk.to(dev), bb.to(dev), stride=s, pad=p, relu=True)
+    t2 = net.maxpool_f32(t1, 3, 2, 1)
+    t3 = net.avgpool(t2)
+    net.fc_f32(t3, fw.to(dev))
+    ws = torch.empty(max(net.workspace_bytes(n), 1), dtype=torch.uint8, device=dev)
+    logits = torch.empty((n, 11), dtype=torch.float32, device=dev)
+    net.forward(x.to(dev), logits, ws)
+    torch.cuda.synchronize()
+
+    def view(tid):
+        c, h, w, bits, off = net.tensor_info(tid, n)
+        return ws[off:off + 4 * n * c * h * w].view(torch.float32).view(n, c, h, w).cpu().numpy()
+
+    y = oracle.conv_f32(x.numpy(), wt.numpy(), s, p)
+    z = oracle.relu(oracle.bn_f32(y, kk.numpy(), bb.numpy()))
+    np.testing.assert_array_equal(view(t1), z)
+    mp = oracle.maxpool_f32(z, 3, 2, 1)
+    np.testing.assert_array_equal(view(t2), mp)
+    ap = oracle.avgpool_f32(mp)
+    np.testing.assert_array_equal(logits.cpu().numpy(), oracle.fc_f32(ap, fw.numpy()))
