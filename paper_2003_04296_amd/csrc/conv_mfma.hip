@@ -1,25 +1,35 @@
-// conv_mfma.hip -- the same layer product (Algorithm 1, inference branch) on
-// the gfx950 matrix cores.  The level codes of both operands ({-1,+1},
+// conv_mfma.hip -- the layer product of Algorithm 1 (inference branch) on the
+// gfx950 matrix cores.  The level codes of both operands ({-1,+1},
 // {-1,0,+1}, {0,+-1,+-2,+-4}) are exact as int8 and as E2M1 (fp4), and every
 // partial sum is an integer below 2^24, so both
 //   v_mfma_i32_32x32x32_i8            (int32 accumulate) and
 //   v_mfma_scale_f32_32x32x64_f8f6f4  (fp4 operands, unit scales, fp32 accumulate)
 // give the exact integer accumulator of the bitplane kernel.
 //
-// Tiling: a block (4 waves, 2 x 2) owns 2 * MTW M-tiles of 32 output pixels
-// and 64 * NTW output channels (2 * NTW N-tiles of 32); a wave owns MTW
-// M-tiles x NTW N-tiles of 32 x 32 accumulators (MTW = 2: 128-pixel blocks,
-// three waves per SIMD, so one block's stores overlap other blocks' MFMAs).  The block's input rows plus halo
-// are expanded once per channel chunk from the packed bitplanes into LDS
-// (int8: 4 words = 128 bytes per pixel, fp4: 8 words = 128 bytes, + 16 bytes
-// of padding so that 16-byte fragment reads of neighbouring pixels fall in
-// different banks).  Each expanded value then feeds every tap and every
-// output channel of the block.  The weights were expanded once at packing
-// time into the same operand format; a lane reads its 16-byte B fragment
-// straight from global memory (L2-resident, shared by all blocks).
-// The epilogue reads the accumulator layout (register v of lane l holds row
-// 8(v/4) + 4(l/32) + v%4, column l%32) and packs requantized outputs with one
-// wave ballot per plane: 32 channels of a pixel become one word.
+// Work unit.  The block's M dimension is a list of "units": output pixels, or
+// with 2x2 pooling whole pooling windows (the pooled output pixels), each of
+// which occupies four consecutive M rows.  A block owns a run of units of one
+// image, or several whole images, and 32 * NT * WN output channels.
+//
+// Tiling.  4 waves in a WM x WN grid; a wave owns MT x NT tiles of 32 x 32
+// accumulators.  The block's input rows plus halo are expanded once per
+// channel chunk from the packed bitplanes into LDS (int8: 32 bytes per 32
+// channels, fp4: 16 bytes; + 16 bytes of padding per pixel, so that 16-byte
+// fragment reads of neighbouring pixels fall in different banks).  Each
+// expanded value then feeds every tap and every output channel of the block.
+// The weights were expanded at packing time into the same operand format; a
+// lane reads its 16-byte B fragment from global memory (L2-resident) through
+// a buffer resource, two k-steps ahead of its use.
+//
+// Epilogue.  Register v of lane l holds M row 8(v/4) + 4(l/32) + v%4 and
+// output channel l%32.  Row r of an M-tile is unit r for plain convolutions,
+// so a lane's registers 4q..4q+3 are four consecutive pixels of one channel
+// (one 16-byte NCHW store).  With pooling, row r is element r%4 of window
+// 4((r/4)%2) + r/8, so registers 4q..4q+3 are the four pixels of one window
+// and a lane ends with four consecutive pooled pixels.  Packed outputs are
+// built with one wave ballot per (register, plane): lanes 0-31 give the 32
+// channels of one pixel, lanes 32-63 those of another, and the words are
+// moved into lanes with writelane so that each lane stores one pixel's word.
 #include <string.h>
 
 #include <type_traits>
@@ -35,22 +45,33 @@ typedef int v8i __attribute__((ext_vector_type(8)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 
-#ifndef QC_MFMA_MTW
-#define QC_MFMA_MTW 2
+constexpr int MAX_LDS = 38 * 1024;  // one halo buffer (two per block, two blocks per CU)
+#ifndef QC_BRING
+#define QC_BRING 2  // weight-fragment register sets in flight
 #endif
-constexpr int MTW = QC_MFMA_MTW;       // M-tiles (of 32 pixels) per wave
-constexpr int BLOCK_PIX = 2 * MTW * 32;  // 2 waves along M
-#ifndef QC_MFMA_WPE
-#define QC_MFMA_WPE 3
-#endif
-constexpr int MAX_LDS = 64 * 1024;
+// Packed words of the next stage held per thread in registers (bounded by
+// the registers left next to the accumulators); items past 256 times this
+// are loaded when the stage is expanded.
+__host__ __device__ constexpr int halo_items_per_thread(int planes) { return planes == 1 ? 4 : 8 / planes; }  // one halo buffer (two per block, two blocks per CU)
 
+// n / d by a multiply-high, exact whenever n * d < 2^32 (checked on the host
+// against the largest dividend of each use).
+struct FastDiv {
+  uint32_t d, m;
+};
+FastDiv make_fastdiv(uint32_t d) {
+  FastDiv f;
+  f.d = d;
+  f.m = d <= 1 ? 0u : (uint32_t)(0xFFFFFFFFu / d + 1u);
+  return f;
+}
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv f) { return f.m ? __umulhi(n, f.m) : n; }
 
 template <int FP4>
 struct OpT;
 template <>
 struct OpT<0> {
-  static constexpr int CHUNK_WORDS = 4;  // words of 32 channels staged per chunk
+  static constexpr int CHUNK_WORDS = 4;  // 32-channel words staged per chunk
   static constexpr int WORD_BYTES = 32;  // LDS bytes per word per pixel
   static constexpr int WORDS_PER_STEP = 1;
   using acc_t = v16i;
@@ -63,23 +84,53 @@ struct OpT<1> {
   using acc_t = v16f;
 };
 
+// Block shapes: WM x WN x SK waves (SK: waves splitting the K range of the
+// same output tile, their partial tiles summed through LDS), each owning
+// MT x NT tiles of 32 x 32 accumulators.
+template <int CFG>
+struct Cfg;
+template <>
+struct Cfg<0> {  // 256 rows x 128 channels
+  static constexpr int WM = 2, WN = 2, SK = 1, MT = 4, NT = 2;
+};
+template <>
+struct Cfg<1> {  // 256 rows x 64 channels (layers with <= 64 output channels)
+  static constexpr int WM = 4, WN = 1, SK = 1, MT = 2, NT = 2;
+};
+template <>
+struct Cfg<2> {  // 64 rows x 64 channels, K split over the four waves (small layers)
+  static constexpr int WM = 1, WN = 1, SK = 4, MT = 2, NT = 2;
+};
+inline int cfg_rows(int cfg) { return cfg == 2 ? 64 : 256; }
+inline int cfg_block_co(int cfg) { return cfg == 0 ? 128 : 64; }
+constexpr int PARAM_BYTES = 2 * 128 * 4;  // per-channel epilogue parameters of the block, in LDS
+constexpr int RED_BYTES = 4 * 4 * 16 * 64 * 4;  // split-K partial tiles: 4 waves x 4 tiles
+
 struct MfmaArgs {
   ConvArgs c;
-  const uint8_t* wx;    // expanded weights in the chosen operand format
-  int wx_bytes;         // size of that operand copy (bounds of the B buffer reads)
-  int ipb;              // whole images per block (1: the block is a pixel range of one image)
-  int blocks_per_img;   // ipb == 1: blocks per image
-  int hr, hc;           // halo rows / cols per image slot
-  int pix_bytes;        // LDS bytes per halo pixel (chunk words * WORD_BYTES + 16)
-  int chunk_words;      // words staged per chunk
-  int ksteps;           // k-steps per tap over all words (int8: cw, fp4: ceil(cw/2))
+  const uint8_t* wx;  // expanded weights in the chosen operand format
+  int wx_bytes;       // size of that operand copy (bounds of the B buffer reads)
+  int pool;           // units are 2x2 windows
+  int upi;            // units per image
+  int uw;             // units per output row
+  FastDiv fd_upi, fd_uw;
+  int ipb;            // whole images per block (1: the block is a run of units of one image)
+  int bpi;            // ipb == 1: blocks per image
+  int units_pb;       // units per block
+  int hr, hc;         // halo rows / cols per image slot
+  int slot_pix;       // hr * hc
+  FastDiv fd_slot, fd_hc, fd_cwc;
+  int pix_bytes;      // LDS bytes per halo pixel
+  int chunk_words;    // words staged per chunk
+  int ksteps;         // k-steps per tap over all words (int8: cw, fp4: ceil(cw/2))
   int nchunks;
-  int vec_store;        // ho*wo % 4 == 0: 4 consecutive pixels are one aligned 16-byte run
-  int tiles_px;         // pixel tiles (blocks of BLOCK_PIX pixels or ipb images)
-  int tiles_co;         // output-channel tiles (64 * NTW channels)
-  int halo_bytes;       // LDS bytes of the halo tile (reused as the output stage)
-  int pool_wo;          // 2x2 max pooling: the conv output width (8, 16, 32 or 64), else 0
-  int mt_interleave;    // wave wm owns M-tiles wm, wm + 2, ... instead of a contiguous run
+  int vec;            // upi % 4 == 0: four consecutive units are one aligned 16-byte run
+  int tiles_px, tiles_co;
+  int halo_bytes;
+  int ht_needed;      // requantization thresholds reach 1: apply HardTanh before comparing
+  int out_bytes;      // byte size of the unpacked output (buffer-resource bound, < 2^31)
+  int buf_bytes;      // LDS bytes of one halo buffer
+  int grid;           // blocks launched (each loops over the work items)
 };
 
 __device__ __forceinline__ v16i mfma(v4i a, v4i b, v16i c) {
@@ -91,8 +142,11 @@ __device__ __forceinline__ v16f mfma(v4i a, v4i b, v16f c) {
   // operand format 4 = E2M1 for both; scales 127 = 2^0
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, c, 4, 4, 0, 127, 0, 127);
 }
-__device__ __forceinline__ int acc_value(const v16i& a, int v) { return a[v]; }
-__device__ __forceinline__ int acc_value(const v16f& a, int v) { return (int)a[v]; }
+// Accumulator register as an exact float / int.
+__device__ __forceinline__ float acc_f(const v16i& a, int v) { return (float)a[v]; }
+__device__ __forceinline__ float acc_f(const v16f& a, int v) { return a[v]; }
+__device__ __forceinline__ int acc_i(const v16i& a, int v) { return a[v]; }
+__device__ __forceinline__ int acc_i(const v16f& a, int v) { return (int)a[v]; }
 
 template <int FP4, int PA>
 __device__ __forceinline__ void expand_to_lds(const uint32_t* pl, uint8_t* dst) {
@@ -108,14 +162,8 @@ __device__ __forceinline__ void expand_to_lds(const uint32_t* pl, uint8_t* dst) 
   }
 }
 
-__device__ __forceinline__ uint32_t quant_rt(float z, int bits, Thr t) {
-  if (bits == 1) return quant_planes<1>(z, t);
-  if (bits == 2) return quant_planes<2>(z, t);
-  return quant_planes<3>(z, t);
-}
-
 // Compile-time loop: f(integral_constant<I>) for I in [B, E), so that the
-// accumulator tiles are only ever indexed with constants (no scratch copy).
+// accumulator tiles are only ever indexed with constants.
 template <int B, int E>
 struct Unroll {
   template <class F>
@@ -130,406 +178,743 @@ struct Unroll<E, E> {
   __device__ __forceinline__ static void run(F&&) {}
 };
 
-struct EpiCtx {
-  int img0, p0, co_blk, hwo, lane;
-};
-
-constexpr int STAGE_LD = 36;                      // floats per staged channel row (32 + 4 pad)
-constexpr int STAGE_BYTES = 32 * STAGE_LD * 4;    // one 32 x 32 tile per wave
-
-// Image and pixel of block pixel t; false past the end of the block's work.
-__device__ __forceinline__ bool block_pixel(const MfmaArgs& m, const EpiCtx& x, int t, int* img,
-                                            int* pp) {
-  int slot;
-  if (m.ipb == 1) {
-    slot = 0;
-    *pp = x.p0 + t;
-    if (*pp >= x.hwo) return false;
+// Ballots of the bitplanes of Q(HardTanh(z)) over the wave (Eqs. 4, 21, 22):
+// the same compares as the quantizer, one ballot each, combined with scalar
+// bit operations.  `ok` = the lane's channel and unit exist.
+template <int OB>
+__device__ __forceinline__ void plane_ballots(float z, bool ok, Thr t, uint64_t* b) {
+  if constexpr (OB == 1) {
+    b[0] = __ballot(ok & (z > 0.0f));
+  } else if constexpr (OB == 2) {
+    const uint64_t nz = __ballot(ok & !(fabsf(z) <= t.t0));
+    const uint64_t s = __ballot(ok & (z > 0.0f));
+    b[0] = s & nz;
+    b[1] = nz;
   } else {
-    slot = t / x.hwo;
-    *pp = t - slot * x.hwo;
-    if (slot >= m.ipb || x.img0 + slot >= m.c.n) return false;
+    const float az = fabsf(z);
+    const uint64_t a1 = __ballot(ok & !(az <= t.t0));
+    const uint64_t a2 = __ballot(ok & !(az <= t.t1));
+    const uint64_t a3 = __ballot(ok & !(az <= t.t2));
+    const uint64_t s = __ballot(ok & (z > 0.0f));
+    b[0] = s & a1;
+    b[1] = a3;
+    b[2] = a2 & ~a3;
+    b[3] = a1 & ~a2;
   }
-  *img = x.img0 + slot;
-  return true;
 }
 
-// Flat NCHW index of block pixel t for channel co, or -1 past the end.
-__device__ __forceinline__ int64_t out_index(const MfmaArgs& m, const EpiCtx& x, int t, int co) {
-  int img, pp;
-  if (!block_pixel(m, x, t, &img, &pp)) return -1;
-  return ((int64_t)img * m.c.cout + co) * x.hwo + pp;
+// Eight v_writelane_b32: lanes L0..L3 of w take lo0..lo3, lanes H0..H3 take
+// hi0..hi3 (wave-uniform values).  The lanes are inline constants, so the
+// value is the instruction's only scalar operand.  The values usually come
+// straight from a VALU compare; s_nop 4 provides the wait states a VALU
+// write of an SGPR needs before v_writelane reads it, which the compiler does
+// not insert across inline assembly.
+template <int L0, int L1, int L2, int L3, int H0, int H1, int H2, int H3>
+__device__ __forceinline__ uint32_t writelanes8(uint32_t w, uint32_t lo0, uint32_t lo1, uint32_t lo2,
+                                                uint32_t lo3, uint32_t hi0, uint32_t hi1, uint32_t hi2,
+                                                uint32_t hi3) {
+  asm("s_nop 4\n\t"
+      "v_writelane_b32 %0, %1, %9\n\t"
+      "v_writelane_b32 %0, %2, %10\n\t"
+      "v_writelane_b32 %0, %3, %11\n\t"
+      "v_writelane_b32 %0, %4, %12\n\t"
+      "v_writelane_b32 %0, %5, %13\n\t"
+      "v_writelane_b32 %0, %6, %14\n\t"
+      "v_writelane_b32 %0, %7, %15\n\t"
+      "v_writelane_b32 %0, %8, %16"
+      : "+v"(w)
+      : "s"(lo0), "s"(lo1), "s"(lo2), "s"(lo3), "s"(hi0), "s"(hi1), "s"(hi2), "s"(hi3), "i"(L0), "i"(L1),
+        "i"(L2), "i"(L3), "i"(H0), "i"(H1), "i"(H2), "i"(H3));
+  return w;
 }
 
-// Epilogue of one 32 x 32 accumulator tile: block pixels [32 mt, 32 mt + 32)
-// x output channels [c32, c32 + 32).  Unpacked outputs go through the wave's
-// LDS stage so that every store instruction writes whole 128-byte runs of
-// one channel's pixels; packed outputs are assembled with ballots.
-template <class AccT>
-__device__ __forceinline__ void store_tile(const MfmaArgs& m, const EpiCtx& x, const AccT& acc,
-                                           int mt, int c32, float* stage) {
+template <int P>
+__device__ __forceinline__ void store_words(uint32_t* dst, const uint32_t* w) {
+  if constexpr (P == 1)
+    *dst = w[0];
+  else if constexpr (P == 2)
+    *reinterpret_cast<uint2*>(dst) = make_uint2(w[0], w[1]);
+  else
+    *reinterpret_cast<uint4*>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// Image and in-image unit of block unit t; false past the end of the block's work.
+__device__ __forceinline__ bool unit_of(const MfmaArgs& m, int img0, int u0, int t, int* img, int* uu) {
+  if (m.ipb == 1) {
+    *img = img0;
+    *uu = u0 + t;
+    return *uu < m.upi;
+  }
+  const int slot = (int)fdiv((uint32_t)t, m.fd_upi);
+  *img = img0 + slot;
+  *uu = t - slot * m.upi;
+  return (slot < m.ipb) & (*img < m.c.n);
+}
+
+enum EpiKind { K_INT32 = 0, K_SCALE = 1, K_BNF32 = 2, K_PACK = 3 };
+
+// Epilogue of one 32 x 32 accumulator tile: M-tile T of the block (units
+// 32T.. or, pooled, windows 8T..) x output channels co32 .. co32 + 31.
+// KIND: what the unpacked output holds; OB: bits of the packed output
+// (0 = none); POOL: units are 2x2 windows.
+template <int KIND, int OB, int POOL, class AccT>
+__device__ __forceinline__ void tile_epilogue(const MfmaArgs& m, const AccT& acc, int img0, int u0,
+                                              int T, int co32, float kk, float bb, int lane) {
   const ConvArgs& a = m.c;
-  const int g = x.lane >> 5, r32 = x.lane & 31;
+  constexpr int POUT = OB ? planes_of(OB) : 1;
+  const int g = lane >> 5, r32 = lane & 31;
   const float inv = 1.0f / (float)(1 << a.shift);
-  const bool pack = a.out_packed != nullptr && c32 < a.cout;  // uniform
-  const int co = c32 + r32;
-  const bool co_ok = co < a.cout;
-  const int cs = min(co, a.cout - 1);
-  float kk = 0.0f, bb = 0.0f, ss = 0.0f;
-  if (a.mode == QCONV_EPI_BN_F32 || a.mode == QCONV_EPI_BN_PACK) {
-    kk = a.bn_k[cs];
-    bb = a.bn_b[cs];
-  } else if (a.mode == QCONV_EPI_SCALE_F32) {
-    ss = a.scale[cs];
-  }
-  // value of register v before any residual: int32 accumulator (INT32 mode)
-  // or the fp32 scale / BN result, bit-cast into the stage
-  auto value_bits = [&](int v) -> uint32_t {
-    const int av = acc_value(acc, v);
-    if (a.mode == QCONV_EPI_INT32) return (uint32_t)av;
-    const float ar = (float)av * inv;
-    const float z = (a.mode == QCONV_EPI_SCALE_F32) ? ss * ar : fmaf(kk, ar, bb);
-    return __float_as_uint(z);
-  };
+  const int co = co32 + r32;
+  const bool cok = co < a.cout;
+  const int64_t oplane = (int64_t)m.upi;  // NCHW channel-plane stride of the output
+  uint32_t pw[POUT];  // packed words of this tile, gathered into lanes
+#pragma unroll
+  for (int p = 0; p < POUT; ++p) pw[p] = 0u;
 
-  if (a.mode != QCONV_EPI_BN_PACK && c32 < a.cout) {
-    // stage: lane (column r32, half g) holds rows 8q + 4g + i, i = 0..3
+  constexpr int NQ = POOL ? 1 : 4;  // 16-byte groups per lane: 4 plain, 1 pooled
+  Unroll<0, NQ>::run([&](auto QI) {
+    constexpr int QQ = decltype(QI)::value;
+    // the lane's four consecutive units
+    const int t0 = POOL ? 8 * T + 4 * g : 32 * T + 8 * QQ + 4 * g;
+    int img, uu;
+    const bool ok0 = unit_of(m, img0, u0, t0, &img, &uu);
+    float z[4];
+    int zi[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint4 w4 = make_uint4(value_bits(4 * q), value_bits(4 * q + 1), value_bits(4 * q + 2),
-                                  value_bits(4 * q + 3));
-      *reinterpret_cast<uint4*>(stage + r32 * STAGE_LD + 8 * q + 4 * g) = w4;
-    }
-    // read back: lane l takes channel 8k + l/8, pixels 4(l%8) .. 4(l%8)+3
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int cl = 8 * k + (x.lane >> 3);
-      const int px = 4 * (x.lane & 7);
-      const uint4 w4 = *reinterpret_cast<const uint4*>(stage + cl * STAGE_LD + px);
-      const int c = c32 + cl;
-      if (c >= a.cout) continue;
-      const int t = 32 * mt + px;
-      const int64_t i0 = out_index(m, x, t, c);
-      uint32_t w[4] = {w4.x, w4.y, w4.z, w4.w};
-      if (m.vec_store && i0 >= 0) {
-        // ho*wo % 4 == 0: the four pixels are one aligned 16-byte run of one image
-        if (a.residual_on) {
-          const float4 rv = *reinterpret_cast<const float4*>(a.residual + i0);
-          w[0] = __float_as_uint(__uint_as_float(w[0]) + rv.x);
-          w[1] = __float_as_uint(__uint_as_float(w[1]) + rv.y);
-          w[2] = __float_as_uint(__uint_as_float(w[2]) + rv.z);
-          w[3] = __float_as_uint(__uint_as_float(w[3]) + rv.w);
-        }
-        *reinterpret_cast<uint4*>(static_cast<uint32_t*>(a.out) + i0) = make_uint4(w[0], w[1], w[2], w[3]);
+    for (int i = 0; i < 4; ++i) {
+      if constexpr (POOL) {
+        // window i: registers 4i .. 4i + 3
+        const float m4 = fmaxf(fmaxf(acc_f(acc, 4 * i), acc_f(acc, 4 * i + 1)),
+                               fmaxf(acc_f(acc, 4 * i + 2), acc_f(acc, 4 * i + 3)));
+        zi[i] = (int)m4;
+        z[i] = m4 * inv;
       } else {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int64_t ie = out_index(m, x, t + e, c);
-          if (ie < 0) continue;
-          uint32_t we = w[e];
-          if (a.residual_on) we = __float_as_uint(__uint_as_float(we) + a.residual[ie]);
-          static_cast<uint32_t*>(a.out)[ie] = we;
-        }
+        zi[i] = acc_i(acc, 4 * QQ + i);
+        z[i] = acc_f(acc, 4 * QQ + i) * inv;
       }
+      if constexpr (KIND == K_SCALE) z[i] = kk * z[i];
+      if constexpr (KIND == K_BNF32 || KIND == K_PACK) z[i] = fmaf(kk, z[i], bb);
     }
-  }
-
-  if (pack) {
-    // one ballot per (pixel row, plane): lanes 0-31 hold the 32 channels of
-    // row t + e (g = 0), lanes 32-63 those of row t + 4 + e (g = 1)
-    const int pout = planes_of(a.out_bits);
-    const int cword = c32 >> 5;
-#pragma unroll
-    for (int v4 = 0; v4 < 16; v4 += 4) {
-      const int t = 32 * mt + 8 * (v4 >> 2) + 4 * g;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int64_t ie = out_index(m, x, t + e, cs);
-        float z = __uint_as_float(value_bits(v4 + e));
-        if (a.residual_on && ie >= 0) z = z + a.residual[ie];
-        const uint32_t pl = (co_ok && ie >= 0) ? quant_rt(hardtanh(z), a.out_bits, a.othr) : 0u;
-        int img, pp;
-        const bool pix_ok = block_pixel(m, x, t + e, &img, &pp);
-        for (int p = 0; p < pout; ++p) {
-          const uint64_t bal = __ballot((pl >> p) & 1u);
-          if (r32 == 0 && pix_ok) {
-            const uint32_t word = g ? (uint32_t)(bal >> 32) : (uint32_t)bal;
-            a.out_packed[(((int64_t)img * x.hwo + pp) * a.out_cw + cword) * pout + p] = word;
+    // unpacked output (+ residual)
+    if constexpr (KIND != K_PACK) {
+      if (m.vec) {
+        if (ok0 && cok) {
+          const int64_t oi = ((int64_t)img * a.cout + co) * oplane + uu;
+          if constexpr (KIND == K_BNF32) {
+            if (a.residual_on) {
+              const float4 rv = *reinterpret_cast<const float4*>(a.residual + oi);
+              z[0] = z[0] + rv.x;
+              z[1] = z[1] + rv.y;
+              z[2] = z[2] + rv.z;
+              z[3] = z[3] + rv.w;
+            }
+          }
+          if constexpr (KIND == K_INT32)
+            *reinterpret_cast<int4*>(static_cast<int32_t*>(a.out) + oi) = make_int4(zi[0], zi[1], zi[2], zi[3]);
+          else
+            *reinterpret_cast<float4*>(static_cast<float*>(a.out) + oi) = make_float4(z[0], z[1], z[2], z[3]);
+        }
+      } else {
+        for (int i = 0; i < 4; ++i) {
+          int im, ui;
+          if (!unit_of(m, img0, u0, t0 + i, &im, &ui) || !cok) continue;
+          const int64_t oi = ((int64_t)im * a.cout + co) * oplane + ui;
+          float zv = z[0];
+          int ziv = zi[0];
+          if (i == 1) { zv = z[1]; ziv = zi[1]; }
+          if (i == 2) { zv = z[2]; ziv = zi[2]; }
+          if (i == 3) { zv = z[3]; ziv = zi[3]; }
+          if constexpr (KIND == K_BNF32) {
+            if (a.residual_on) zv = zv + a.residual[oi];
+          }
+          if constexpr (KIND == K_INT32)
+            static_cast<int32_t*>(a.out)[oi] = ziv;
+          else
+            static_cast<float*>(a.out)[oi] = zv;
+          if constexpr (OB > 0) {
+            if (i == 0) z[0] = zv;
+            if (i == 1) z[1] = zv;
+            if (i == 2) z[2] = zv;
+            if (i == 3) z[3] = zv;
           }
         }
       }
     }
+    // packed output: one ballot per (unit, plane); lanes 0-31 hold unit
+    // t0 + i of half g = 0, lanes 32-63 that of half g = 1
+    if constexpr (OB > 0) {
+      uint64_t bl[4][POUT];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float zz = z[i];
+        if (m.ht_needed) zz = hardtanh(zz);
+        int im, ui;
+        const bool uok = unit_of(m, img0, u0, t0 + i, &im, &ui);
+        plane_ballots<OB>(zz, uok & cok, a.othr, bl[i]);
+      }
+      constexpr int B = POOL ? 0 : 8 * QQ;
+#pragma unroll
+      for (int p = 0; p < POUT; ++p)
+        pw[p] = writelanes8<B, B + 1, B + 2, B + 3, B + 4, B + 5, B + 6, B + 7>(
+            pw[p], (uint32_t)bl[0][p], (uint32_t)bl[1][p], (uint32_t)bl[2][p], (uint32_t)bl[3][p],
+            (uint32_t)(bl[0][p] >> 32), (uint32_t)(bl[1][p] >> 32), (uint32_t)(bl[2][p] >> 32),
+            (uint32_t)(bl[3][p] >> 32));
+    }
+  });
+  if constexpr (OB > 0) {
+    // lane L < (POOL ? 8 : 32) stores the words of tile unit L
+    const int nl = POOL ? 8 : 32;
+    int img, uu;
+    if (lane < nl && unit_of(m, img0, u0, nl * T + lane, &img, &uu)) {
+      uint32_t* dst = a.out_packed + (((int64_t)img * m.upi + uu) * a.out_cw + (co32 >> 5)) * POUT;
+      store_words<POUT>(dst, pw);
+    }
   }
 }
 
-// Pooled epilogue (2x2 max over the integer accumulator, before BN) of one
-// wave's two M-tiles for output channels [c32, c32 + 32).  The block starts
-// at an even conv row and the M-tiles are assigned so that all four pixels of
-// every window sit in the same lane:
-//   wo = 32: the two tiles are rows 2r and 2r+1 (same register);
-//   wo = 64: the tiles are the same half of rows 2r and 2r+1 (interleaved tiles);
-//   wo = 16: one tile is two rows, the lower pixel is register v + 8;
-//   wo =  8: one tile is four rows, the lower pixel is register v + 4;
-// and the horizontal neighbour of an even pixel (even v) is register v + 1.
-// Lane (g, r32) ends with 8 pooled pixels of channel c32 + r32.
-template <int WO, class AccT>
-__device__ __forceinline__ void store_pool_tiles(const MfmaArgs& m, const EpiCtx& x, const AccT& a0,
-                                                 const AccT& a1, int mt0, int mt1, int c32) {
+// Epilogue of one tile in the swapped orientation (weights as the A
+// operand): register v = 4q + i of lane l holds output channel
+// co32 + 8q + 4(l/32) + i of unit 32T + l%32.  Each register is one store
+// instruction writing two 128-byte runs (32 consecutive units of two
+// channels) through a buffer resource; the per-register part of the offset
+// is a scalar.  Lanes whose unit does not exist get an offset past the end
+// of the buffer, so their stores and residual loads are dropped.  The
+// block's per-channel parameters come from LDS.
+template <int KIND, class AccT>
+__device__ __forceinline__ void tile_epilogue_swap(const MfmaArgs& m, const AccT& acc, int img0, int u0,
+                                                   int T, int co32, int co_blk, const float* prm,
+                                                   int lane) {
   const ConvArgs& a = m.c;
-  const int g = x.lane >> 5, r32 = x.lane & 31;
+  const int g = lane >> 5, r32 = lane & 31;
   const float inv = 1.0f / (float)(1 << a.shift);
-  const bool pack = a.out_packed != nullptr && c32 < a.cout;  // uniform
-  const int co = c32 + r32;
-  const bool co_ok = co < a.cout;
-  const int cs = min(co, a.cout - 1);
-  float kk = 0.0f, bb = 0.0f, ss = 0.0f;
-  if (a.mode == QCONV_EPI_BN_F32 || a.mode == QCONV_EPI_BN_PACK) {
-    kk = a.bn_k[cs];
-    bb = a.bn_b[cs];
-  } else if (a.mode == QCONV_EPI_SCALE_F32) {
-    ss = a.scale[cs];
-  }
-  const int64_t plane = (int64_t)a.oh_out * a.ow_out;
-  const int pout = pack ? planes_of(a.out_bits) : 0;
-  const int cword = c32 >> 5;
-  Unroll<0, 8>::run([&](auto S) {
-    constexpr int s = decltype(S)::value;
-    constexpr bool pair_tiles = WO >= 32;
-    constexpr int ti = pair_tiles ? 0 : s / 4;  // tile holding the window's upper row
-    constexpr int u = pair_tiles ? s : s % 4;
-    constexpr int v = (WO == 8) ? (u & 1) * 2 + (u >> 1) * 8 : 2 * u;
-    constexpr int dv = pair_tiles ? 0 : (WO == 16 ? 8 : 4);
-    const AccT& top = (ti == 0) ? a0 : a1;
-    const AccT& bot = pair_tiles ? a1 : top;
-    const int best = max(max(acc_value(top, v), acc_value(top, v + 1)),
-                         max(acc_value(bot, v + dv), acc_value(bot, v + dv + 1)));
-    const int t = 32 * ((ti == 0) ? mt0 : mt1) + 8 * (v / 4) + 4 * g + (v % 4);
-    int img = 0, pp = 0;
-    bool ok = block_pixel(m, x, t, &img, &pp);
-    const int oy = pp / a.wo, ox = pp - (pp / a.wo) * a.wo;
-    const int py = oy >> 1, px = ox >> 1;
-    ok = ok && py < a.oh_out;  // an odd last conv row has no pooled row
-    const float ar = (float)best * inv;
-    float z = (a.mode == QCONV_EPI_SCALE_F32) ? ss * ar : fmaf(kk, ar, bb);
-    const int64_t oi = ((int64_t)img * a.cout + cs) * plane + (int64_t)py * a.ow_out + px;
-    if (a.mode != QCONV_EPI_BN_PACK && co_ok && ok) {
-      if (a.mode == QCONV_EPI_INT32) {
-        static_cast<int32_t*>(a.out)[oi] = best;
-      } else {
-        if (a.residual_on) z = z + a.residual[oi];
-        static_cast<float*>(a.out)[oi] = z;
-      }
+  int img, uu;
+  const bool uok = unit_of(m, img0, u0, 32 * T + r32, &img, &uu);
+  const int cbase = co32 + 4 * g;
+  const int voff = uok ? (int)((((int64_t)img * a.cout + cbase) * m.upi + uu) * 4) : 0x7FFFFFF0;
+  const __amdgpu_buffer_rsrc_t orsrc =
+      __builtin_amdgcn_make_buffer_rsrc(a.out, (short)0, m.out_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rrsrc = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(a.residual_on ? a.residual : (const float*)a.out), (short)0, m.out_bytes, 0x00020000);
+  const bool full = co32 + 32 <= a.cout;  // uniform: no channel of the tile is missing
+  const int pstride = m.upi * 4;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    float4 k4 = make_float4(0.f, 0.f, 0.f, 0.f), b4 = k4;
+    if constexpr (KIND != K_INT32) {
+      const int pc = co32 - co_blk + 8 * q + 4 * g;
+      k4 = *reinterpret_cast<const float4*>(prm + pc);
+      b4 = *reinterpret_cast<const float4*>(prm + 128 + pc);
     }
-    if (pack) {
-      const uint32_t pl = (co_ok && ok) ? quant_rt(hardtanh(z), a.out_bits, a.othr) : 0u;
-      for (int p = 0; p < pout; ++p) {
-        const uint64_t bal = __ballot((pl >> p) & 1u);
-        if (r32 == 0 && ok) {
-          const uint32_t word = g ? (uint32_t)(bal >> 32) : (uint32_t)bal;
-          a.out_packed[((((int64_t)img * a.oh_out + py) * a.ow_out + px) * a.out_cw + cword) * pout + p] =
-              word;
+    const float kv[4] = {k4.x, k4.y, k4.z, k4.w};
+    const float bv[4] = {b4.x, b4.y, b4.z, b4.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int so = (8 * q + i) * pstride;
+      uint32_t bits;
+      if constexpr (KIND == K_INT32) {
+        bits = (uint32_t)acc_i(acc, 4 * q + i);
+      } else {
+        float z = acc_f(acc, 4 * q + i) * inv;
+        if constexpr (KIND == K_SCALE) z = kv[i] * z;
+        if constexpr (KIND == K_BNF32) {
+          z = fmaf(kv[i], z, bv[i]);
+          if (a.residual_on)
+            z = z + __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rrsrc, voff, so, 0));
+        }
+        bits = __float_as_uint(z);
+      }
+      if (full || cbase + 8 * q + i < a.cout) __builtin_amdgcn_raw_buffer_store_b32(bits, orsrc, voff, so, 0);
+    }
+  }
+}
+
+// The epilogue over the wave's MT x NT tiles: a loop at run time that copies
+// one tile at a time out of the (statically indexed) accumulator array.
+template <int KIND, int OB, int POOL, int MT, int NT, class AccT>
+__device__ __forceinline__ void epilogue(const MfmaArgs& m, const AccT (&acc)[MT][NT], int img0,
+                                         int u0, int tile_m0, int co_w, int lane) {
+  const ConvArgs& a = m.c;
+  const int r32 = lane & 31;
+  float kk[NT], bb[NT];
+#pragma unroll
+  for (int j = 0; j < NT; ++j) {
+    const int co = co_w + 32 * j + r32;
+    const int cs = co < a.cout ? co : a.cout - 1;
+    kk[j] = 0.0f;
+    bb[j] = 0.0f;
+    if constexpr (KIND == K_SCALE) kk[j] = a.scale[cs];
+    if constexpr (KIND == K_BNF32 || KIND == K_PACK) {
+      kk[j] = a.bn_k[cs];
+      bb[j] = a.bn_b[cs];
+    }
+  }
+#pragma nounroll
+  for (int tt = 0; tt < MT * NT; ++tt) {
+    const int i = tt / NT, j = tt - (tt / NT) * NT;
+    if (co_w + 32 * j >= a.cout) continue;  // uniform: tile past the last channel
+    AccT cur;
+    switch (tt) {
+#define QC_PICK(K)                   \
+  case K:                            \
+    if constexpr (K < MT * NT) cur = acc[K / NT][K % NT]; \
+    break;
+      QC_PICK(0) QC_PICK(1) QC_PICK(2) QC_PICK(3) QC_PICK(4) QC_PICK(5) QC_PICK(6) QC_PICK(7)
+#undef QC_PICK
+      default: break;
+    }
+    float kj = kk[0], bj = bb[0];
+#pragma unroll
+    for (int jj = 1; jj < NT; ++jj)
+      if (j == jj) {
+        kj = kk[jj];
+        bj = bb[jj];
+      }
+    tile_epilogue<KIND, OB, POOL>(m, cur, img0, u0, tile_m0 + i, co_w + 32 * j, kj, bj, lane);
+  }
+}
+
+template <int KIND, int POOL, int MT, int NT, class AccT>
+__device__ __forceinline__ void epilogue_ob(const MfmaArgs& m, const AccT (&acc)[MT][NT], int img0,
+                                            int u0, int tile_m0, int co_w, int lane) {
+  const int ob = m.c.out_packed ? m.c.out_bits : 0;
+  if (ob == 0) epilogue<KIND, 0, POOL>(m, acc, img0, u0, tile_m0, co_w, lane);
+  else if (ob == 1) epilogue<KIND, 1, POOL>(m, acc, img0, u0, tile_m0, co_w, lane);
+  else if (ob == 2) epilogue<KIND, 2, POOL>(m, acc, img0, u0, tile_m0, co_w, lane);
+  else epilogue<KIND, 3, POOL>(m, acc, img0, u0, tile_m0, co_w, lane);
+}
+
+template <int POOL, int MT, int NT, class AccT>
+__device__ __forceinline__ void epilogue_mode(const MfmaArgs& m, const AccT (&acc)[MT][NT], int img0,
+                                              int u0, int tile_m0, int co_w, int lane) {
+  switch (m.c.mode) {
+    case QCONV_EPI_INT32: epilogue<K_INT32, 0, POOL>(m, acc, img0, u0, tile_m0, co_w, lane); break;
+    case QCONV_EPI_SCALE_F32: epilogue<K_SCALE, 0, POOL>(m, acc, img0, u0, tile_m0, co_w, lane); break;
+    case QCONV_EPI_BN_F32: epilogue_ob<K_BNF32, POOL>(m, acc, img0, u0, tile_m0, co_w, lane); break;
+    default: epilogue_ob<K_PACK, POOL>(m, acc, img0, u0, tile_m0, co_w, lane); break;
+  }
+}
+
+// Geometry of one work item (a pixel tile x a channel tile) as seen by one lane.
+template <int MT>
+struct Item {
+  int img0, u0, co_blk, iy0;
+  int abase[MT];  // LDS byte offset (tap (0, 0), this lane's k-half) of the pixel fed into row r32 of each M-tile
+};
+
+// Image and first input row of the halo tile of work item w.
+__device__ __forceinline__ void item_origin(const MfmaArgs& m, int w, int* img0, int* iy0) {
+  const int pt = w / m.tiles_co;
+  int u0;
+  if (m.ipb == 1) {
+    *img0 = pt / m.bpi;
+    u0 = (pt - *img0 * m.bpi) * m.units_pb;
+  } else {
+    *img0 = pt * m.ipb;
+    u0 = 0;
+  }
+  const int uy0 = (int)fdiv((uint32_t)u0, m.fd_uw);
+  *iy0 = (m.pool ? 2 * uy0 : uy0) * m.c.stride - m.c.pad;
+}
+
+template <int MT, int NT, int WN>
+__device__ __forceinline__ void decode_item(const MfmaArgs& m, int w, int wm, int r32, int g, Item<MT>* it) {
+  const ConvArgs& a = m.c;
+  const int pt = w / m.tiles_co;
+  const int ct = w - pt * m.tiles_co;
+  it->co_blk = ct * (32 * NT * WN);
+  if (m.ipb == 1) {
+    it->img0 = pt / m.bpi;
+    it->u0 = (pt - it->img0 * m.bpi) * m.units_pb;
+  } else {
+    it->img0 = pt * m.ipb;
+    it->u0 = 0;
+  }
+  // first conv row held in the halo tile (ipb > 1: every slot starts at row 0)
+  const int uy0 = (int)fdiv((uint32_t)it->u0, m.fd_uw);
+  const int oy0 = m.pool ? 2 * uy0 : uy0;
+  it->iy0 = oy0 * a.stride - a.pad;
+#pragma unroll
+  for (int i = 0; i < MT; ++i) {
+    const int T = wm * MT + i;
+    int unit, e = 0;
+    if (m.pool) {
+      unit = 8 * T + 4 * ((r32 >> 2) & 1) + (r32 >> 3);
+      e = r32 & 3;
+    } else {
+      unit = 32 * T + r32;
+    }
+    int img, uu;
+    if (!unit_of(m, it->img0, it->u0, unit, &img, &uu)) {
+      uu = it->u0;  // a row past the end: read any valid pixel, its result is dropped
+      img = it->img0;
+    }
+    const int slot = img - it->img0;
+    const int uy = (int)fdiv((uint32_t)uu, m.fd_uw);
+    const int ux = uu - uy * m.uw;
+    const int oy = m.pool ? 2 * uy + (e >> 1) : uy;
+    const int ox = m.pool ? 2 * ux + (e & 1) : ux;
+    const int hp = slot * m.slot_pix + (oy - oy0) * a.stride * m.hc + ox * a.stride;
+    it->abase[i] = hp * m.pix_bytes + g * 16;
+  }
+}
+
+// Packed words of this thread's share of a halo tile: item it = tid + 256 u
+// is (halo pixel it / chunk_words, word it % chunk_words).  Pixels outside
+// the image and words past the last channel read as 0 (= Q(0)).
+template <int PA, int NI>
+__device__ __forceinline__ void load_halo(const MfmaArgs& m, int img0, int iy0, int chunk, int tid,
+                                          uint32_t (&raw)[NI][PA]) {
+  const ConvArgs& a = m.c;
+  const int items = m.ipb * m.slot_pix * m.chunk_words;
+  const int apix = a.cw * PA;
+#pragma unroll
+  for (int u = 0; u < NI; ++u) {
+    const int it = tid + 256 * u;
+#pragma unroll
+    for (int p = 0; p < PA; ++p) raw[u][p] = 0u;
+    if (it < items) {
+      const int hp = (int)fdiv((uint32_t)it, m.fd_cwc);
+      const int cwl = it - hp * m.chunk_words;
+      const int slot = (int)fdiv((uint32_t)hp, m.fd_slot);
+      const int rem = hp - slot * m.slot_pix;
+      const int hrow = (int)fdiv((uint32_t)rem, m.fd_hc);
+      const int hcol = rem - hrow * m.hc;
+      const int img = img0 + slot;
+      const int iy = iy0 + hrow, ix = hcol - a.pad;
+      const int cw = chunk * m.chunk_words + cwl;
+      if (img < a.n && iy >= 0 && iy < a.h && ix >= 0 && ix < a.w && cw < a.cw) {
+        const uint32_t* src = a.act + (((int64_t)img * a.h + iy) * a.w + ix) * apix + cw * PA;
+        if constexpr (PA == 1) {
+          raw[u][0] = src[0];
+        } else if constexpr (PA == 2) {
+          const uint2 v = *reinterpret_cast<const uint2*>(src);
+          raw[u][0] = v.x;
+          raw[u][1] = v.y;
+        } else {
+          const uint4 v = *reinterpret_cast<const uint4*>(src);
+          raw[u][0] = v.x;
+          raw[u][1] = v.y;
+          raw[u][2] = v.z;
+          raw[u][3] = v.w;
         }
       }
     }
-  });
+  }
 }
 
-template <int FP4, int PA, int NTW>
-__global__ __launch_bounds__(256, QC_MFMA_WPE) void conv_mfma_kernel(const MfmaArgs m) {
+// Expands this thread's share of a halo tile into an LDS buffer: the items
+// already held in raw, then any items past NI * 256 loaded here directly.
+template <int FP4, int PA, int NI>
+__device__ __forceinline__ void store_halo(const MfmaArgs& m, int img0, int iy0, int chunk, int tid,
+                                           const uint32_t (&raw)[NI][PA], uint8_t* buf) {
+  const int items = m.ipb * m.slot_pix * m.chunk_words;
+#pragma unroll
+  for (int u = 0; u < NI; ++u) {
+    const int it = tid + 256 * u;
+    if (it < items) {
+      const int hp = (int)fdiv((uint32_t)it, m.fd_cwc);
+      const int cwl = it - hp * m.chunk_words;
+      expand_to_lds<FP4, PA>(raw[u], buf + hp * m.pix_bytes + cwl * OpT<FP4>::WORD_BYTES);
+    }
+  }
+  for (int it = NI * 256 + tid; it < items; it += 256) {
+    uint32_t one[1][PA];
+    load_halo<PA, 1>(m, img0, iy0, chunk, it, one);
+    const int hp = (int)fdiv((uint32_t)it, m.fd_cwc);
+    const int cwl = it - hp * m.chunk_words;
+    expand_to_lds<FP4, PA>(one[0], buf + hp * m.pix_bytes + cwl * OpT<FP4>::WORD_BYTES);
+  }
+}
+
+// Per-channel parameters of the swapped epilogue for channels co_blk.. of the item.
+template <int BCO>
+__device__ __forceinline__ void load_params(const ConvArgs& a, int co_blk, int tid, float* prm) {
+  if (tid < 2 * BCO) {
+    const int half = tid / BCO, c = tid - half * BCO;
+    const int cs = min(co_blk + c, a.cout - 1);
+    float v = 0.0f;
+    if (a.mode == QCONV_EPI_SCALE_F32) v = half ? 0.0f : a.scale[cs];
+    else if (a.mode == QCONV_EPI_BN_F32) v = half ? a.bn_b[cs] : a.bn_k[cs];
+    prm[half * 128 + c] = v;
+  }
+}
+
+// The convolution kernel.  Blocks loop over work items (pixel tile x channel
+// tile) with a stride of the grid size.  Each (item, channel chunk) is a
+// stage; the packed words of stage s + 1 are loaded into registers before
+// the MFMAs of stage s and expanded into the other of two LDS halo buffers
+// after them, so that global latency, the expansion and the epilogue's
+// stores overlap the matrix work.  Split-K shapes run one item per block.
+template <int FP4, int PA, int CFG, int SWAP>
+__global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
   using O = OpT<FP4>;
   using acc_t = typename O::acc_t;
-  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  using C = Cfg<CFG>;
+  constexpr int MT = C::MT, NT = C::NT, WN = C::WN, SK = C::SK;
+  constexpr int BCO = 32 * NT * WN;
+  constexpr int NI = halo_items_per_thread(PA);  // halo items per thread and stage
+  static_assert(SK == 1 || SK == MT * NT, "a split-K block has one tile per wave");
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds_raw[];
   const ConvArgs& a = m.c;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wk = wave % SK;  // K-split index
+  const int wmn = wave / SK;
+  const int wm = wmn / WN, wn = wmn - (wmn / WN) * WN;
   const int g = lane >> 5, r32 = lane & 31;
-  const int hwo = a.ho * a.wo;
+  const int total = m.tiles_px * m.tiles_co;
+  // LDS: two parameter sets, then two halo buffers
+  float* prm_base = reinterpret_cast<float*>(lds_raw);
+  uint8_t* halo_base = lds_raw + 2 * PARAM_BYTES;
+  const int buf_bytes = m.buf_bytes;
 
-  const int slot_pix = m.hr * m.hc;
-  const int apix = a.cw * PA;
-  const int n_slots = (m.ipb == 1) ? 1 : m.ipb;
-  const int items_per_chunk = n_slots * slot_pix * m.chunk_words;
-  const int taps = a.kh * a.kw;
-  const int steps_per_chunk = m.chunk_words / O::WORDS_PER_STEP;
-  // B fragments are read through a buffer resource: the per-lane part of
-  // the address is a vector offset, the per-step part a scalar offset, and
-  // reads past the operand copy return 0.
+  int w = blockIdx.x;
+  if (w >= total) return;
+  Item<MT> cur;
+  decode_item<MT, NT, WN>(m, w, wm, r32, g, &cur);
+  uint32_t raw[NI][PA];
+  load_halo<PA, NI>(m, cur.img0, cur.iy0, 0, tid, raw);
+  if constexpr (SWAP) load_params<BCO>(a, cur.co_blk, tid, prm_base);
+  store_halo<FP4, PA, NI>(m, cur.img0, cur.iy0, 0, tid, raw, halo_base);
+  __syncthreads();
+
+  acc_t acc[MT][NT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < NT; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0;
+
+  // B fragments are read through a buffer resource: the per-lane part of the
+  // address is a vector offset, the per-step part a scalar offset, and reads
+  // past the operand copy return 0.
   const __amdgpu_buffer_rsrc_t brsrc =
       __builtin_amdgcn_make_buffer_rsrc((void*)m.wx, (short)0, m.wx_bytes, 0x00020000);
   const int bstride = a.cop * 32;  // bytes between consecutive k-steps
-  // one (pixel tile, channel tile) per block
-  {
-    const int pb = blockIdx.x;
-    const int co_blk = blockIdx.y * (64 * NTW);
-    int img0, p0;
-    if (m.ipb == 1) {
-      img0 = pb / m.blocks_per_img;
-      p0 = (pb % m.blocks_per_img) * BLOCK_PIX;
-    } else {
-      img0 = pb * m.ipb;
-      p0 = 0;
-    }
-    const int oy0 = p0 / a.wo;
-    const int iy0 = oy0 * a.stride - a.pad;
+  const int taps = a.kh * a.kw;
+  const int steps_per_chunk = m.chunk_words / O::WORDS_PER_STEP;
+  int chunk = 0, sbuf = 0, ipar = 0;
 
-    // LDS byte offset of each of the wave's M-tile rows at tap (0, 0), plus
-    // this lane's 16-byte half of the k-step.
-    int abase[MTW];
-#pragma unroll
-    for (int i = 0; i < MTW; ++i) {
-      const int t = 32 * (m.mt_interleave ? wm + 2 * i : wm * MTW + i) + r32;
-      int slot, pp;
-      if (m.ipb == 1) {
-        slot = 0;
-        pp = p0 + t;
-      } else {
-        slot = t / hwo;
-        pp = t - slot * hwo;
-      }
-      bool ok = (m.ipb == 1) ? (pp < hwo) : (slot < m.ipb);
-      if (!ok) {  // a row past the end: read any valid LDS pixel, its result is dropped
-        slot = 0;
-        pp = p0;
-      }
-      const int oy = pp / a.wo, ox = pp - (pp / a.wo) * a.wo;
-      const int hp = slot * slot_pix + (oy - oy0) * a.stride * m.hc + ox * a.stride;
-      abase[i] = hp * m.pix_bytes + g * 16;
+  for (;;) {
+    // ---- the next stage: its packed words go into registers now ----
+    int nw = w, nchunk = chunk + 1;
+    if (nchunk == m.nchunks) {
+      nchunk = 0;
+      nw = w + gridDim.x;
+    }
+    const bool has_next = nw < total;
+    int nimg0 = cur.img0, niy0 = cur.iy0;
+    if (has_next) {
+      if (nchunk == 0) item_origin(m, nw, &nimg0, &niy0);
+      load_halo<PA, NI>(m, nimg0, niy0, nchunk, tid, raw);
     }
 
-    acc_t acc[MTW][NTW];
+    // ---- MFMA over this wave's share of the (tap, k-step) steps of the stage ----
+    // B fragments come from a ring of three register sets, each loaded two
+    // steps before its MFMAs; A fragments are read from LDS one step ahead.
+    {
+      const uint8_t* lds = halo_base + sbuf * buf_bytes;
+      const int co_w = cur.co_blk + 32 * NT * wn;
+      int bvoff[NT];
 #pragma unroll
-    for (int i = 0; i < MTW; ++i)
-#pragma unroll
-      for (int j = 0; j < NTW; ++j)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc[i][j][v] = 0;
-
-    int bvoff[NTW];
-#pragma unroll
-    for (int j = 0; j < NTW; ++j) bvoff[j] = (co_blk + 32 * (wn * NTW + j) + r32) * 32 + g * 16;
-
-    for (int chunk = 0; chunk < m.nchunks; ++chunk) {
-      __syncthreads();
-      // ---- expand the halo tile of this channel chunk into LDS ----
-      // loads of up to 4 items are issued together before any is expanded
-      for (int it0 = 0; it0 < items_per_chunk; it0 += 4 * 256) {
-        uint32_t pl[4][PA];
-        int dst[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int it = it0 + u * 256 + tid;
-          dst[u] = -1;
-#pragma unroll
-          for (int p = 0; p < PA; ++p) pl[u][p] = 0u;
-          if (it < items_per_chunk) {
-            const int cwl = it % m.chunk_words;
-            const int hp = it / m.chunk_words;
-            const int slot = hp / slot_pix;
-            const int rem = hp - slot * slot_pix;
-            const int hrow = rem / m.hc, hcol = rem - (rem / m.hc) * m.hc;
-            const int img = img0 + slot;
-            const int iy = iy0 + hrow, ix = hcol - a.pad;
-            const int cw = chunk * m.chunk_words + cwl;
-            dst[u] = hp * m.pix_bytes + cwl * O::WORD_BYTES;
-            if (img < a.n && iy >= 0 && iy < a.h && ix >= 0 && ix < a.w && cw < a.cw) {
-              const uint32_t* src = a.act + (((int64_t)img * a.h + iy) * a.w + ix) * apix + cw * PA;
-#pragma unroll
-              for (int p = 0; p < PA; ++p) pl[u][p] = src[p];
-            }
-          }
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-          if (dst[u] >= 0) expand_to_lds<FP4, PA>(pl[u], lds + dst[u]);
-      }
-      __syncthreads();
-
-      // ---- MFMA over (tap, k-step) of this chunk ----
-      // B fragments come from a ring of three register sets, each loaded two
-      // k-steps before its MFMAs (buffer loads, so the compiler keeps them
-      // where they are issued).  A fragments are read from LDS in the step
-      // that uses them.  Steps advance (tap, k-step) incrementally.
+      for (int j = 0; j < NT; ++j) bvoff[j] = (co_w + 32 * j + r32) * 32 + g * 16;
       const int ks0 = chunk * steps_per_chunk;
       const int spc = min(m.ksteps, ks0 + steps_per_chunk) - ks0;  // k-steps per tap in this chunk
-      const int nsteps = taps * spc;
-      // load stream (runs two steps ahead of the compute stream)
-      int l_tap = 0, l_ksl = 0, l_count = 0;
-      auto bload = [&](v4i (&dst)[NTW]) {
-        const int so = (l_tap * m.ksteps + ks0 + l_ksl) * bstride;
+      const int nsteps_all = taps * spc;
+      const int sbeg = (nsteps_all * wk) / SK, send = (nsteps_all * (wk + 1)) / SK;
+      const int nsteps = send - sbeg;
+      if (nsteps > 0) {
+        const int tap0 = sbeg / spc;
+        int l_tap = tap0, l_ksl = sbeg - tap0 * spc, l_count = 0;
+        auto bload = [&](v4i (&dstb)[NT]) {
+          const int so = (l_tap * m.ksteps + ks0 + l_ksl) * bstride;
 #pragma unroll
-        for (int j = 0; j < NTW; ++j)
-          dst[j] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(brsrc, bvoff[j], so, 0));
-        if (l_count + 1 < nsteps) {  // the last step is reloaded past the end (never used)
-          ++l_count;
-          if (++l_ksl == spc) {
-            l_ksl = 0;
-            ++l_tap;
+          for (int j = 0; j < NT; ++j)
+            dstb[j] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(brsrc, bvoff[j], so, 0));
+          if (l_count + 1 < nsteps) {  // the last step is reloaded past the end (never used)
+            ++l_count;
+            if (++l_ksl == spc) {
+              l_ksl = 0;
+              ++l_tap;
+            }
           }
-        }
-      };
-      // compute stream
-      int c_ksl = 0, c_ky = 0, c_kx = 0;
-      auto step = [&](const v4i (&bf)[NTW]) {
-        const int lo = (c_ky * m.hc + c_kx) * m.pix_bytes + c_ksl * 32;
-        v4i af[MTW];
+        };
+        int r_ksl = sbeg - tap0 * spc, r_ky = tap0 / a.kw, r_kx = tap0 - (tap0 / a.kw) * a.kw, r_count = 0;
+        auto aload = [&](v4i (&dsta)[MT]) {
+          const int lo = (r_ky * m.hc + r_kx) * m.pix_bytes + r_ksl * 32;
 #pragma unroll
-        for (int i = 0; i < MTW; ++i) af[i] = *reinterpret_cast<const v4i*>(lds + abase[i] + lo);
-#pragma unroll
-        for (int i = 0; i < MTW; ++i)
-#pragma unroll
-          for (int j = 0; j < NTW; ++j) acc[i][j] = mfma(af[i], bf[j], acc[i][j]);
-        if (++c_ksl == spc) {
-          c_ksl = 0;
-          if (++c_kx == a.kw) {
-            c_kx = 0;
-            ++c_ky;
+          for (int i = 0; i < MT; ++i) dsta[i] = *reinterpret_cast<const v4i*>(lds + cur.abase[i] + lo);
+          ++r_count;
+          if (++r_ksl == spc) {
+            r_ksl = 0;
+            if (++r_kx == a.kw) {
+              r_kx = 0;
+              ++r_ky;
+            }
           }
-        }
-      };
-      v4i B0[NTW], B1[NTW], B2[NTW];
-      bload(B0);
-      bload(B1);
-      for (int st = 0; st < nsteps; st += 3) {
-        bload(B2);
-        step(B0);
-        if (st + 1 >= nsteps) break;
+        };
+        v4i Acur[MT], Anext[MT];
+        auto step = [&](const v4i (&bf)[NT]) {
+#pragma unroll
+          for (int i = 0; i < MT; ++i) Acur[i] = Anext[i];
+          if (r_count < nsteps) aload(Anext);
+#pragma unroll
+          for (int i = 0; i < MT; ++i)
+#pragma unroll
+            for (int j = 0; j < NT; ++j) {
+              if constexpr (SWAP)
+                acc[i][j] = mfma(bf[j], Acur[i], acc[i][j]);
+              else
+                acc[i][j] = mfma(Acur[i], bf[j], acc[i][j]);
+            }
+        };
+#if QC_BRING == 3
+        v4i B0[NT], B1[NT], B2[NT];
         bload(B0);
-        step(B1);
-        if (st + 2 >= nsteps) break;
         bload(B1);
-        step(B2);
+        aload(Anext);
+        for (int st = 0; st < nsteps; st += 3) {
+          bload(B2);
+          step(B0);
+          if (st + 1 >= nsteps) break;
+          bload(B0);
+          step(B1);
+          if (st + 2 >= nsteps) break;
+          bload(B1);
+          step(B2);
+        }
+#else
+        v4i B0[NT], B1[NT];
+        bload(B0);
+        aload(Anext);
+        for (int st = 0; st < nsteps; st += 2) {
+          bload(B1);
+          step(B0);
+          if (st + 1 >= nsteps) break;
+          bload(B0);
+          step(B1);
+        }
+#endif
       }
     }
 
-    // ---- epilogue ----
-    __syncthreads();  // every wave is done with the halo tile; LDS becomes the output stage
-    float* stage = reinterpret_cast<float*>(lds + wave * STAGE_BYTES);
-    const EpiCtx x = {img0, p0, co_blk, hwo, lane};
-    if constexpr (MTW == 2) {
-      if (m.pool_wo) {
-        const int mt0 = m.mt_interleave ? wm : 2 * wm;
-        const int mt1 = m.mt_interleave ? wm + 2 : 2 * wm + 1;
-        Unroll<0, NTW>::run([&](auto J) {
-          const int c32 = co_blk + 32 * (wn * NTW + J);
-          switch (m.pool_wo) {
-            case 8: store_pool_tiles<8>(m, x, acc[0][J], acc[1][J], mt0, mt1, c32); break;
-            case 16: store_pool_tiles<16>(m, x, acc[0][J], acc[1][J], mt0, mt1, c32); break;
-            case 32: store_pool_tiles<32>(m, x, acc[0][J], acc[1][J], mt0, mt1, c32); break;
-            default: store_pool_tiles<64>(m, x, acc[0][J], acc[1][J], mt0, mt1, c32); break;
+    // ---- the next stage's halo into the other buffer (the epilogue below
+    // reads no halo buffer; a split-K block never has a next stage) ----
+    if (has_next)
+      store_halo<FP4, PA, NI>(m, nimg0, niy0, nchunk, tid, raw, halo_base + (sbuf ^ 1) * buf_bytes);
+
+    // ---- epilogue of a finished item ----
+    if (chunk == m.nchunks - 1) {
+      const float* prm = prm_base + ipar * (PARAM_BYTES / 4);
+      const int co_w = cur.co_blk + 32 * NT * wn;
+      if constexpr (SK > 1) {
+        // split-K: sum the partial tiles through LDS (both halo buffers:
+        // a split-K block has no next stage), one tile per wave
+        __syncthreads();
+        float4* red = reinterpret_cast<float4*>(halo_base);
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+          for (int j = 0; j < NT; ++j)
+#pragma unroll
+            for (int v4 = 0; v4 < 4; ++v4) {
+              float4 t;
+              t.x = acc_f(acc[i][j], 4 * v4);
+              t.y = acc_f(acc[i][j], 4 * v4 + 1);
+              t.z = acc_f(acc[i][j], 4 * v4 + 2);
+              t.w = acc_f(acc[i][j], 4 * v4 + 3);
+              red[((wave * (MT * NT) + i * NT + j) * 4 + v4) * 64 + lane] = t;
+            }
+        __syncthreads();
+        const int tile = wave;  // this wave's tile after the reduction
+        acc_t sum;
+#pragma unroll
+        for (int v4 = 0; v4 < 4; ++v4) {
+          float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+#pragma unroll
+          for (int ww = 0; ww < SK; ++ww) {
+            const float4 t = red[((ww * (MT * NT) + tile) * 4 + v4) * 64 + lane];
+            s0 += t.x;
+            s1 += t.y;
+            s2 += t.z;
+            s3 += t.w;
           }
-        });
-        return;
+          sum[4 * v4] = s0;
+          sum[4 * v4 + 1] = s1;
+          sum[4 * v4 + 2] = s2;
+          sum[4 * v4 + 3] = s3;
+        }
+        const int ti = tile / NT, tj = tile - (tile / NT) * NT;
+        const int co32 = co_w + 32 * tj;
+        if (co32 < a.cout) {
+          if constexpr (SWAP) {
+            if (a.mode == QCONV_EPI_INT32)
+              tile_epilogue_swap<K_INT32>(m, sum, cur.img0, cur.u0, ti, co32, cur.co_blk, prm, lane);
+            else if (a.mode == QCONV_EPI_SCALE_F32)
+              tile_epilogue_swap<K_SCALE>(m, sum, cur.img0, cur.u0, ti, co32, cur.co_blk, prm, lane);
+            else
+              tile_epilogue_swap<K_BNF32>(m, sum, cur.img0, cur.u0, ti, co32, cur.co_blk, prm, lane);
+          } else {
+            acc_t one[1][1] = {{sum}};
+            if (m.pool)
+              epilogue_mode<1>(m, one, cur.img0, cur.u0, ti, co32, lane);
+            else
+              epilogue_mode<0>(m, one, cur.img0, cur.u0, ti, co32, lane);
+          }
+        }
+      } else if (co_w < a.cout) {
+        if constexpr (SWAP) {
+#pragma nounroll
+          for (int tt = 0; tt < MT * NT; ++tt) {
+            const int i = tt / NT, j = tt - (tt / NT) * NT;
+            const int co32 = co_w + 32 * j;
+            if (co32 >= a.cout) continue;
+            acc_t tcur;
+            switch (tt) {
+#define QC_PICK(K)                                         \
+  case K:                                                  \
+    if constexpr (K < MT * NT) tcur = acc[K / NT][K % NT]; \
+    break;
+              QC_PICK(0) QC_PICK(1) QC_PICK(2) QC_PICK(3) QC_PICK(4) QC_PICK(5) QC_PICK(6) QC_PICK(7)
+#undef QC_PICK
+              default: break;
+            }
+            if (a.mode == QCONV_EPI_INT32)
+              tile_epilogue_swap<K_INT32>(m, tcur, cur.img0, cur.u0, wm * MT + i, co32, cur.co_blk, prm, lane);
+            else if (a.mode == QCONV_EPI_SCALE_F32)
+              tile_epilogue_swap<K_SCALE>(m, tcur, cur.img0, cur.u0, wm * MT + i, co32, cur.co_blk, prm, lane);
+            else
+              tile_epilogue_swap<K_BNF32>(m, tcur, cur.img0, cur.u0, wm * MT + i, co32, cur.co_blk, prm, lane);
+          }
+        } else {
+          if (m.pool)
+            epilogue_mode<1>(m, acc, cur.img0, cur.u0, wm * MT, co_w, lane);
+          else
+            epilogue_mode<0>(m, acc, cur.img0, cur.u0, wm * MT, co_w, lane);
+        }
       }
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) acc[i][j][v] = 0;
     }
-    Unroll<0, MTW>::run([&](auto I) {
-      Unroll<0, NTW>::run([&](auto J) {
-        store_tile(m, x, acc[I][J], wm * MTW + I, co_blk + 32 * (wn * NTW + J), stage);
-      });
-    });
+
+    if (!has_next) break;
+    if (nchunk == 0) {
+      ipar ^= 1;
+      w = nw;
+      decode_item<MT, NT, WN>(m, w, wm, r32, g, &cur);
+      if constexpr (SWAP) load_params<BCO>(a, cur.co_blk, tid, prm_base + ipar * (PARAM_BYTES / 4));
+    }
+    chunk = nchunk;
+    sbuf ^= 1;
+    __syncthreads();
   }
 }
 
-bool plan(const ConvArgs& a, MfmaArgs* m) {
+bool plan(const ConvArgs& a, int cfg, MfmaArgs* m) {
   memset(m, 0, sizeof(*m));
   m->c = a;
   const int fp4 = a.mfma_fp4;
@@ -539,13 +924,23 @@ bool plan(const ConvArgs& a, MfmaArgs* m) {
   const int cw_round = ceil_div(a.cw, wpstep) * wpstep;
   m->ksteps = ceil_div(a.cw, wpstep);
   m->wx = fp4 ? a.w_fp4 : a.w_i8;
-  m->wx_bytes = (int)(a.kh * a.kw * m->ksteps * a.cop * 32);
-  const int hwo = a.ho * a.wo;
+  const int64_t wxb = (int64_t)a.kh * a.kw * m->ksteps * a.cop * 32;
+  if (wxb >= ((int64_t)1 << 31)) return false;
+  m->wx_bytes = (int)wxb;
+  m->pool = a.pool;
+  m->uw = a.pool ? a.wo / 2 : a.wo;
+  const int uh = a.pool ? a.ho / 2 : a.ho;
+  m->upi = uh * m->uw;
+  if (m->upi < 1) return false;
+  const int rows = cfg_rows(cfg);
+  const int rows_per_unit = a.pool ? 4 : 1;
+  const int units_pb = rows / rows_per_unit;
+  m->units_pb = units_pb;
   m->hc = (a.wo - 1) * a.stride + a.kw;
-  m->vec_store = (hwo % 4 == 0) ? 1 : 0;
-  // Candidate channel chunks, largest first; smaller chunks shrink the LDS
-  // tile so that more small images fit in one block.
-  int best_pix = -1;
+  m->vec = (m->upi % 4 == 0) ? 1 : 0;
+  // Channel chunks, largest first; smaller chunks shrink the LDS tile so
+  // that more small images fit in one block.
+  int best_units = -1;
   MfmaArgs best = *m;
   for (int cwc = min(chunk_max, cw_round); cwc >= wpstep; cwc /= 2) {
     if (cwc % wpstep) break;
@@ -553,55 +948,124 @@ bool plan(const ConvArgs& a, MfmaArgs* m) {
     t.chunk_words = cwc;
     t.pix_bytes = cwc * word_bytes + 16;
     t.nchunks = ceil_div(cw_round, cwc);
-    int pix;
-    if (hwo * 2 <= BLOCK_PIX) {
-      t.hr = (a.ho - 1) * a.stride + a.kh;
+    int units;
+    const int conv_rows_img = a.pool ? 2 * uh : a.ho;
+    if (m->upi * 2 <= units_pb) {
+      t.hr = (conv_rows_img - 1) * a.stride + a.kh;
       const size_t slot = (size_t)t.hr * t.hc * t.pix_bytes;
       const int fit = (int)(MAX_LDS / slot);
-      t.ipb = min(BLOCK_PIX / hwo, fit);
-      t.blocks_per_img = 0;
+      t.ipb = min(units_pb / m->upi, fit);
+      t.bpi = 0;
       if (t.ipb < 1) continue;
-      pix = t.ipb * hwo;
+      units = t.ipb * m->upi;
     } else {
       t.ipb = 1;
-      t.blocks_per_img = ceil_div(hwo, BLOCK_PIX);
-      const int rows = min(a.ho, ceil_div(BLOCK_PIX, a.wo) + 1);
-      t.hr = (rows - 1) * a.stride + a.kh;
+      t.bpi = ceil_div(m->upi, units_pb);
+      // unit rows a run of units_pb units can touch, then conv rows
+      const int urows = min(uh, ceil_div(units_pb, m->uw) + 1);
+      const int crows = a.pool ? 2 * urows : urows;
+      t.hr = (crows - 1) * a.stride + a.kh;
       if ((size_t)t.hr * t.hc * t.pix_bytes > (size_t)MAX_LDS) continue;
-      pix = BLOCK_PIX;
+      units = units_pb;
     }
-    if (pix > best_pix) {
-      best_pix = pix;
+    if (units > best_units) {
+      best_units = units;
       best = t;
     }
-    if (pix == BLOCK_PIX || (hwo * 2 <= BLOCK_PIX && t.ipb == BLOCK_PIX / hwo)) break;
+    if (units == units_pb || (m->upi * 2 <= units_pb && t.ipb == units_pb / m->upi)) break;
   }
-  if (best_pix < 0) return false;
+  if (best_units < 0) return false;
   *m = best;
-  if (a.pool) {
-    // every 2x2 window must fall in one lane of one wave (see store_pool_tiles)
-    if (MTW != 2 || !(a.wo == 8 || a.wo == 16 || a.wo == 32 || a.wo == 64)) return false;
-    if (m->ipb > 1 && a.ho % 2 != 0) return false;
-    m->pool_wo = a.wo;
-    m->mt_interleave = (a.wo == 64) ? 1 : 0;
+  m->slot_pix = m->hr * m->hc;
+  m->fd_upi = make_fastdiv((uint32_t)m->upi);
+  m->fd_uw = make_fastdiv((uint32_t)m->uw);
+  m->fd_slot = make_fastdiv((uint32_t)m->slot_pix);
+  m->fd_hc = make_fastdiv((uint32_t)m->hc);
+  m->fd_cwc = make_fastdiv((uint32_t)m->chunk_words);
+  // every fast division stays exact: dividend * divisor < 2^32
+  const uint64_t items = (uint64_t)m->ipb * m->slot_pix * m->chunk_words;
+  const uint64_t max_unit = (uint64_t)m->upi + 256;
+  if (items * m->chunk_words >= (1ull << 32) || items * m->slot_pix >= (1ull << 32) ||
+      (uint64_t)m->slot_pix * m->hc >= (1ull << 32) || max_unit * m->upi >= (1ull << 32) ||
+      max_unit * m->uw >= (1ull << 32))
+    return false;
+  m->tiles_px = (m->ipb == 1) ? a.n * m->bpi : ceil_div(a.n, m->ipb);
+  m->tiles_co = ceil_div(a.cout, cfg_block_co(cfg));
+  m->halo_bytes = m->slot_pix * m->pix_bytes * m->ipb;
+  m->ht_needed = 0;
+  if (a.out_packed) {
+    const Thr& t = a.othr;
+    m->ht_needed = (a.out_bits == 2 && t.t0 >= 1.0f) || (a.out_bits == 3 && t.t2 >= 1.0f);
   }
-  if (m->ipb == 1 && m->blocks_per_img == 0) m->blocks_per_img = 1;
-  m->tiles_px = (m->ipb == 1) ? a.n * m->blocks_per_img : ceil_div(a.n, m->ipb);
-  m->tiles_co = (a.cout > 64) ? ceil_div(a.cout, 128) : 1;
-  m->halo_bytes = m->hr * m->hc * m->pix_bytes * (m->ipb == 1 ? 1 : m->ipb);
+  const int64_t ob = (int64_t)a.n * a.cout * m->upi * 4;
+  m->out_bytes = ob < ((int64_t)1 << 31) ? (int)ob : 0;
+  m->buf_bytes = (m->halo_bytes + 15) & ~15;
+  if (cfg == 2) m->buf_bytes = max(m->buf_bytes, RED_BYTES / 2);  // the two buffers hold the split-K partials
   return true;
 }
 
-template <int FP4, int PA>
-int launch_fp(const MfmaArgs& m, hipStream_t s) {
+// LDS bytes of one block: two parameter sets and two halo buffers.
+size_t block_lds(const MfmaArgs& m) { return 2 * PARAM_BYTES + (size_t)m.buf_bytes * 2; }
+
+// Block shape: 64-row split-K blocks when the 256-row shapes would leave the
+// chip under-filled (fewer than two blocks per CU); otherwise 128 or 64
+// output channels per block.
+int pick_cfg(const ConvArgs& a) {
+  const int big = a.cout <= 64 ? 1 : 0;
+  MfmaArgs m;
+  if (!plan(a, big, &m)) return big;
+  const int64_t blocks = (int64_t)m.tiles_px * m.tiles_co;
+  const int steps = a.kh * a.kw * m.ksteps;
+  if (blocks < 512 && steps >= 8) {
+    MfmaArgs s;
+    if (plan(a, 2, &s)) return 2;
+  }
+  return big;
+}
+
+// The swapped orientation serves unpacked, unpooled outputs whose byte size
+// fits a buffer resource.
+bool use_swap(const MfmaArgs& m) {
   const ConvArgs& a = m.c;
-  const size_t lds = max((size_t)m.halo_bytes, (size_t)(4 * STAGE_BYTES));
-  const dim3 grid((unsigned)m.tiles_px, (unsigned)m.tiles_co);
-  if (a.cout > 64)
-    conv_mfma_kernel<FP4, PA, 2><<<grid, 256, lds, s>>>(m);
+  return !a.pool && a.out_packed == nullptr && a.mode != QCONV_EPI_BN_PACK && m.out_bytes > 0;
+}
+
+template <int FP4, int PA, int CFG>
+int launch_cfg(MfmaArgs m, hipStream_t s) {
+  const size_t lds = block_lds(m);
+  const int total = m.tiles_px * m.tiles_co;
+  if (CFG == 2) {
+    m.grid = total;  // split-K: one item per block
+  } else {
+    int dev = 0, cus = 256;
+    if (hipGetDevice(&dev) == hipSuccess) {
+      int v = 0;
+      if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0) cus = v;
+    }
+    const int per_cu = max(1, min(2, (int)((160 * 1024) / lds)));
+    m.grid = min(total, per_cu * cus);
+  }
+  if (use_swap(m))
+    conv_mfma_kernel<FP4, PA, CFG, 1><<<dim3((unsigned)m.grid), 256, lds, s>>>(m);
   else
-    conv_mfma_kernel<FP4, PA, 1><<<grid, 256, lds, s>>>(m);
+    conv_mfma_kernel<FP4, PA, CFG, 0><<<dim3((unsigned)m.grid), 256, lds, s>>>(m);
   return hip_status();
+}
+
+template <int FP4, int PA>
+int launch_fp(const MfmaArgs& m, int cfg, hipStream_t s) {
+#ifdef QC_ONLY_ONE
+  if constexpr (!(FP4 == QC_ONLY_FP4 && PA == QC_ONLY_PA)) {
+    return QCONV_EUNSUPPORTED;
+  } else {
+    return launch_cfg<FP4, PA, 0>(m, s);
+    (void)cfg;
+  }
+#else
+  if (cfg == 0) return launch_cfg<FP4, PA, 0>(m, s);
+  if (cfg == 1) return launch_cfg<FP4, PA, 1>(m, s);
+  return launch_cfg<FP4, PA, 2>(m, s);
+#endif
 }
 
 }  // namespace
@@ -609,21 +1073,22 @@ int launch_fp(const MfmaArgs& m, hipStream_t s) {
 bool mfma_supports(const ConvArgs& a) {
   if (a.stride > 2 || a.n == 0) return false;
   MfmaArgs m;
-  return plan(a, &m);
+  return plan(a, pick_cfg(a), &m);
 }
 
 int launch_conv_mfma(const ConvArgs& a, hipStream_t s) {
   MfmaArgs m;
-  if (!plan(a, &m)) return QCONV_EUNSUPPORTED;
+  const int cfg = pick_cfg(a);
+  if (!plan(a, cfg, &m)) return QCONV_EUNSUPPORTED;
   const int pa = planes_of(a.a_bits);
   if (a.mfma_fp4) {
-    if (pa == 1) return launch_fp<1, 1>(m, s);
-    if (pa == 2) return launch_fp<1, 2>(m, s);
-    return launch_fp<1, 4>(m, s);
+    if (pa == 1) return launch_fp<1, 1>(m, cfg, s);
+    if (pa == 2) return launch_fp<1, 2>(m, cfg, s);
+    return launch_fp<1, 4>(m, cfg, s);
   }
-  if (pa == 1) return launch_fp<0, 1>(m, s);
-  if (pa == 2) return launch_fp<0, 2>(m, s);
-  return launch_fp<0, 4>(m, s);
+  if (pa == 1) return launch_fp<0, 1>(m, cfg, s);
+  if (pa == 2) return launch_fp<0, 2>(m, cfg, s);
+  return launch_fp<0, 4>(m, cfg, s);
 }
 
 }  // namespace qc

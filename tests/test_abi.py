@@ -98,12 +98,16 @@ def test_fold_bn_matches_oracle(oracle_mod):
 
 
 def test_pooled_resolution():
-    """AUTO takes the matrix cores for pooled layers whose windows fit one lane."""
+    """AUTO takes the matrix cores for pooled layers of any geometry (every 2x2
+    window occupies four M rows of one lane) whose input tile fits the staging
+    buffer; rows too wide for it fall back to the bitplane kernel."""
     fp4 = q.ALGO_MFMA_FP4
     assert q.resolve_algo(2, 128, 32, 32, 128, 3, 1, 1, 1, 1, flags=q.EPI_POOL2) == fp4
     assert q.resolve_algo(2, 128, 8, 8, 128, 3, 1, 1, 1, 1, flags=q.EPI_POOL2) == fp4
-    assert q.resolve_algo(2, 128, 9, 9, 128, 3, 1, 1, 1, 1, flags=q.EPI_POOL2) == q.ALGO_BITPLANE
-    assert q.resolve_algo(2, 128, 8, 128, 128, 3, 1, 1, 1, 1, flags=q.EPI_POOL2) == q.ALGO_BITPLANE
+    assert q.resolve_algo(2, 128, 9, 9, 128, 3, 1, 1, 1, 1, flags=q.EPI_POOL2) == fp4
+    assert q.resolve_algo(2, 128, 8, 64, 128, 3, 1, 1, 1, 1, flags=q.EPI_POOL2) == fp4
+    assert q.resolve_algo(1, 128, 8, 4096, 128, 3, 1, 1, 1, 1, flags=q.EPI_POOL2) == q.ALGO_BITPLANE
+    assert q.resolve_algo(1, 128, 8, 4096, 128, 3, 1, 1, 1, 1) == q.ALGO_BITPLANE
 
 
 FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails validation first
