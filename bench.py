@@ -110,16 +110,17 @@ class ConvWorkload:
         return n * c * h * w * 4 + q.packed_act_words(n, c, h, w, self.case.a_bits) * 4
 
 
-def measured_traffic(kernel: str):
-    """HBM bytes per launch from the committed rocprofv3 counter runs, or None
-    when the kernel's sources changed since the counters were taken."""
+def measured_traffic(workload: str, kernel: str):
+    """HBM bytes per launch of `kernel` (a name prefix) on `workload` from the
+    committed rocprofv3 counter runs, or None when there is no record or the
+    kernel's sources changed since the counters were taken."""
     import hashlib
 
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
-    rec = json.load(open(path)).get(kernel)
-    if not rec:
+    rec = json.load(open(path)).get(workload)
+    if not rec or not rec["kernel"].startswith(kernel):
         return None
     h = hashlib.sha256()
     for src in rec["sources"]:
@@ -247,8 +248,9 @@ def main():
                     f"{32 if max(case.a_bits, case.w_bits) < 3 else (8 if case.a_bits == case.w_bits else 16)}, false>"
         else:
             peak, cbound = MFMA_PEAK_GOPS[used], "mfma"
-            kname = f"conv_mfma_kernel<{1 if used == 'mfma_fp4' else 0}, {q.planes(case.a_bits)}, " \
-                    f"{2 if W.cout > 64 else 1}>"
+            # template arguments after the operand format and activation planes
+            # (block shape, operand orientation) are the library's choice
+            kname = f"conv_mfma_kernel<{1 if used == 'mfma_fp4' else 0}, {q.planes(case.a_bits)},"
         hbm_gbs = W.conv_bytes() / t_conv / 1e9
         frac_c = gops_conv / peak if peak else 0.0
         frac_h = hbm_gbs / HBM_PEAK_GBS
@@ -272,7 +274,7 @@ def main():
                                   "frac": round(frac_h, 4)}}),
         })
         out["roofline"].update({
-            "traffic": measured_traffic(kname), "traffic_unit": "HBM bytes per launch",
+            "traffic": measured_traffic(case.name, kname), "traffic_unit": "HBM bytes per launch",
             "algorithmic_bytes": W.conv_bytes(), "avg_us": round(t_conv * 1e6, 2)})
         out.update({
             "pack_act": {"avg_us": round(t_pack * 1e6, 2), "achieved_gbs": round(W.pack_bytes() / t_pack / 1e9, 1),

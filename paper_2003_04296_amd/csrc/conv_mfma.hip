@@ -1008,12 +1008,16 @@ bool plan(const ConvArgs& a, int cfg, MfmaArgs* m) {
 size_t block_lds(const MfmaArgs& m) { return 2 * PARAM_BYTES + (size_t)m.buf_bytes * 2; }
 
 // Block shape: 64-row split-K blocks when the 256-row shapes would leave the
-// chip under-filled (fewer than two blocks per CU); otherwise 128 or 64
-// output channels per block.
+// chip under-filled (fewer than two blocks per CU) or their input tile does
+// not fit the staging buffer; otherwise 128 or 64 output channels per block.
 int pick_cfg(const ConvArgs& a) {
   const int big = a.cout <= 64 ? 1 : 0;
   MfmaArgs m;
-  if (!plan(a, big, &m)) return big;
+  if (!plan(a, big, &m)) {
+    // the 256-row halo does not fit (wide rows, stride 2): 64-row items
+    MfmaArgs s;
+    return plan(a, 2, &s) ? 2 : big;
+  }
   const int64_t blocks = (int64_t)m.tiles_px * m.tiles_co;
   const int steps = a.kh * a.kw * m.ksteps;
   if (blocks < 512 && steps >= 8) {
