@@ -173,9 +173,14 @@ def cpu_baseline_conv(case, mode, budget_s=12.0):
             "sample": f"{m} of {n} images of the same layer (quantize + direct conv + epilogue), {tm:.1f} s"}
 
 
-def cpu_baseline_net(params, forward, budget_s=12.0):
+def cpu_baseline_net(params, wl, budget_s=12.0):
     import oracle
 
+    if wl == "convnet":
+        forward = oracle.convnet_forward
+    else:
+        def forward(p):
+            return oracle.resnet18_forward(p, 2, 2)
     n = params["x"].shape[0]
 
     def run(m):
@@ -284,16 +289,13 @@ def main():
             out["cpu_baseline"] = cpu_baseline_conv(case, mode)
     elif wl in ("convnet", "resnet18"):
         from paper_2003_04296_amd.nets import build_convnet, build_resnet18
-        import oracle
 
         if wl == "convnet":
             params = synth.convnet_params(seed=1003, batch=256)
             net = build_convnet(params, dev)
-            fwd = oracle.convnet_forward
         else:
             params = synth.resnet18_params(seed=1004, batch=64)
             net = build_resnet18(params, dev)
-            fwd = lambda p: oracle.resnet18_forward(p, 2, 2)  # noqa: E731
         x = params["x"].to(dev)
         logits = torch.empty((x.shape[0], net.out_features), dtype=torch.float32, device=dev)
         for _ in range(args.warmup):
@@ -309,7 +311,7 @@ def main():
                     "config": {"workload": wl + ("_1w1a_batch256_32x32" if wl == "convnet" else "_2w2a_batch64_224x224"),
                                "batch": int(x.shape[0])}})
         if not args.no_cpu:
-            out["cpu_baseline"] = cpu_baseline_net(params, fwd)
+            out["cpu_baseline"] = cpu_baseline_net(params, wl)
     else:
         print(f"unknown workload {wl}", file=sys.stderr)
         sys.exit(2)

@@ -182,10 +182,11 @@ int qconv_out_size(int in, int k, int stride, int pad);
  * BN_F32 mode (quantizing the fp32 result).  Requires ceil(cout/32)*32
  * channels of room in out_packed's last word, K = cin*kh*kw with
  * K * max|a| * max|w| < 2^31.  The matrix-core algorithms support stride 1
- * or 2 without pooling and an input tile that fits their staging buffer;
- * asked for explicitly otherwise they return QCONV_EUNSUPPORTED, and AUTO
- * falls back to the bitplane kernels.  Every algorithm returns the same
- * bits. */
+ * or 2 (with or without pooling) and an input tile that fits their LDS
+ * staging buffer (at least one input row of 64 output pixels' receptive
+ * field); asked for explicitly otherwise they return QCONV_EUNSUPPORTED,
+ * and AUTO falls back to the bitplane kernels.  Every algorithm returns the
+ * same bits. */
 int qconv_forward(const qconv_desc* d, const uint32_t* act_packed, const uint32_t* w_packed,
                   const qconv_epilogue* epi, void* out, uint32_t* out_packed, void* stream);
 
