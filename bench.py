@@ -111,7 +111,7 @@ class ConvWorkload:
 
 
 def measured_traffic(workload: str, kernel: str):
-    """HBM bytes per launch of `kernel` (a name prefix) on `workload` from the
+    """HBM bytes per launch of `kernel` on `workload` from the
     committed rocprofv3 counter runs, or None when there is no record or the
     kernel's sources changed since the counters were taken."""
     import hashlib
@@ -120,7 +120,7 @@ def measured_traffic(workload: str, kernel: str):
     if not os.path.exists(path):
         return None
     rec = json.load(open(path)).get(workload)
-    if not rec or not rec["kernel"].startswith(kernel):
+    if not rec or rec["kernel"] != kernel:
         return None
     h = hashlib.sha256()
     for src in rec["sources"]:
@@ -247,15 +247,13 @@ def main():
         n, c, h, w = W.shape
         used = q.ALGO_NAMES[q.resolve_algo(n, c, h, w, W.cout, W.k, case.stride, case.pad, case.a_bits,
                                            case.w_bits, mode, 0, 0, algo)]
+        # the instantiation the library launches for this layer (as the profiler names it)
+        kname = q.kernel_name(n, c, h, w, W.cout, W.k, case.stride, case.pad, case.a_bits, case.w_bits,
+                              mode=mode, algo=algo)
         if used == "bitplane":
             peak, cbound = valu_peak_gops(case.a_bits, case.w_bits), "alu"
-            kname = f"conv_bitplane_kernel<{q.planes(case.a_bits)}, {q.planes(case.w_bits)}, " \
-                    f"{32 if max(case.a_bits, case.w_bits) < 3 else (8 if case.a_bits == case.w_bits else 16)}, false>"
         else:
             peak, cbound = MFMA_PEAK_GOPS[used], "mfma"
-            # template arguments after the operand format and activation planes
-            # (block shape, operand orientation) are the library's choice
-            kname = f"conv_mfma_kernel<{1 if used == 'mfma_fp4' else 0}, {q.planes(case.a_bits)},"
         hbm_gbs = W.conv_bytes() / t_conv / 1e9
         frac_c = gops_conv / peak if peak else 0.0
         frac_h = hbm_gbs / HBM_PEAK_GBS

@@ -195,6 +195,15 @@ int qconv_forward(const qconv_desc* d, const uint32_t* act_packed, const uint32_
  * status if the call would be rejected.  Launches nothing. */
 int qconv_resolve_algo(const qconv_desc* d, const qconv_epilogue* epi);
 
+/* Name of the GPU kernel instantiation qconv_forward would launch for d and
+ * epi on the current device (packed_out != 0: an out_packed buffer would be
+ * passed; BN_PACK implies one), written NUL-terminated into buf (truncated
+ * to len bytes; buf may be NULL).  The name and template arguments are those
+ * a profiler shows, e.g. "conv_mfma_pp_kernel<1, 2, 0>".  Returns the length
+ * of the full name, or a negative status if the call would be rejected.
+ * Launches nothing; the choice depends on the device's compute-unit count. */
+int qconv_kernel_name(const qconv_desc* d, const qconv_epilogue* epi, int packed_out, char* buf, int len);
+
 /* ------------------------------------------------------------------------ */
 /* Whole networks (Algorithm 1, inference branch, layer by layer)            */
 /* ------------------------------------------------------------------------ */

@@ -25,6 +25,7 @@ EXPORTED = (
     "qconv_out_size", "qconv_forward", "qnet_create", "qnet_destroy", "qnet_add_conv_f32",
     "qnet_add_maxpool_f32", "qnet_add_quantize", "qnet_add_qconv", "qnet_add_avgpool",
     "qnet_add_fc_f32", "qnet_workspace_bytes", "qnet_forward", "qnet_tensor_info", "qconv_resolve_algo",
+    "qconv_kernel_name",
 )
 
 
@@ -77,6 +78,8 @@ def lib() -> ctypes.CDLL:
     L.qconv_out_size.argtypes = [i32] * 4
     L.qconv_forward.argtypes = [ctypes.POINTER(qconv_desc), vp, vp, ctypes.POINTER(qconv_epilogue), vp, vp, vp]
     L.qconv_resolve_algo.argtypes = [ctypes.POINTER(qconv_desc), ctypes.POINTER(qconv_epilogue)]
+    L.qconv_kernel_name.argtypes = [ctypes.POINTER(qconv_desc), ctypes.POINTER(qconv_epilogue), i32,
+                                    ctypes.c_char_p, i32]
     L.qnet_create.restype = vp
     L.qnet_create.argtypes = [i32, i32, i32]
     L.qnet_destroy.argtypes = [vp]
@@ -212,6 +215,18 @@ def resolve_algo(n, cin, h, w, cout, k, stride, pad, a_bits, w_bits, mode=EPI_IN
     d = qconv_desc(n, cin, h, w, cout, k, k, stride, pad, a_bits, w_bits, algo)
     e = qconv_epilogue(mode, flags, None, None, None, None, out_bits, None)
     return _check(lib().qconv_resolve_algo(ctypes.byref(d), ctypes.byref(e)), "qconv_resolve_algo")
+
+
+def kernel_name(n, cin, h, w, cout, k, stride, pad, a_bits, w_bits, mode=EPI_INT32, flags=0, out_bits=0,
+                algo=ALGO_AUTO, packed_out=False) -> str:
+    """The GPU kernel instantiation qconv_forward would launch on the current
+    device, as a profiler names it (launches nothing)."""
+    d = qconv_desc(n, cin, h, w, cout, k, k, stride, pad, a_bits, w_bits, algo)
+    e = qconv_epilogue(mode, flags, None, None, None, None, out_bits, None)
+    buf = ctypes.create_string_buffer(128)
+    _check(lib().qconv_kernel_name(ctypes.byref(d), ctypes.byref(e), int(bool(packed_out)), buf, 128),
+           "qconv_kernel_name")
+    return buf.value.decode()
 
 
 class Net:

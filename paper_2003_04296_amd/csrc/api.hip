@@ -235,6 +235,15 @@ int qconv_resolve_algo(const qconv_desc* d, const qconv_epilogue* epi) {
   return prepare_conv(d, nullptr, nullptr, epi, nullptr, nullptr, false, &a);
 }
 
+int qconv_kernel_name(const qconv_desc* d, const qconv_epilogue* epi, int packed_out, char* buf, int len) {
+  ConvArgs a;
+  static uint32_t marker;  // stands for a packed output buffer; never accessed
+  const int algo = prepare_conv(d, nullptr, nullptr, epi, nullptr, packed_out ? &marker : nullptr, false, &a);
+  if (algo < 0) return algo;
+  if (algo == QCONV_ALGO_BITPLANE) return bitplane_kernel_name(a, buf, len);
+  return mfma_kernel_name(a, buf, len);
+}
+
 int qconv_forward(const qconv_desc* d, const uint32_t* act_packed, const uint32_t* w_packed,
                   const qconv_epilogue* epi, void* out, uint32_t* out_packed, void* stream) {
   ConvArgs a;

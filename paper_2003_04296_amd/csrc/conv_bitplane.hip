@@ -20,6 +20,9 @@
 // runs in registers before the only store.
 #include <type_traits>
 
+#include <stdio.h>
+#include <string.h>
+
 #include "qconv_internal.h"
 
 namespace qc {
@@ -249,6 +252,28 @@ int launch_pp(const ConvArgs& a, hipStream_t s) {
 }
 
 }  // namespace
+
+int bitplane_kernel_name(const ConvArgs& a, char* buf, int len) {
+  const int pa = planes_of(a.a_bits), pw = planes_of(a.w_bits);
+  int tn = 0;
+#define QC_CASE(A, W) \
+  if (pa == A && pw == W) tn = default_tn<A, W>();
+  QC_CASE(1, 1)
+  QC_CASE(2, 1)
+  QC_CASE(1, 2)
+  QC_CASE(2, 2)
+  QC_CASE(4, 4)
+  QC_CASE(4, 1)
+  QC_CASE(1, 4)
+  QC_CASE(4, 2)
+  QC_CASE(2, 4)
+#undef QC_CASE
+  if (!tn) return QCONV_EUNSUPPORTED;
+  char name[96];
+  snprintf(name, sizeof(name), "conv_bitplane_kernel<%d, %d, %d, %s>", pa, pw, tn, a.pool ? "true" : "false");
+  if (buf && len > 0) snprintf(buf, (size_t)len, "%s", name);
+  return (int)strlen(name);
+}
 
 int launch_conv_bitplane(const ConvArgs& a, hipStream_t s) {
   const int pa = planes_of(a.a_bits), pw = planes_of(a.w_bits);

@@ -30,6 +30,7 @@
 // built with one wave ballot per (register, plane): lanes 0-31 give the 32
 // channels of one pixel, lanes 32-63 those of another, and the words are
 // moved into lanes with writelane so that each lane stores one pixel's word.
+#include <stdio.h>
 #include <string.h>
 
 #include <type_traits>
@@ -131,6 +132,7 @@ struct MfmaArgs {
   int out_bytes;      // byte size of the unpacked output (buffer-resource bound, < 2^31)
   int buf_bytes;      // LDS bytes of one halo buffer
   int grid;           // blocks launched (each loops over the work items)
+  int act_bytes;      // byte size of the packed activations (buffer-resource bound; 0 if >= 2^31)
 };
 
 __device__ __forceinline__ v16i mfma(v4i a, v4i b, v16i c) {
@@ -500,6 +502,18 @@ struct Item {
   int img0, u0, co_blk, iy0;
   int abase[MT];  // LDS byte offset (tap (0, 0), this lane's k-half) of the pixel fed into row r32 of each M-tile
 };
+
+// First image and first unit of work item w.
+__device__ __forceinline__ void item_units(const MfmaArgs& m, int w, int* img0, int* u0) {
+  const int pt = w / m.tiles_co;
+  if (m.ipb == 1) {
+    *img0 = pt / m.bpi;
+    *u0 = (pt - *img0 * m.bpi) * m.units_pb;
+  } else {
+    *img0 = pt * m.ipb;
+    *u0 = 0;
+  }
+}
 
 // Image and first input row of the halo tile of work item w.
 __device__ __forceinline__ void item_origin(const MfmaArgs& m, int w, int* img0, int* iy0) {
@@ -914,6 +928,375 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
   }
 }
 
+// Per-wave LDS buffer through which the store-overlapped kernel transposes
+// a 32 x 32 tile: rows of 40 words, so that the two channel rows one
+// ds_write_b32 covers (c and c + 4) fall in disjoint banks.
+constexpr int TR_STRIDE = 40;
+constexpr int TR_BYTES = 32 * TR_STRIDE * 4;
+
+// Epilogue of one tile of the swapped orientation (register v = 4q + i of
+// lane l: channel co32 + 8q + 4(l/32) + i, unit 32T + l%32) through LDS: the
+// accumulators go to a [channel][unit] buffer, and each lane reads back four
+// consecutive units of one channel, so that one 16-byte store per lane
+// writes eight whole 128-byte runs per instruction.  Same arithmetic as the
+// other epilogues, element by element.
+template <int KIND, bool RES, class AccT>
+__device__ __forceinline__ void tile_epilogue_lds(const MfmaArgs& m, const AccT& acc, int img0, int u0,
+                                                  int T, int co32, int co_blk, const float* prm,
+                                                  uint32_t* tr, int lane) {
+  const ConvArgs& a = m.c;
+  const int g = lane >> 5, r32 = lane & 31;
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t bits =
+          KIND == K_INT32 ? (uint32_t)acc_i(acc, 4 * q + i) : __float_as_uint(acc_f(acc, 4 * q + i));
+      tr[(8 * q + 4 * g + i) * TR_STRIDE + r32] = bits;
+    }
+  const int sub = lane & 7, crow = lane >> 3;
+  const float inv = 1.0f / (float)(1 << a.shift);
+  const int t0 = 32 * T + 4 * sub;
+  int img, uu;
+  const bool uok = unit_of(m, img0, u0, t0, &img, &uu);
+  const __amdgpu_buffer_rsrc_t orsrc =
+      __builtin_amdgcn_make_buffer_rsrc(a.out, (short)0, m.out_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rrsrc =
+      __builtin_amdgcn_make_buffer_rsrc((void*)(RES ? a.residual : (const float*)a.out), (short)0, m.out_bytes,
+                                        0x00020000);
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+    const int c = 8 * kk + crow;
+    const int co = co32 + c;
+    const uint4 v = *reinterpret_cast<const uint4*>(tr + c * TR_STRIDE + 4 * sub);
+    uint32_t o[4] = {v.x, v.y, v.z, v.w};
+    if constexpr (KIND != K_INT32) {
+      const float kc = prm[co - co_blk], bc = prm[128 + co - co_blk];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float z = __uint_as_float(o[e]) * inv;
+        if constexpr (KIND == K_SCALE) z = kc * z;
+        if constexpr (KIND == K_BNF32) z = fmaf(kc, z, bc);
+        o[e] = __float_as_uint(z);
+      }
+    }
+    const bool cok = co < a.cout;
+    if (m.vec) {
+      // four consecutive units of one image: one aligned 16-byte run
+      const int voff = (uok && cok) ? (int)((((int64_t)img * a.cout + co) * m.upi + uu) * 4) : 0x7FFFFFF0;
+      if constexpr (RES) {
+        {
+          const v4i r = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(rrsrc, voff, 0, 0));
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o[e] = __float_as_uint(__uint_as_float(o[e]) + __int_as_float(r[e]));
+        }
+      }
+      const v4i ov = {(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(__attribute__((ext_vector_type(4))) unsigned, ov),
+                                             orsrc, voff, 0, 0);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        int im, ue;
+        const bool ok = cok && unit_of(m, img0, u0, t0 + e, &im, &ue);
+        const int voff = ok ? (int)((((int64_t)im * a.cout + co) * m.upi + ue) * 4) : 0x7FFFFFF0;
+        uint32_t ov = o[e];
+        if constexpr (RES) {
+          ov = __float_as_uint(__uint_as_float(ov) +
+                                 __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rrsrc, voff, 0, 0)));
+        }
+        __builtin_amdgcn_raw_buffer_store_b32(ov, orsrc, voff, 0, 0);
+      }
+    }
+  }
+}
+
+// s_waitcnt vmcnt(0): every vector memory access of the wave has completed.
+__device__ __forceinline__ void vm_wait_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// Workgroup barrier that orders LDS accesses only: outstanding global
+// stores are not waited for, so they keep draining across it.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Packed words of this thread's share of a halo tile (as load_halo), read
+// through a buffer resource over the packed activations: every lane issues
+// every load, and words outside the image or past the last channel use an
+// offset past the end of the buffer, which reads as 0 (= Q(0)).  The
+// destination registers are written by the loads alone.
+template <int PA, int NI>
+__device__ __forceinline__ void load_halo_rsrc(const MfmaArgs& m, __amdgpu_buffer_rsrc_t rsrc, int img0,
+                                               int iy0, int tid, uint32_t (&raw)[NI][PA]) {
+  const ConvArgs& a = m.c;
+  const int items = m.ipb * m.slot_pix * m.chunk_words;
+  const int apix = a.cw * PA;
+#pragma unroll
+  for (int u = 0; u < NI; ++u) {
+    const int it = tid + 256 * u;
+    const int hp = (int)fdiv((uint32_t)it, m.fd_cwc);
+    const int cw = it - hp * m.chunk_words;
+    const int slot = (int)fdiv((uint32_t)hp, m.fd_slot);
+    const int rem = hp - slot * m.slot_pix;
+    const int hrow = (int)fdiv((uint32_t)rem, m.fd_hc);
+    const int hcol = rem - hrow * m.hc;
+    const int img = img0 + slot;
+    const int iy = iy0 + hrow, ix = hcol - a.pad;
+    const bool ok = it < items && img < a.n && iy >= 0 && iy < a.h && ix >= 0 && ix < a.w && cw < a.cw;
+    const int off = ok ? (((img * a.h + iy) * a.w + ix) * apix + cw * PA) * 4 : 0x7FFFFFF0;
+    if constexpr (PA == 1) {
+      raw[u][0] = __builtin_amdgcn_raw_buffer_load_b32(rsrc, off, 0, 0);
+    } else if constexpr (PA == 2) {
+      const auto v = __builtin_amdgcn_raw_buffer_load_b64(rsrc, off, 0, 0);
+      raw[u][0] = v[0];
+      raw[u][1] = v[1];
+    } else {
+      const auto v = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, 0);
+      raw[u][0] = v[0];
+      raw[u][1] = v[1];
+      raw[u][2] = v[2];
+      raw[u][3] = v[3];
+    }
+  }
+}
+
+// Layers whose output is written unpacked in fp32/int32 are bound by those
+// stores.  This variant alternates two groups of four waves in one block per
+// CU: while one group runs the MFMAs of an item, the other expands the halo
+// tile of its next item and stores the item it finished before, and the
+// roles swap at every LDS barrier.  The block's weights stay in LDS for the
+// whole launch (every item of a block has the same output channels); the
+// only global accesses of a computing group are the loads of its next halo
+// tile, issued first so that they arrive under the MFMAs.  The stores are
+// issued last in a phase and the barrier does not wait for them, so they
+// drain while the same group computes its next item.
+// The block's items are w = blockIdx.x + k * gridDim.x; group k % 2 owns
+// item k, computes it in phase k and stores it in phase k + 1; its halo
+// words are loaded in phase k - 2 (the prologue for k < 2) and expanded in
+// phase k - 1.  Each group runs its own loop over pairs of phases, so that
+// every path from one phase to the next is the program order (the loads of
+// a compute phase are always consumed by the following store phase).
+// LDS: parameters, weights [tap][k-step][k-half][channel][16 B], one halo
+// buffer per group, one tile-transpose buffer per wave of a group.  Needs a
+// single channel chunk, the swapped (unpacked, unpooled) epilogue and packed
+// activations below 2 GiB.
+template <int FP4, int PA, int CFG>
+__global__ __launch_bounds__(512, 1) void conv_mfma_pp_kernel(const MfmaArgs m) {
+  using O = OpT<FP4>;
+  using acc_t = typename O::acc_t;
+  using C = Cfg<CFG>;
+  constexpr int MT = C::MT, NT = C::NT, WN = C::WN;
+  constexpr int BCO = 32 * NT * WN;
+  constexpr int NI = PA == 4 ? 4 : 6;  // halo items per thread held in registers
+  static_assert(C::SK == 1, "one wave per output tile");
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds_raw[];
+  const ConvArgs& a = m.c;
+  const int tid = threadIdx.x, wave = tid >> 6;
+  const int grp = wave >> 2, wq = wave & 3;
+  const int wm = wq / WN, wn = wq - (wq / WN) * WN;
+  const int total = m.tiles_px * m.tiles_co;
+  if ((int)blockIdx.x >= total) return;
+  const int n_my = (total - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x;
+  const int taps = a.kh * a.kw;
+  const int ksteps = m.ksteps;
+  float* prm = reinterpret_cast<float*>(lds_raw);
+  uint8_t* bw = lds_raw + PARAM_BYTES;
+  const int bw_bytes = taps * ksteps * BCO * 32;
+  uint8_t* halo = bw + bw_bytes + grp * m.buf_bytes;
+  uint32_t* tr = reinterpret_cast<uint32_t*>(bw + bw_bytes + 2 * m.buf_bytes + wq * TR_BYTES);
+  const int co_blk = ((int)blockIdx.x % m.tiles_co) * BCO;  // gridDim.x is a multiple of tiles_co
+  const int co_w = co_blk + 32 * NT * wn;
+  const __amdgpu_buffer_rsrc_t arsrc =
+      __builtin_amdgcn_make_buffer_rsrc((void*)a.act, (short)0, m.act_bytes, 0x00020000);
+  auto item_w = [&](int k) { return (int)blockIdx.x + k * (int)gridDim.x; };
+
+  // ---- prologue: weights and parameters into LDS (eight 16-byte loads in
+  // flight per thread); group 0 stages item 0, group 1 loads item 1 ----
+  uint32_t raw[NI][PA];
+  {
+    const __amdgpu_buffer_rsrc_t brsrc =
+        __builtin_amdgcn_make_buffer_rsrc((void*)m.wx, (short)0, m.wx_bytes, 0x00020000);
+    const int chunks = taps * ksteps * BCO * 2;  // 16-byte pieces
+    for (int c0 = 0; c0 < chunks; c0 += 8 * 512) {
+      // a thread past the last piece copies the last piece again (same
+      // value, same place), so that every load is consumed
+      v4i v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int c = min(c0 + u * 512 + tid, chunks - 1);
+        const int tk = c / (2 * BCO);
+        const int rem = c - tk * (2 * BCO);
+        v[u] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(
+                                           brsrc, (tk * a.cop + co_blk + (rem >> 1)) * 32 + (rem & 1) * 16, 0, 0));
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int c = min(c0 + u * 512 + tid, chunks - 1);
+        const int tk = c / (2 * BCO);
+        const int rem = c - tk * (2 * BCO);
+        *reinterpret_cast<v4i*>(bw + ((tk * 2 + (rem & 1)) * BCO + (rem >> 1)) * 16) = v[u];
+      }
+    }
+    load_params<BCO>(a, co_blk, tid, prm);
+    int img0, iy0;
+    item_origin(m, item_w(grp < n_my ? grp : 0), &img0, &iy0);
+    load_halo_rsrc<PA, NI>(m, arsrc, img0, iy0, tid & 255, raw);
+    if (grp == 0) store_halo<FP4, PA, NI>(m, img0, iy0, 0, tid & 255, raw, halo);
+  }
+  // Explicit waits for every outstanding global access where that costs
+  // nothing (here, and at the start of each store phase, where the only ones
+  // are the halo loads of a phase ago): no load issued before them is then
+  // taken as pending anywhere in the loops below, so the compute phases
+  // never wait for the stores still draining from the phase before.
+  vm_wait_all();
+  lds_barrier();
+
+  // Accumulators and the loaded halo words are the only per-lane state
+  // carried from one phase to the next; the first (tap, k-step) of an item
+  // starts from a zero C operand, and the item geometry is recomputed in
+  // every phase.
+  acc_t acc[MT][NT];
+
+  // The thread index passes through an empty asm in every phase, so that the
+  // index arithmetic derived from it is recomputed there rather than hoisted
+  // out of the loops (where it would be held in scratch memory).
+  auto fresh_tid = [&]() {
+    int t = tid;
+    asm volatile("" : "+v"(t));
+    return t;
+  };
+
+  // compute item k; first the halo words of item k + 2
+  auto compute = [&](int k) {
+    const int ptid = fresh_tid();
+    const int plane = ptid & 63, pg = plane >> 5, pr32 = plane & 31;
+    if (k + 2 < n_my) {
+      int nimg0, niy0;
+      item_origin(m, item_w(k + 2), &nimg0, &niy0);
+      load_halo_rsrc<PA, NI>(m, arsrc, nimg0, niy0, ptid & 255, raw);
+    }
+    Item<MT> cur;
+    decode_item<MT, NT, WN>(m, item_w(k), wm, pr32, pg, &cur);
+    int boff[NT];
+#pragma unroll
+    for (int j = 0; j < NT; ++j) boff[j] = (32 * NT * wn + 32 * j + pr32) * 16 + pg * (BCO * 16);
+    // A (pixels) and B (weights) fragments from LDS in two register sets,
+    // each read one (tap, k-step) before its MFMAs
+    const int nsteps = taps * ksteps;
+    int t_ky = 0, t_kx = 0, t_ks = 0, t_tk = 0;
+    auto fetch = [&](v4i (&A)[MT], v4i (&B)[NT]) {
+      const int lo = (t_ky * m.hc + t_kx) * m.pix_bytes + t_ks * 32;
+#pragma unroll
+      for (int i = 0; i < MT; ++i) A[i] = *reinterpret_cast<const v4i*>(halo + cur.abase[i] + lo);
+      const uint8_t* bs = bw + t_tk * (2 * BCO * 16);
+#pragma unroll
+      for (int j = 0; j < NT; ++j) B[j] = *reinterpret_cast<const v4i*>(bs + boff[j]);
+      ++t_tk;
+      if (++t_ks == ksteps) {
+        t_ks = 0;
+        if (++t_kx == a.kw) {
+          t_kx = 0;
+          ++t_ky;
+        }
+      }
+    };
+    auto mm = [&](const v4i (&A)[MT], const v4i (&B)[NT]) {
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) acc[i][j] = mfma(B[j], A[i], acc[i][j]);
+    };
+    v4i AX[MT], BX[NT], AY[MT], BY[NT];
+    fetch(AX, BX);                  // step 0
+    if (nsteps > 1) fetch(AY, BY);  // step 1
+    {
+      const acc_t zero = {};
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) acc[i][j] = mfma(BX[j], AX[i], zero);
+    }
+    // steps 1 .. nsteps - 1 in pairs (Y, X); reads run one step ahead
+    int st = 1;
+    for (; st + 2 < nsteps; st += 2) {
+      fetch(AX, BX);  // step st + 1
+      mm(AY, BY);     // step st
+      fetch(AY, BY);  // step st + 2
+      mm(AX, BX);     // step st + 1
+    }
+    if (st < nsteps) {
+      if (st + 1 < nsteps) fetch(AX, BX);
+      mm(AY, BY);
+      if (st + 1 < nsteps) mm(AX, BX);
+    }
+  };
+
+  // expand the halo words of item k + 1 (loaded a phase ago), then store item k - 1
+  auto store = [&](int k) {
+    vm_wait_all();
+    const int ptid = fresh_tid();
+    const int plane = ptid & 63;
+    if (k + 1 < n_my) {
+      int nimg0, niy0;
+      item_origin(m, item_w(k + 1), &nimg0, &niy0);
+      store_halo<FP4, PA, NI>(m, nimg0, niy0, 0, ptid & 255, raw, halo);
+    }
+    if (k >= 1 && co_w < a.cout) {
+      int pimg0, pu0;
+      item_units(m, item_w(k - 1), &pimg0, &pu0);
+#pragma nounroll
+      for (int tt = 0; tt < MT * NT; ++tt) {
+        const int i = tt / NT, j = tt - (tt / NT) * NT;
+        const int co32 = co_w + 32 * j;
+        if (co32 >= a.cout) continue;
+        acc_t tcur;
+        switch (tt) {
+#define QC_PICK(K)                                         \
+  case K:                                                  \
+    if constexpr (K < MT * NT) tcur = acc[K / NT][K % NT]; \
+    break;
+          QC_PICK(0) QC_PICK(1) QC_PICK(2) QC_PICK(3) QC_PICK(4) QC_PICK(5) QC_PICK(6) QC_PICK(7)
+#undef QC_PICK
+          default: break;
+        }
+        const int T = wm * MT + i;
+        if (a.mode == QCONV_EPI_INT32)
+          tile_epilogue_lds<K_INT32, false>(m, tcur, pimg0, pu0, T, co32, co_blk, prm, tr, plane);
+        else if (a.mode == QCONV_EPI_SCALE_F32)
+          tile_epilogue_lds<K_SCALE, false>(m, tcur, pimg0, pu0, T, co32, co_blk, prm, tr, plane);
+        else if (!a.residual_on)
+          tile_epilogue_lds<K_BNF32, false>(m, tcur, pimg0, pu0, T, co32, co_blk, prm, tr, plane);
+        else
+          tile_epilogue_lds<K_BNF32, true>(m, tcur, pimg0, pu0, T, co32, co_blk, prm, tr, plane);
+      }
+    }
+  };
+
+  // phases 0 .. n_my: group 0 computes in the even ones, group 1 in the odd
+  // ones; both groups pass n_my + 1 barriers
+  if (grp == 0) {
+    for (int p = 0; p <= n_my; p += 2) {
+      if (p < n_my) compute(p);
+      lds_barrier();
+      if (p + 1 <= n_my) {
+        store(p + 1);
+        lds_barrier();
+      }
+    }
+  } else {
+    for (int p = 0; p <= n_my; p += 2) {
+      store(p);
+      lds_barrier();
+      if (p + 1 <= n_my) {
+        if (p + 1 < n_my) compute(p + 1);
+        lds_barrier();
+      }
+    }
+  }
+}
+
 bool plan(const ConvArgs& a, int cfg, MfmaArgs* m) {
   memset(m, 0, sizeof(*m));
   m->c = a;
@@ -997,6 +1380,8 @@ bool plan(const ConvArgs& a, int cfg, MfmaArgs* m) {
     const Thr& t = a.othr;
     m->ht_needed = (a.out_bits == 2 && t.t0 >= 1.0f) || (a.out_bits == 3 && t.t2 >= 1.0f);
   }
+  const int64_t ab = (int64_t)a.n * a.h * a.w * a.cw * planes_of(a.a_bits) * 4;
+  m->act_bytes = ab < ((int64_t)1 << 31) ? (int)ab : 0;
   const int64_t ob = (int64_t)a.n * a.cout * m->upi * 4;
   m->out_bytes = ob < ((int64_t)1 << 31) ? (int)ob : 0;
   m->buf_bytes = (m->halo_bytes + 15) & ~15;
@@ -1034,19 +1419,55 @@ bool use_swap(const MfmaArgs& m) {
   return !a.pool && a.out_packed == nullptr && a.mode != QCONV_EPI_BN_PACK && m.out_bytes > 0;
 }
 
+constexpr int LDS_PER_CU = 160 * 1024;
+
+int device_cus() {
+  int dev = 0, cus = 256;
+  if (hipGetDevice(&dev) == hipSuccess) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0) cus = v;
+  }
+  return cus;
+}
+
+// LDS bytes of one ping-pong block: parameters, the block's weights, one
+// halo buffer per group, one transpose buffer per wave of a group.
+size_t pp_lds(const MfmaArgs& m, int cfg) {
+  const int bco = cfg_block_co(cfg);
+  return PARAM_BYTES + (size_t)m.c.kh * m.c.kw * m.ksteps * bco * 32 + (size_t)m.buf_bytes * 2 + 4 * TR_BYTES;
+}
+
+// The ping-pong kernel serves 256-row shapes with unpacked, unpooled outputs
+// whose channels fit one stage and whose weights fit next to two halo
+// buffers, when every block gets at least one item per group.
+bool use_pp(const MfmaArgs& m, int cfg, int cus) {
+  if (cfg == 2 || !use_swap(m) || m.nchunks != 1 || m.act_bytes == 0) return false;
+  if (pp_lds(m, cfg) > (size_t)LDS_PER_CU) return false;
+  return (int64_t)m.tiles_px * m.tiles_co >= 2 * (int64_t)cus;
+}
+
 template <int FP4, int PA, int CFG>
 int launch_cfg(MfmaArgs m, hipStream_t s) {
   const size_t lds = block_lds(m);
   const int total = m.tiles_px * m.tiles_co;
+  const int cus = device_cus();
+  if constexpr (CFG != 2) {
+    if (use_pp(m, CFG, cus)) {
+      const size_t plds = pp_lds(m, CFG);
+      // every block keeps one output-channel tile: a multiple of tiles_co blocks
+      m.grid = max(m.tiles_co, (min(total, cus) / m.tiles_co) * m.tiles_co);
+      auto kern = conv_mfma_pp_kernel<FP4, PA, CFG>;
+      if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)plds) != hipSuccess)
+        return QCONV_EHIP;
+      kern<<<dim3((unsigned)m.grid), 512, plds, s>>>(m);
+      return hip_status();
+    }
+  }
   if (CFG == 2) {
     m.grid = total;  // split-K: one item per block
   } else {
-    int dev = 0, cus = 256;
-    if (hipGetDevice(&dev) == hipSuccess) {
-      int v = 0;
-      if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0) cus = v;
-    }
-    const int per_cu = max(1, min(2, (int)((160 * 1024) / lds)));
+    const int per_cu = max(1, min(2, (int)(LDS_PER_CU / lds)));
     m.grid = min(total, per_cu * cus);
   }
   if (use_swap(m))
@@ -1078,6 +1499,20 @@ bool mfma_supports(const ConvArgs& a) {
   if (a.stride > 2 || a.n == 0) return false;
   MfmaArgs m;
   return plan(a, pick_cfg(a), &m);
+}
+
+int mfma_kernel_name(const ConvArgs& a, char* buf, int len) {
+  MfmaArgs m;
+  const int cfg = pick_cfg(a);
+  if (!plan(a, cfg, &m)) return QCONV_EUNSUPPORTED;
+  char name[96];
+  if (use_pp(m, cfg, device_cus()))
+    snprintf(name, sizeof(name), "conv_mfma_pp_kernel<%d, %d, %d>", a.mfma_fp4, planes_of(a.a_bits), cfg);
+  else
+    snprintf(name, sizeof(name), "conv_mfma_kernel<%d, %d, %d, %d>", a.mfma_fp4, planes_of(a.a_bits), cfg,
+             use_swap(m) ? 1 : 0);
+  if (buf && len > 0) snprintf(buf, (size_t)len, "%s", name);
+  return (int)strlen(name);
 }
 
 int launch_conv_mfma(const ConvArgs& a, hipStream_t s) {

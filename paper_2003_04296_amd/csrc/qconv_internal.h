@@ -169,6 +169,10 @@ struct ConvArgs {
 int launch_conv_bitplane(const ConvArgs& a, hipStream_t s);
 int launch_conv_mfma(const ConvArgs& a, hipStream_t s);
 bool mfma_supports(const ConvArgs& a);
+// Name of the kernel instantiation each launcher would run (template
+// arguments as the profiler prints them); returns the name's length.
+int bitplane_kernel_name(const ConvArgs& a, char* buf, int len);
+int mfma_kernel_name(const ConvArgs& a, char* buf, int len);
 
 int launch_conv_f32(const float* x, const float* wt_t /* [cin][k][k][cout_pad32] */, int n, int cin,
                     int h, int w, int cout, int k, int stride, int pad, const float* bn_k,

@@ -219,6 +219,99 @@ def test_bn_residual_and_repack(dev, bits, algo, hw):
                                   oracle.quantize(oracle.hardtanh(zz), ab))
 
 
+# ---------------------------------------------------------------------------
+# the store-overlapped kernel: two wave groups per block alternate between
+# the MFMAs of one item and the stores of the previous one; chosen for
+# unpacked, unpooled outputs with at least two items per compute unit
+# ---------------------------------------------------------------------------
+
+PP_CASES = [
+    # n, cin, h, w, cout, k, stride, pad
+    (128, 128, 32, 32, 128, 3, 1, 1),  # 512 items of 256 pixels x 128 channels
+    (128, 64, 28, 28, 64, 3, 1, 1),    # 784-pixel images: ragged last item; 64-channel blocks
+    (64, 96, 32, 32, 256, 3, 1, 1),    # two channel tiles; cin padded to a whole k-step
+    (1023, 64, 16, 16, 128, 3, 2, 1),  # stride 2, two whole images per item, odd batch
+]
+
+
+def _kernel(case, ab, wb, algo, mode=q.EPI_INT32, flags=0):
+    n, cin, h, w, cout, k, s, p = case
+    return q.kernel_name(n, cin, h, w, cout, k, s, p, ab, wb, mode=mode, flags=flags, algo=algo)
+
+
+@pytest.mark.parametrize("bits", [(2, 1), (1, 1), (3, 3), (1, 2)])
+@pytest.mark.parametrize("case", PP_CASES)
+def test_pp_kernel_int32_bit_exact(dev, case, bits):
+    n, cin, h, w, cout, k, s, p = case
+    ab, wb = bits
+    name = _kernel(case, ab, wb, q.ALGO_MFMA_FP4)
+    assert name.startswith("conv_mfma_pp_kernel<1,"), name
+    x, wt = _inputs(300 + sum(case), n, cin, h, w, cout, k)
+    out, _, _ = _gpu_conv(dev, x, wt, ab, wb, s, p, algo=q.ALGO_MFMA_FP4)
+    want, _ = _oracle_acc(x, wt, ab, wb, s, p)
+    np.testing.assert_array_equal(out.cpu().numpy(), want)
+
+
+def test_pp_kernel_int8_operands(dev):
+    case = PP_CASES[1]
+    n, cin, h, w, cout, k, s, p = case
+    name = _kernel(case, 2, 2, q.ALGO_MFMA_I8)
+    assert name.startswith("conv_mfma_pp_kernel<0,"), name
+    x, wt = _inputs(310, n, cin, h, w, cout, k)
+    out, _, _ = _gpu_conv(dev, x, wt, 2, 2, s, p, algo=q.ALGO_MFMA_I8)
+    want, _ = _oracle_acc(x, wt, 2, 2, s, p)
+    np.testing.assert_array_equal(out.cpu().numpy(), want)
+
+
+@pytest.mark.parametrize("epi", ["scale", "bn", "bn_residual"])
+@pytest.mark.parametrize("ci", [1, 2])
+def test_pp_kernel_epilogues(dev, ci, epi):
+    case = PP_CASES[ci]
+    n, cin, h, w, cout, k, s, p = case
+    ab, wb = 2, 1
+    mode = q.EPI_SCALE_F32 if epi == "scale" else q.EPI_BN_F32
+    flags = q.EPI_RESIDUAL if epi == "bn_residual" else 0
+    name = _kernel(case, ab, wb, q.ALGO_AUTO, mode=mode, flags=flags)
+    assert name.startswith("conv_mfma_pp_kernel<1,"), name
+    x, wt = _inputs(320 + ci, n, cin, h, w, cout, k)
+    kk, bb = _bn(320 + ci, cout)
+    ho, wo = q.out_size(h, k, s, p), q.out_size(w, k, s, p)
+    res = synth.normal(synth.generator(321 + ci), (n, cout, ho, wo), 1.0)
+    act = q.pack_act(x.to(dev), ab)
+    wq, scale = q.pack_weight(wt.to(dev), wb)
+    kw = dict(mode=mode, flags=flags)
+    if epi == "scale":
+        kw["scale"] = scale
+    else:
+        kw.update(bn_k=kk.to(dev), bn_b=bb.to(dev))
+    if flags:
+        kw["residual"] = res.to(dev)
+    out, _ = q.conv(act, wq, n, cin, h, w, cout, k, s, p, ab, wb, **kw)
+    torch.cuda.synchronize()
+    acc, sc = _oracle_acc(x, wt, ab, wb, s, p)
+    shift = oracle.level_shift(ab) + oracle.level_shift(wb)
+    if epi == "scale":
+        want = oracle.epi_scale(acc, sc, shift)
+    else:
+        want = oracle.epi_bn(acc, kk.numpy(), bb.numpy(), shift)
+        if flags:
+            want = oracle.add(want, res.numpy())
+    np.testing.assert_array_equal(out.cpu().numpy(), want)
+
+
+def test_pp_kernel_repeated_launches_agree(dev):
+    """Back-to-back launches on one stream (the second overlapping the first's
+    drained stores) give identical outputs, also after an unrelated launch."""
+    case = PP_CASES[0]
+    n, cin, h, w, cout, k, s, p = case
+    x, wt = _inputs(330, n, cin, h, w, cout, k)
+    act = q.pack_act(x.to(dev), 2)
+    wq, _ = q.pack_weight(wt.to(dev), 1)
+    outs = [q.conv(act, wq, n, cin, h, w, cout, k, s, p, 2, 1)[0] for _ in range(3)]
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0], outs[1]) and torch.equal(outs[0], outs[2])
+
+
 POOL_CASES = [
     # n, cin, h, w, cout, k, stride, pad -- conv output widths 8, 16, 32, 64
     (3, 40, 8, 8, 70, 3, 1, 1),     # wo 8, two whole images per block, last block half empty
