@@ -375,14 +375,15 @@ __device__ __forceinline__ void tile_epilogue(const MfmaArgs& m, const AccT& acc
 }
 
 // Epilogue of one tile in the swapped orientation (weights as the A
-// operand): register v = 4q + i of lane l holds output channel
+// operand; RES: 0 no residual, 1 residual, 2 as the arguments say):
+// register v = 4q + i of lane l holds output channel
 // co32 + 8q + 4(l/32) + i of unit 32T + l%32.  Each register is one store
 // instruction writing two 128-byte runs (32 consecutive units of two
 // channels) through a buffer resource; the per-register part of the offset
 // is a scalar.  Lanes whose unit does not exist get an offset past the end
 // of the buffer, so their stores and residual loads are dropped.  The
 // block's per-channel parameters come from LDS.
-template <int KIND, class AccT>
+template <int KIND, int RES = 2, class AccT>
 __device__ __forceinline__ void tile_epilogue_swap(const MfmaArgs& m, const AccT& acc, int img0, int u0,
                                                    int T, int co32, int co_blk, const float* prm,
                                                    int lane) {
@@ -420,7 +421,7 @@ __device__ __forceinline__ void tile_epilogue_swap(const MfmaArgs& m, const AccT
         if constexpr (KIND == K_SCALE) z = kv[i] * z;
         if constexpr (KIND == K_BNF32) {
           z = fmaf(kv[i], z, bv[i]);
-          if (a.residual_on)
+          if (RES == 1 || (RES == 2 && a.residual_on))
             z = z + __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rrsrc, voff, so, 0));
         }
         bits = __float_as_uint(z);
@@ -928,89 +929,6 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
   }
 }
 
-// Per-wave LDS buffer through which the store-overlapped kernel transposes
-// a 32 x 32 tile: rows of 40 words, so that the two channel rows one
-// ds_write_b32 covers (c and c + 4) fall in disjoint banks.
-constexpr int TR_STRIDE = 40;
-constexpr int TR_BYTES = 32 * TR_STRIDE * 4;
-
-// Epilogue of one tile of the swapped orientation (register v = 4q + i of
-// lane l: channel co32 + 8q + 4(l/32) + i, unit 32T + l%32) through LDS: the
-// accumulators go to a [channel][unit] buffer, and each lane reads back four
-// consecutive units of one channel, so that one 16-byte store per lane
-// writes eight whole 128-byte runs per instruction.  Same arithmetic as the
-// other epilogues, element by element.
-template <int KIND, bool RES, class AccT>
-__device__ __forceinline__ void tile_epilogue_lds(const MfmaArgs& m, const AccT& acc, int img0, int u0,
-                                                  int T, int co32, int co_blk, const float* prm,
-                                                  uint32_t* tr, int lane) {
-  const ConvArgs& a = m.c;
-  const int g = lane >> 5, r32 = lane & 31;
-#pragma unroll
-  for (int q = 0; q < 4; ++q)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const uint32_t bits =
-          KIND == K_INT32 ? (uint32_t)acc_i(acc, 4 * q + i) : __float_as_uint(acc_f(acc, 4 * q + i));
-      tr[(8 * q + 4 * g + i) * TR_STRIDE + r32] = bits;
-    }
-  const int sub = lane & 7, crow = lane >> 3;
-  const float inv = 1.0f / (float)(1 << a.shift);
-  const int t0 = 32 * T + 4 * sub;
-  int img, uu;
-  const bool uok = unit_of(m, img0, u0, t0, &img, &uu);
-  const __amdgpu_buffer_rsrc_t orsrc =
-      __builtin_amdgcn_make_buffer_rsrc(a.out, (short)0, m.out_bytes, 0x00020000);
-  const __amdgpu_buffer_rsrc_t rrsrc =
-      __builtin_amdgcn_make_buffer_rsrc((void*)(RES ? a.residual : (const float*)a.out), (short)0, m.out_bytes,
-                                        0x00020000);
-#pragma unroll
-  for (int kk = 0; kk < 4; ++kk) {
-    const int c = 8 * kk + crow;
-    const int co = co32 + c;
-    const uint4 v = *reinterpret_cast<const uint4*>(tr + c * TR_STRIDE + 4 * sub);
-    uint32_t o[4] = {v.x, v.y, v.z, v.w};
-    if constexpr (KIND != K_INT32) {
-      const float kc = prm[co - co_blk], bc = prm[128 + co - co_blk];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        float z = __uint_as_float(o[e]) * inv;
-        if constexpr (KIND == K_SCALE) z = kc * z;
-        if constexpr (KIND == K_BNF32) z = fmaf(kc, z, bc);
-        o[e] = __float_as_uint(z);
-      }
-    }
-    const bool cok = co < a.cout;
-    if (m.vec) {
-      // four consecutive units of one image: one aligned 16-byte run
-      const int voff = (uok && cok) ? (int)((((int64_t)img * a.cout + co) * m.upi + uu) * 4) : 0x7FFFFFF0;
-      if constexpr (RES) {
-        {
-          const v4i r = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(rrsrc, voff, 0, 0));
-#pragma unroll
-          for (int e = 0; e < 4; ++e) o[e] = __float_as_uint(__uint_as_float(o[e]) + __int_as_float(r[e]));
-        }
-      }
-      const v4i ov = {(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
-      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(__attribute__((ext_vector_type(4))) unsigned, ov),
-                                             orsrc, voff, 0, 0);
-    } else {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        int im, ue;
-        const bool ok = cok && unit_of(m, img0, u0, t0 + e, &im, &ue);
-        const int voff = ok ? (int)((((int64_t)im * a.cout + co) * m.upi + ue) * 4) : 0x7FFFFFF0;
-        uint32_t ov = o[e];
-        if constexpr (RES) {
-          ov = __float_as_uint(__uint_as_float(ov) +
-                                 __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rrsrc, voff, 0, 0)));
-        }
-        __builtin_amdgcn_raw_buffer_store_b32(ov, orsrc, voff, 0, 0);
-      }
-    }
-  }
-}
-
 // s_waitcnt vmcnt(0): every vector memory access of the wave has completed.
 __device__ __forceinline__ void vm_wait_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
@@ -1022,12 +940,13 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-// Packed words of this thread's share of a halo tile (as load_halo), read
-// through a buffer resource over the packed activations: every lane issues
-// every load, and words outside the image or past the last channel use an
-// offset past the end of the buffer, which reads as 0 (= Q(0)).  The
-// destination registers are written by the loads alone.
-template <int PA, int NI>
+// Packed words of this thread's share of a halo tile (items it = tid +
+// STRIDE u, as in load_halo), read through a buffer resource over the packed
+// activations: every lane issues every load, and words outside the image or
+// past the last channel use an offset past the end of the buffer, which
+// reads as 0 (= Q(0)).  The destination registers are written by the loads
+// alone.
+template <int PA, int NI, int STRIDE>
 __device__ __forceinline__ void load_halo_rsrc(const MfmaArgs& m, __amdgpu_buffer_rsrc_t rsrc, int img0,
                                                int iy0, int tid, uint32_t (&raw)[NI][PA]) {
   const ConvArgs& a = m.c;
@@ -1035,7 +954,7 @@ __device__ __forceinline__ void load_halo_rsrc(const MfmaArgs& m, __amdgpu_buffe
   const int apix = a.cw * PA;
 #pragma unroll
   for (int u = 0; u < NI; ++u) {
-    const int it = tid + 256 * u;
+    const int it = tid + STRIDE * u;
     const int hp = (int)fdiv((uint32_t)it, m.fd_cwc);
     const int cw = it - hp * m.chunk_words;
     const int slot = (int)fdiv((uint32_t)hp, m.fd_slot);
@@ -1062,16 +981,56 @@ __device__ __forceinline__ void load_halo_rsrc(const MfmaArgs& m, __amdgpu_buffe
   }
 }
 
+// Expands a thread's share of a halo tile into LDS: the NI items held in raw,
+// then the items past NI * STRIDE, loaded here one at a time.
+template <int FP4, int PA, int NI, int STRIDE>
+__device__ __forceinline__ void expand_halo(const MfmaArgs& m, __amdgpu_buffer_rsrc_t rsrc, int img0, int iy0,
+                                            int tid, const uint32_t (&raw)[NI][PA], uint8_t* buf) {
+  const int items = m.ipb * m.slot_pix * m.chunk_words;
+#pragma unroll
+  for (int u = 0; u < NI; ++u) {
+    const int it = tid + STRIDE * u;
+    if (it < items) {
+      const int hp = (int)fdiv((uint32_t)it, m.fd_cwc);
+      expand_to_lds<FP4, PA>(raw[u], buf + hp * m.pix_bytes + (it - hp * m.chunk_words) * OpT<FP4>::WORD_BYTES);
+    }
+  }
+  for (int it0 = NI * STRIDE; it0 < items; it0 += STRIDE) {
+    uint32_t one[1][PA];
+    load_halo_rsrc<PA, 1, STRIDE>(m, rsrc, img0, iy0, it0 + tid, one);
+    const int it = it0 + tid;
+    if (it < items) {
+      const int hp = (int)fdiv((uint32_t)it, m.fd_cwc);
+      expand_to_lds<FP4, PA>(one[0], buf + hp * m.pix_bytes + (it - hp * m.chunk_words) * OpT<FP4>::WORD_BYTES);
+    }
+  }
+}
+
+// Block shapes of the store-overlapped kernel: a group of 8 waves covers 256
+// units x BCO channels, WM x WN waves of MT x NT tiles of 32 x 32.
+template <int CFG>
+struct PCfg;
+template <>
+struct PCfg<0> {  // 256 x 128
+  static constexpr int WM = 4, WN = 2, MT = 2, NT = 2;
+};
+template <>
+struct PCfg<1> {  // 256 x 64
+  static constexpr int WM = 4, WN = 2, MT = 2, NT = 1;
+};
+constexpr int PP_GROUP = 512;  // threads per wave group
+
 // Layers whose output is written unpacked in fp32/int32 are bound by those
-// stores.  This variant alternates two groups of four waves in one block per
-// CU: while one group runs the MFMAs of an item, the other expands the halo
-// tile of its next item and stores the item it finished before, and the
-// roles swap at every LDS barrier.  The block's weights stay in LDS for the
-// whole launch (every item of a block has the same output channels); the
-// only global accesses of a computing group are the loads of its next halo
-// tile, issued first so that they arrive under the MFMAs.  The stores are
-// issued last in a phase and the barrier does not wait for them, so they
-// drain while the same group computes its next item.
+// stores, and the store rate of a CU grows with the number of waves that
+// store at once.  This variant runs 16 waves in one block per CU, in two
+// groups of eight: while one group runs the MFMAs of an item, the other
+// expands the halo tile of its next item and stores the item it finished
+// before, and the roles swap at every LDS barrier.  The block's weights stay
+// in LDS for the whole launch (every item of a block has the same output
+// channels); the only global accesses of a computing group are the loads of
+// its next halo tile, issued first so that they arrive under the MFMAs.  The
+// stores are issued last in a phase and the barrier does not wait for them,
+// so they drain while the same group computes its next item.
 // The block's items are w = blockIdx.x + k * gridDim.x; group k % 2 owns
 // item k, computes it in phase k and stores it in phase k + 1; its halo
 // words are loaded in phase k - 2 (the prologue for k < 2) and expanded in
@@ -1079,22 +1038,21 @@ __device__ __forceinline__ void load_halo_rsrc(const MfmaArgs& m, __amdgpu_buffe
 // every path from one phase to the next is the program order (the loads of
 // a compute phase are always consumed by the following store phase).
 // LDS: parameters, weights [tap][k-step][k-half][channel][16 B], one halo
-// buffer per group, one tile-transpose buffer per wave of a group.  Needs a
-// single channel chunk, the swapped (unpacked, unpooled) epilogue and packed
-// activations below 2 GiB.
+// buffer per group.  Needs a single channel chunk, the swapped (unpacked,
+// unpooled) epilogue and packed activations below 2 GiB.
 template <int FP4, int PA, int CFG>
-__global__ __launch_bounds__(512, 1) void conv_mfma_pp_kernel(const MfmaArgs m) {
+__global__ __launch_bounds__(1024, 1) void conv_mfma_pp_kernel(const MfmaArgs m) {
   using O = OpT<FP4>;
   using acc_t = typename O::acc_t;
-  using C = Cfg<CFG>;
+  using C = PCfg<CFG>;
   constexpr int MT = C::MT, NT = C::NT, WN = C::WN;
   constexpr int BCO = 32 * NT * WN;
-  constexpr int NI = PA == 4 ? 4 : 6;  // halo items per thread held in registers
-  static_assert(C::SK == 1, "one wave per output tile");
+  constexpr int NI = PA == 4 ? 2 : 3;  // halo items per thread held in registers
   extern __shared__ __attribute__((aligned(16))) uint8_t lds_raw[];
   const ConvArgs& a = m.c;
-  const int tid = threadIdx.x, wave = tid >> 6;
-  const int grp = wave >> 2, wq = wave & 3;
+  // wave-uniform indices in scalar registers
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = wave >> 3, wq = wave & 7;
   const int wm = wq / WN, wn = wq - (wq / WN) * WN;
   const int total = m.tiles_px * m.tiles_co;
   if ((int)blockIdx.x >= total) return;
@@ -1105,46 +1063,46 @@ __global__ __launch_bounds__(512, 1) void conv_mfma_pp_kernel(const MfmaArgs m) 
   uint8_t* bw = lds_raw + PARAM_BYTES;
   const int bw_bytes = taps * ksteps * BCO * 32;
   uint8_t* halo = bw + bw_bytes + grp * m.buf_bytes;
-  uint32_t* tr = reinterpret_cast<uint32_t*>(bw + bw_bytes + 2 * m.buf_bytes + wq * TR_BYTES);
   const int co_blk = ((int)blockIdx.x % m.tiles_co) * BCO;  // gridDim.x is a multiple of tiles_co
   const int co_w = co_blk + 32 * NT * wn;
   const __amdgpu_buffer_rsrc_t arsrc =
       __builtin_amdgcn_make_buffer_rsrc((void*)a.act, (short)0, m.act_bytes, 0x00020000);
   auto item_w = [&](int k) { return (int)blockIdx.x + k * (int)gridDim.x; };
 
-  // ---- prologue: weights and parameters into LDS (eight 16-byte loads in
-  // flight per thread); group 0 stages item 0, group 1 loads item 1 ----
+  // ---- prologue: each group loads the halo words of its first item, the
+  // weights and parameters go into LDS (four 16-byte loads in flight per
+  // thread), then group 0 expands item 0 ----
   uint32_t raw[NI][PA];
+  int img0, iy0;
+  item_origin(m, item_w(grp < n_my ? grp : 0), &img0, &iy0);
+  load_halo_rsrc<PA, NI, PP_GROUP>(m, arsrc, img0, iy0, tid & (PP_GROUP - 1), raw);
   {
     const __amdgpu_buffer_rsrc_t brsrc =
         __builtin_amdgcn_make_buffer_rsrc((void*)m.wx, (short)0, m.wx_bytes, 0x00020000);
     const int chunks = taps * ksteps * BCO * 2;  // 16-byte pieces
-    for (int c0 = 0; c0 < chunks; c0 += 8 * 512) {
+    for (int c0 = 0; c0 < chunks; c0 += 4 * 1024) {
       // a thread past the last piece copies the last piece again (same
       // value, same place), so that every load is consumed
-      v4i v[8];
+      v4i v[4];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int c = min(c0 + u * 512 + tid, chunks - 1);
+      for (int u = 0; u < 4; ++u) {
+        const int c = min(c0 + u * 1024 + tid, chunks - 1);
         const int tk = c / (2 * BCO);
         const int rem = c - tk * (2 * BCO);
         v[u] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(
                                            brsrc, (tk * a.cop + co_blk + (rem >> 1)) * 32 + (rem & 1) * 16, 0, 0));
       }
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int c = min(c0 + u * 512 + tid, chunks - 1);
+      for (int u = 0; u < 4; ++u) {
+        const int c = min(c0 + u * 1024 + tid, chunks - 1);
         const int tk = c / (2 * BCO);
         const int rem = c - tk * (2 * BCO);
         *reinterpret_cast<v4i*>(bw + ((tk * 2 + (rem & 1)) * BCO + (rem >> 1)) * 16) = v[u];
       }
     }
     load_params<BCO>(a, co_blk, tid, prm);
-    int img0, iy0;
-    item_origin(m, item_w(grp < n_my ? grp : 0), &img0, &iy0);
-    load_halo_rsrc<PA, NI>(m, arsrc, img0, iy0, tid & 255, raw);
-    if (grp == 0) store_halo<FP4, PA, NI>(m, img0, iy0, 0, tid & 255, raw, halo);
   }
+  if (grp == 0) expand_halo<FP4, PA, NI, PP_GROUP>(m, arsrc, img0, iy0, tid & (PP_GROUP - 1), raw, halo);
   // Explicit waits for every outstanding global access where that costs
   // nothing (here, and at the start of each store phase, where the only ones
   // are the halo loads of a phase ago): no load issued before them is then
@@ -1175,7 +1133,7 @@ __global__ __launch_bounds__(512, 1) void conv_mfma_pp_kernel(const MfmaArgs m) 
     if (k + 2 < n_my) {
       int nimg0, niy0;
       item_origin(m, item_w(k + 2), &nimg0, &niy0);
-      load_halo_rsrc<PA, NI>(m, arsrc, nimg0, niy0, ptid & 255, raw);
+      load_halo_rsrc<PA, NI, PP_GROUP>(m, arsrc, nimg0, niy0, ptid & (PP_GROUP - 1), raw);
     }
     Item<MT> cur;
     decode_item<MT, NT, WN>(m, item_w(k), wm, pr32, pg, &cur);
@@ -1241,7 +1199,7 @@ __global__ __launch_bounds__(512, 1) void conv_mfma_pp_kernel(const MfmaArgs m) 
     if (k + 1 < n_my) {
       int nimg0, niy0;
       item_origin(m, item_w(k + 1), &nimg0, &niy0);
-      store_halo<FP4, PA, NI>(m, nimg0, niy0, 0, ptid & 255, raw, halo);
+      expand_halo<FP4, PA, NI, PP_GROUP>(m, arsrc, nimg0, niy0, ptid & (PP_GROUP - 1), raw, halo);
     }
     if (k >= 1 && co_w < a.cout) {
       int pimg0, pu0;
@@ -1257,19 +1215,19 @@ __global__ __launch_bounds__(512, 1) void conv_mfma_pp_kernel(const MfmaArgs m) 
   case K:                                                  \
     if constexpr (K < MT * NT) tcur = acc[K / NT][K % NT]; \
     break;
-          QC_PICK(0) QC_PICK(1) QC_PICK(2) QC_PICK(3) QC_PICK(4) QC_PICK(5) QC_PICK(6) QC_PICK(7)
+          QC_PICK(0) QC_PICK(1) QC_PICK(2) QC_PICK(3)
 #undef QC_PICK
           default: break;
         }
         const int T = wm * MT + i;
         if (a.mode == QCONV_EPI_INT32)
-          tile_epilogue_lds<K_INT32, false>(m, tcur, pimg0, pu0, T, co32, co_blk, prm, tr, plane);
+          tile_epilogue_swap<K_INT32, 0>(m, tcur, pimg0, pu0, T, co32, co_blk, prm, plane);
         else if (a.mode == QCONV_EPI_SCALE_F32)
-          tile_epilogue_lds<K_SCALE, false>(m, tcur, pimg0, pu0, T, co32, co_blk, prm, tr, plane);
+          tile_epilogue_swap<K_SCALE, 0>(m, tcur, pimg0, pu0, T, co32, co_blk, prm, plane);
         else if (!a.residual_on)
-          tile_epilogue_lds<K_BNF32, false>(m, tcur, pimg0, pu0, T, co32, co_blk, prm, tr, plane);
+          tile_epilogue_swap<K_BNF32, 0>(m, tcur, pimg0, pu0, T, co32, co_blk, prm, plane);
         else
-          tile_epilogue_lds<K_BNF32, true>(m, tcur, pimg0, pu0, T, co32, co_blk, prm, tr, plane);
+          tile_epilogue_swap<K_BNF32, 1>(m, tcur, pimg0, pu0, T, co32, co_blk, prm, plane);
       }
     }
   };
@@ -1430,11 +1388,11 @@ int device_cus() {
   return cus;
 }
 
-// LDS bytes of one ping-pong block: parameters, the block's weights, one
-// halo buffer per group, one transpose buffer per wave of a group.
+// LDS bytes of one store-overlapped block: parameters, the block's weights,
+// one halo buffer per group.
 size_t pp_lds(const MfmaArgs& m, int cfg) {
   const int bco = cfg_block_co(cfg);
-  return PARAM_BYTES + (size_t)m.c.kh * m.c.kw * m.ksteps * bco * 32 + (size_t)m.buf_bytes * 2 + 4 * TR_BYTES;
+  return PARAM_BYTES + (size_t)m.c.kh * m.c.kw * m.ksteps * bco * 32 + (size_t)m.buf_bytes * 2;
 }
 
 // The ping-pong kernel serves 256-row shapes with unpacked, unpooled outputs
@@ -1460,7 +1418,7 @@ int launch_cfg(MfmaArgs m, hipStream_t s) {
       if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
                               (int)plds) != hipSuccess)
         return QCONV_EHIP;
-      kern<<<dim3((unsigned)m.grid), 512, plds, s>>>(m);
+      kern<<<dim3((unsigned)m.grid), 2 * PP_GROUP, plds, s>>>(m);
       return hip_status();
     }
   }
