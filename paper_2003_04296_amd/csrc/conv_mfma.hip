@@ -1038,8 +1038,9 @@ constexpr int PP_GROUP = 512;  // threads per wave group
 // every path from one phase to the next is the program order (the loads of
 // a compute phase are always consumed by the following store phase).
 // LDS: parameters, weights [tap][k-step][k-half][channel][16 B], one halo
-// buffer per group.  Needs a single channel chunk, the swapped (unpacked,
-// unpooled) epilogue and packed activations below 2 GiB.
+// buffer per group.  Serves unpacked, unpooled outputs (pixels as the A
+// operand, so that a lane holds one channel); needs a single channel chunk
+// and packed activations below 2 GiB.
 template <int FP4, int PA, int CFG>
 __global__ __launch_bounds__(1024, 1) void conv_mfma_pp_kernel(const MfmaArgs m) {
   using O = OpT<FP4>;
@@ -1067,42 +1068,45 @@ __global__ __launch_bounds__(1024, 1) void conv_mfma_pp_kernel(const MfmaArgs m)
   const int co_w = co_blk + 32 * NT * wn;
   const __amdgpu_buffer_rsrc_t arsrc =
       __builtin_amdgcn_make_buffer_rsrc((void*)a.act, (short)0, m.act_bytes, 0x00020000);
-  auto item_w = [&](int k) { return (int)blockIdx.x + k * (int)gridDim.x; };
+  auto item_w = [&](int k) __attribute__((always_inline)) { return (int)blockIdx.x + k * (int)gridDim.x; };
 
-  // ---- prologue: each group loads the halo words of its first item, the
-  // weights and parameters go into LDS (four 16-byte loads in flight per
-  // thread), then group 0 expands item 0 ----
+  // ---- prologue: each group loads the halo words of its first item; group
+  // 1 then copies the weights and parameters into LDS (up to eight 16-byte
+  // loads in flight per thread, all issued before the first is used) while
+  // group 0 expands item 0 ----
   uint32_t raw[NI][PA];
+  const int gtid0 = tid & (PP_GROUP - 1);
   int img0, iy0;
   item_origin(m, item_w(grp < n_my ? grp : 0), &img0, &iy0);
-  load_halo_rsrc<PA, NI, PP_GROUP>(m, arsrc, img0, iy0, tid & (PP_GROUP - 1), raw);
-  {
+  load_halo_rsrc<PA, NI, PP_GROUP>(m, arsrc, img0, iy0, gtid0, raw);
+  if (grp == 1) {
     const __amdgpu_buffer_rsrc_t brsrc =
         __builtin_amdgcn_make_buffer_rsrc((void*)m.wx, (short)0, m.wx_bytes, 0x00020000);
     const int chunks = taps * ksteps * BCO * 2;  // 16-byte pieces
-    for (int c0 = 0; c0 < chunks; c0 += 4 * 1024) {
+    for (int c0 = 0; c0 < chunks; c0 += 8 * PP_GROUP) {
       // a thread past the last piece copies the last piece again (same
       // value, same place), so that every load is consumed
-      v4i v[4];
+      v4i v[8];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int c = min(c0 + u * 1024 + tid, chunks - 1);
+      for (int u = 0; u < 8; ++u) {
+        const int c = min(c0 + u * PP_GROUP + gtid0, chunks - 1);
         const int tk = c / (2 * BCO);
         const int rem = c - tk * (2 * BCO);
         v[u] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(
                                            brsrc, (tk * a.cop + co_blk + (rem >> 1)) * 32 + (rem & 1) * 16, 0, 0));
       }
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int c = min(c0 + u * 1024 + tid, chunks - 1);
+      for (int u = 0; u < 8; ++u) {
+        const int c = min(c0 + u * PP_GROUP + gtid0, chunks - 1);
         const int tk = c / (2 * BCO);
         const int rem = c - tk * (2 * BCO);
         *reinterpret_cast<v4i*>(bw + ((tk * 2 + (rem & 1)) * BCO + (rem >> 1)) * 16) = v[u];
       }
     }
-    load_params<BCO>(a, co_blk, tid, prm);
+    load_params<BCO>(a, co_blk, gtid0, prm);
+  } else {
+    expand_halo<FP4, PA, NI, PP_GROUP>(m, arsrc, img0, iy0, gtid0, raw, halo);
   }
-  if (grp == 0) expand_halo<FP4, PA, NI, PP_GROUP>(m, arsrc, img0, iy0, tid & (PP_GROUP - 1), raw, halo);
   // Explicit waits for every outstanding global access where that costs
   // nothing (here, and at the start of each store phase, where the only ones
   // are the halo loads of a phase ago): no load issued before them is then
@@ -1120,14 +1124,14 @@ __global__ __launch_bounds__(1024, 1) void conv_mfma_pp_kernel(const MfmaArgs m)
   // The thread index passes through an empty asm in every phase, so that the
   // index arithmetic derived from it is recomputed there rather than hoisted
   // out of the loops (where it would be held in scratch memory).
-  auto fresh_tid = [&]() {
+  auto fresh_tid = [&]() __attribute__((always_inline)) {
     int t = tid;
     asm volatile("" : "+v"(t));
     return t;
   };
 
   // compute item k; first the halo words of item k + 2
-  auto compute = [&](int k) {
+  auto compute = [&](int k) __attribute__((always_inline)) {
     const int ptid = fresh_tid();
     const int plane = ptid & 63, pg = plane >> 5, pr32 = plane & 31;
     if (k + 2 < n_my) {
@@ -1191,43 +1195,56 @@ __global__ __launch_bounds__(1024, 1) void conv_mfma_pp_kernel(const MfmaArgs m)
     }
   };
 
-  // expand the halo words of item k + 1 (loaded a phase ago), then store item k - 1
-  auto store = [&](int k) {
+  // store item k - 1 and expand the halo words of item k + 1 (loaded a
+  // phase ago), one halo item after each tile's stores: the stores' issue is
+  // limited by the memory system, and the expansion fills those stalls
+  auto store = [&](int k) __attribute__((always_inline)) {
     vm_wait_all();
     const int ptid = fresh_tid();
-    const int plane = ptid & 63;
-    if (k + 1 < n_my) {
-      int nimg0, niy0;
-      item_origin(m, item_w(k + 1), &nimg0, &niy0);
-      expand_halo<FP4, PA, NI, PP_GROUP>(m, arsrc, nimg0, niy0, ptid & (PP_GROUP - 1), raw, halo);
-    }
-    if (k >= 1 && co_w < a.cout) {
-      int pimg0, pu0;
-      item_units(m, item_w(k - 1), &pimg0, &pu0);
-#pragma nounroll
-      for (int tt = 0; tt < MT * NT; ++tt) {
-        const int i = tt / NT, j = tt - (tt / NT) * NT;
-        const int co32 = co_w + 32 * j;
-        if (co32 >= a.cout) continue;
-        acc_t tcur;
-        switch (tt) {
-#define QC_PICK(K)                                         \
-  case K:                                                  \
-    if constexpr (K < MT * NT) tcur = acc[K / NT][K % NT]; \
-    break;
-          QC_PICK(0) QC_PICK(1) QC_PICK(2) QC_PICK(3)
-#undef QC_PICK
-          default: break;
-        }
+    const int plane = ptid & 63, gt = ptid & (PP_GROUP - 1);
+    const bool stage = k + 1 < n_my;
+    int nimg0 = 0, niy0 = 0;
+    if (stage) item_origin(m, item_w(k + 1), &nimg0, &niy0);
+    const int items = m.ipb * m.slot_pix * m.chunk_words;
+    auto expand_one = [&](auto UI) __attribute__((always_inline)) {
+      constexpr int U = decltype(UI)::value;
+      const int it = gt + PP_GROUP * U;
+      if (stage && it < items) {
+        const int hp = (int)fdiv((uint32_t)it, m.fd_cwc);
+        expand_to_lds<FP4, PA>(raw[U], halo + hp * m.pix_bytes + (it - hp * m.chunk_words) * O::WORD_BYTES);
+      }
+    };
+    const bool st = k >= 1 && co_w < a.cout;
+    int pimg0 = 0, pu0 = 0;
+    if (st) item_units(m, item_w(k - 1), &pimg0, &pu0);
+    Unroll<0, MT * NT>::run([&](auto TI) __attribute__((always_inline)) {
+      constexpr int TT = decltype(TI)::value;
+      constexpr int i = TT / NT, j = TT % NT;
+      const int co32 = co_w + 32 * j;
+      if (st && co32 < a.cout) {
         const int T = wm * MT + i;
         if (a.mode == QCONV_EPI_INT32)
-          tile_epilogue_swap<K_INT32, 0>(m, tcur, pimg0, pu0, T, co32, co_blk, prm, plane);
+          tile_epilogue_swap<K_INT32, 0>(m, acc[i][j], pimg0, pu0, T, co32, co_blk, prm, plane);
         else if (a.mode == QCONV_EPI_SCALE_F32)
-          tile_epilogue_swap<K_SCALE, 0>(m, tcur, pimg0, pu0, T, co32, co_blk, prm, plane);
+          tile_epilogue_swap<K_SCALE, 0>(m, acc[i][j], pimg0, pu0, T, co32, co_blk, prm, plane);
         else if (!a.residual_on)
-          tile_epilogue_swap<K_BNF32, 0>(m, tcur, pimg0, pu0, T, co32, co_blk, prm, plane);
+          tile_epilogue_swap<K_BNF32, 0>(m, acc[i][j], pimg0, pu0, T, co32, co_blk, prm, plane);
         else
-          tile_epilogue_swap<K_BNF32, 1>(m, tcur, pimg0, pu0, T, co32, co_blk, prm, plane);
+          tile_epilogue_swap<K_BNF32, 1>(m, acc[i][j], pimg0, pu0, T, co32, co_blk, prm, plane);
+      }
+      if constexpr (TT < NI) expand_one(std::integral_constant<int, TT>{});
+    });
+    Unroll<(MT * NT < NI ? MT * NT : NI), NI>::run([&](auto UI) __attribute__((always_inline)) { expand_one(UI); });
+    // halo items past NI per thread (large tiles): loaded here, one at a time
+    if (stage) {
+      for (int it0 = NI * PP_GROUP; it0 < items; it0 += PP_GROUP) {
+        uint32_t one[1][PA];
+        load_halo_rsrc<PA, 1, PP_GROUP>(m, arsrc, nimg0, niy0, it0 + gt, one);
+        const int it = it0 + gt;
+        if (it < items) {
+          const int hp = (int)fdiv((uint32_t)it, m.fd_cwc);
+          expand_to_lds<FP4, PA>(one[0], halo + hp * m.pix_bytes + (it - hp * m.chunk_words) * O::WORD_BYTES);
+        }
       }
     }
   };
