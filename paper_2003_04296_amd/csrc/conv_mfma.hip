@@ -33,6 +33,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <atomic>
 #include <type_traits>
 
 #include "qconv_internal.h"
@@ -1396,13 +1397,22 @@ bool use_swap(const MfmaArgs& m) {
 
 constexpr int LDS_PER_CU = 160 * 1024;
 
+constexpr int MAX_DEVICES = 64;
+
+// Compute units of the current device, queried once per device.
 int device_cus() {
-  int dev = 0, cus = 256;
-  if (hipGetDevice(&dev) == hipSuccess) {
-    int v = 0;
-    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0) cus = v;
+  static std::atomic<int> cache[MAX_DEVICES];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  const bool cached = dev >= 0 && dev < MAX_DEVICES;
+  if (cached) {
+    const int c = cache[dev].load(std::memory_order_relaxed);
+    if (c > 0) return c;
   }
-  return cus;
+  int v = 0;
+  if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) return 256;
+  if (cached) cache[dev].store(v, std::memory_order_relaxed);
+  return v;
 }
 
 // LDS bytes of one store-overlapped block: parameters, the block's weights,
@@ -1432,9 +1442,17 @@ int launch_cfg(MfmaArgs m, hipStream_t s) {
       // every block keeps one output-channel tile: a multiple of tiles_co blocks
       m.grid = max(m.tiles_co, (min(total, cus) / m.tiles_co) * m.tiles_co);
       auto kern = conv_mfma_pp_kernel<FP4, PA, CFG>;
-      if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
-                              (int)plds) != hipSuccess)
-        return QCONV_EHIP;
+      // the dynamic-LDS limit of this instantiation, raised once per device
+      static std::atomic<int> lds_set[MAX_DEVICES];
+      int dev = 0;
+      if (hipGetDevice(&dev) != hipSuccess) return QCONV_EHIP;
+      std::atomic<int>* done = (dev >= 0 && dev < MAX_DEVICES) ? &lds_set[dev] : nullptr;
+      if (!done || done->load(std::memory_order_relaxed) < (int)plds) {
+        if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)plds) != hipSuccess)
+          return QCONV_EHIP;
+        if (done) done->store((int)plds, std::memory_order_relaxed);
+      }
       kern<<<dim3((unsigned)m.grid), 2 * PP_GROUP, plds, s>>>(m);
       return hip_status();
     }
