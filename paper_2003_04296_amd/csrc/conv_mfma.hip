@@ -375,9 +375,29 @@ __device__ __forceinline__ void tile_epilogue(const MfmaArgs& m, const AccT& acc
   }
 }
 
+// Residual values of one tile of the swapped orientation (register
+// v = 4q + i of lane l: channel co32 + 8q + 4(l/32) + i, unit 32T + l%32),
+// loaded in one batch: on gfx9 loads and stores share one in-order counter,
+// so a residual load issued after a store also waits for that store.
+__device__ __forceinline__ void swap_res_load(const MfmaArgs& m, int img0, int u0, int T, int co32, int lane,
+                                              float (&r)[16]) {
+  const ConvArgs& a = m.c;
+  const int g = lane >> 5, r32 = lane & 31;
+  int img, uu;
+  const bool uok = unit_of(m, img0, u0, 32 * T + r32, &img, &uu);
+  const int voff = uok ? (int)((((int64_t)img * a.cout + co32 + 4 * g) * m.upi + uu) * 4) : 0x7FFFFFF0;
+  const __amdgpu_buffer_rsrc_t rrsrc =
+      __builtin_amdgcn_make_buffer_rsrc((void*)a.residual, (short)0, m.out_bytes, 0x00020000);
+  const int pstride = m.upi * 4;
+#pragma unroll
+  for (int v = 0; v < 16; ++v)
+    r[v] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rrsrc, voff, (8 * (v / 4) + v % 4) * pstride, 0));
+}
+
 // Epilogue of one tile in the swapped orientation (weights as the A
-// operand; RES: 0 no residual, 1 residual, 2 as the arguments say):
-// register v = 4q + i of lane l holds output channel
+// operand; RES: 0 no residual, 1 residual, 2 as the arguments say; the
+// residual values come from `pre` when given, else from one batch of loads
+// before the tile's stores): register v = 4q + i of lane l holds output channel
 // co32 + 8q + 4(l/32) + i of unit 32T + l%32.  Each register is one store
 // instruction writing two 128-byte runs (32 consecutive units of two
 // channels) through a buffer resource; the per-register part of the offset
@@ -387,7 +407,7 @@ __device__ __forceinline__ void tile_epilogue(const MfmaArgs& m, const AccT& acc
 template <int KIND, int RES = 2, class AccT>
 __device__ __forceinline__ void tile_epilogue_swap(const MfmaArgs& m, const AccT& acc, int img0, int u0,
                                                    int T, int co32, int co_blk, const float* prm,
-                                                   int lane) {
+                                                   int lane, const float (*pre)[16] = nullptr) {
   const ConvArgs& a = m.c;
   const int g = lane >> 5, r32 = lane & 31;
   const float inv = 1.0f / (float)(1 << a.shift);
@@ -397,8 +417,16 @@ __device__ __forceinline__ void tile_epilogue_swap(const MfmaArgs& m, const AccT
   const int voff = uok ? (int)((((int64_t)img * a.cout + cbase) * m.upi + uu) * 4) : 0x7FFFFFF0;
   const __amdgpu_buffer_rsrc_t orsrc =
       __builtin_amdgcn_make_buffer_rsrc(a.out, (short)0, m.out_bytes, 0x00020000);
-  const __amdgpu_buffer_rsrc_t rrsrc = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(a.residual_on ? a.residual : (const float*)a.out), (short)0, m.out_bytes, 0x00020000);
+  const bool res = KIND == K_BNF32 && (RES == 1 || (RES == 2 && a.residual_on));
+  float rv[16];
+  if (res) {
+    if (pre) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) rv[v] = (*pre)[v];
+    } else {
+      swap_res_load(m, img0, u0, T, co32, lane, rv);
+    }
+  }
   const bool full = co32 + 32 <= a.cout;  // uniform: no channel of the tile is missing
   const int pstride = m.upi * 4;
 #pragma unroll
@@ -422,8 +450,7 @@ __device__ __forceinline__ void tile_epilogue_swap(const MfmaArgs& m, const AccT
         if constexpr (KIND == K_SCALE) z = kv[i] * z;
         if constexpr (KIND == K_BNF32) {
           z = fmaf(kv[i], z, bv[i]);
-          if (RES == 1 || (RES == 2 && a.residual_on))
-            z = z + __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rrsrc, voff, so, 0));
+          if (res) z = z + rv[4 * q + i];
         }
         bits = __float_as_uint(z);
       }
@@ -1218,23 +1245,44 @@ __global__ __launch_bounds__(1024, 1) void conv_mfma_pp_kernel(const MfmaArgs m)
     const bool st = k >= 1 && co_w < a.cout;
     int pimg0 = 0, pu0 = 0;
     if (st) item_units(m, item_w(k - 1), &pimg0, &pu0);
-    Unroll<0, MT * NT>::run([&](auto TI) __attribute__((always_inline)) {
-      constexpr int TT = decltype(TI)::value;
-      constexpr int i = TT / NT, j = TT % NT;
-      const int co32 = co_w + 32 * j;
-      if (st && co32 < a.cout) {
-        const int T = wm * MT + i;
-        if (a.mode == QCONV_EPI_INT32)
-          tile_epilogue_swap<K_INT32, 0>(m, acc[i][j], pimg0, pu0, T, co32, co_blk, prm, plane);
-        else if (a.mode == QCONV_EPI_SCALE_F32)
-          tile_epilogue_swap<K_SCALE, 0>(m, acc[i][j], pimg0, pu0, T, co32, co_blk, prm, plane);
-        else if (!a.residual_on)
-          tile_epilogue_swap<K_BNF32, 0>(m, acc[i][j], pimg0, pu0, T, co32, co_blk, prm, plane);
-        else
-          tile_epilogue_swap<K_BNF32, 1>(m, acc[i][j], pimg0, pu0, T, co32, co_blk, prm, plane);
-      }
-      if constexpr (TT < NI) expand_one(std::integral_constant<int, TT>{});
-    });
+    if (a.mode == QCONV_EPI_BN_F32 && a.residual_on) {
+      // residual layers: the residual values of tile t + 1 are loaded before
+      // the stores of tile t, so no load waits for the stores of its own tile
+      float rcur[16], rnext[16];
+      if (st && co_w < a.cout) swap_res_load(m, pimg0, pu0, wm * MT, co_w, plane, rcur);
+      Unroll<0, MT * NT>::run([&](auto TI) __attribute__((always_inline)) {
+        constexpr int TT = decltype(TI)::value;
+        constexpr int i = TT / NT, j = TT % NT;
+        const int co32 = co_w + 32 * j;
+        if constexpr (TT + 1 < MT * NT) {
+          constexpr int i1 = (TT + 1) / NT, j1 = (TT + 1) % NT;
+          if (st && co_w + 32 * j1 < a.cout) swap_res_load(m, pimg0, pu0, wm * MT + i1, co_w + 32 * j1, plane, rnext);
+        }
+        if (st && co32 < a.cout)
+          tile_epilogue_swap<K_BNF32, 1>(m, acc[i][j], pimg0, pu0, wm * MT + i, co32, co_blk, prm, plane, &rcur);
+        if constexpr (TT + 1 < MT * NT) {
+#pragma unroll
+          for (int v = 0; v < 16; ++v) rcur[v] = rnext[v];
+        }
+        if constexpr (TT < NI) expand_one(std::integral_constant<int, TT>{});
+      });
+    } else {
+      Unroll<0, MT * NT>::run([&](auto TI) __attribute__((always_inline)) {
+        constexpr int TT = decltype(TI)::value;
+        constexpr int i = TT / NT, j = TT % NT;
+        const int co32 = co_w + 32 * j;
+        if (st && co32 < a.cout) {
+          const int T = wm * MT + i;
+          if (a.mode == QCONV_EPI_INT32)
+            tile_epilogue_swap<K_INT32, 0>(m, acc[i][j], pimg0, pu0, T, co32, co_blk, prm, plane);
+          else if (a.mode == QCONV_EPI_SCALE_F32)
+            tile_epilogue_swap<K_SCALE, 0>(m, acc[i][j], pimg0, pu0, T, co32, co_blk, prm, plane);
+          else
+            tile_epilogue_swap<K_BNF32, 0>(m, acc[i][j], pimg0, pu0, T, co32, co_blk, prm, plane);
+        }
+        if constexpr (TT < NI) expand_one(std::integral_constant<int, TT>{});
+      });
+    }
     Unroll<(MT * NT < NI ? MT * NT : NI), NI>::run([&](auto UI) __attribute__((always_inline)) { expand_one(UI); });
     // halo items past NI per thread (large tiles): loaded here, one at a time
     if (stage) {
