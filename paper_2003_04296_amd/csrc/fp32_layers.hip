@@ -86,30 +86,52 @@ __global__ __launch_bounds__(256) void conv_f32_kernel(const float* __restrict__
   }
 }
 
-__global__ __launch_bounds__(256) void maxpool_f32_kernel(const float* __restrict__ x, int n,
-                                                          int c, int h, int w, int k, int stride,
-                                                          int pad, int ho, int wo,
-                                                          float* __restrict__ y) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t total = (int64_t)n * c * ho * wo;
-  if (i >= total) return;
-  const int ow = (int)(i % wo);
-  const int64_t r = i / wo;
-  const int oh = (int)(r % ho);
-  const int64_t bc = r / ho;
-  const float* p = x + bc * h * w;
-  float m = -INFINITY;
-  for (int dy = 0; dy < k; ++dy) {
-    const int ih = oh * stride - pad + dy;
-    if (ih < 0 || ih >= h) continue;
-    for (int dx = 0; dx < k; ++dx) {
-      const int iw = ow * stride - pad + dx;
-      if (iw < 0 || iw >= w) continue;
-      const float v = p[(int64_t)ih * w + iw];
-      if (v > m) m = v;
+// k x k / stride max pooling, one output per thread.  Planes (image, channel)
+// come from blockIdx.y plus a loop over plane groups, positions inside a
+// plane from a 32-bit division.  The window is scanned in (dy, dx) order from
+// -inf with "v > m": padding never wins, a NaN never replaces the running
+// maximum, and of equal values the first stays.  KC > 0: the window size is
+// KC and all its loads are issued before the first compare (taps outside the
+// image read the plane's first element and are masked out).
+template <int KC>
+__global__ __launch_bounds__(256) void maxpool_f32_kernel(const float* __restrict__ x, int64_t planes,
+                                                          int h, int w, int k, int stride, int pad,
+                                                          int ho, int wo, float* __restrict__ y) {
+  const int pos = blockIdx.x * blockDim.x + threadIdx.x;
+  if (pos >= ho * wo) return;
+  const int oh = pos / wo, ow = pos - (pos / wo) * wo;
+  const int ih0 = oh * stride - pad, iw0 = ow * stride - pad;
+  for (int64_t bc = blockIdx.y; bc < planes; bc += gridDim.y) {
+    const float* p = x + bc * h * w;
+    float m = -INFINITY;
+    if constexpr (KC > 0) {
+      float v[KC * KC];
+      bool ok[KC * KC];
+#pragma unroll
+      for (int dy = 0; dy < KC; ++dy)
+#pragma unroll
+        for (int dx = 0; dx < KC; ++dx) {
+          const int ih = ih0 + dy, iw = iw0 + dx;
+          ok[dy * KC + dx] = ih >= 0 && ih < h && iw >= 0 && iw < w;
+          v[dy * KC + dx] = p[ok[dy * KC + dx] ? ih * w + iw : 0];
+        }
+#pragma unroll
+      for (int t = 0; t < KC * KC; ++t)
+        if (ok[t] && v[t] > m) m = v[t];
+    } else {
+      for (int dy = 0; dy < k; ++dy) {
+        const int ih = ih0 + dy;
+        if (ih < 0 || ih >= h) continue;
+        for (int dx = 0; dx < k; ++dx) {
+          const int iw = iw0 + dx;
+          if (iw < 0 || iw >= w) continue;
+          const float v = p[ih * w + iw];
+          if (v > m) m = v;
+        }
+      }
     }
+    y[bc * ho * wo + pos] = m;
   }
-  y[i] = m;
 }
 
 __global__ __launch_bounds__(256) void avgpool_f32_kernel(const float* __restrict__ x,
@@ -266,10 +288,16 @@ int launch_conv_f32(const float* x, const float* wt, int n, int cin, int h, int 
 int launch_maxpool_f32(const float* x, int n, int c, int h, int w, int k, int stride, int pad,
                        float* y, hipStream_t s) {
   const int ho = (h + 2 * pad - k) / stride + 1, wo = (w + 2 * pad - k) / stride + 1;
-  const int64_t total = (int64_t)n * c * ho * wo;
-  if (total == 0) return QCONV_OK;
-  maxpool_f32_kernel<<<(unsigned)((total + 255) / 256), 256, 0, s>>>(x, n, c, h, w, k, stride,
-                                                                     pad, ho, wo, y);
+  const int64_t planes = (int64_t)n * c;
+  if ((int64_t)h * w >= ((int64_t)1 << 31)) return QCONV_EUNSUPPORTED;
+  if (planes == 0 || ho < 1 || wo < 1) return QCONV_OK;
+  const dim3 grid((unsigned)ceil_div(ho * wo, 256), (unsigned)(planes < 65535 ? planes : 65535));
+  if (k == 3)
+    maxpool_f32_kernel<3><<<grid, 256, 0, s>>>(x, planes, h, w, k, stride, pad, ho, wo, y);
+  else if (k == 2)
+    maxpool_f32_kernel<2><<<grid, 256, 0, s>>>(x, planes, h, w, k, stride, pad, ho, wo, y);
+  else
+    maxpool_f32_kernel<0><<<grid, 256, 0, s>>>(x, planes, h, w, k, stride, pad, ho, wo, y);
   return hip_status();
 }
 

@@ -601,9 +601,14 @@ def test_fc_f32_binary_input(dev, n, c, out):
     np.testing.assert_array_equal(got, oracle.fc_f32(lv, wt.numpy(), b.numpy()))
 
 
-@pytest.mark.parametrize("n,cin,hw,cout,k,s,p", [(2, 3, 32, 128, 3, 1, 1), (1, 3, 37, 64, 7, 2, 3), (3, 5, 9, 40, 3, 2, 0)])
-def test_conv_f32_pools_and_head(dev, n, cin, hw, cout, k, s, p):
-    """fp32 conv -> BN -> ReLU -> max pool 3x3/2 -> avg pool -> FC, layer by layer."""
+@pytest.mark.parametrize("pk,ps,pp", [(3, 2, 1), (2, 2, 0), (4, 3, 1)])
+@pytest.mark.parametrize("n,cin,hw,cout,k,s,p", [(2, 3, 32, 128, 3, 1, 1), (1, 3, 37, 64, 7, 2, 3), (3, 5, 9, 40, 3, 2, 0),
+                                                 (1, 3, 64, 96, 7, 2, 3), (2, 40, 18, 33, 5, 1, 2)])
+def test_conv_f32_pools_and_head(dev, n, cin, hw, cout, k, s, p, pk, ps, pp):
+    """fp32 conv -> BN -> ReLU -> max pool -> avg pool -> FC, layer by layer
+    (several 16 x 16 output tiles with ragged edges, two channel blocks, more
+    input channels than one LDS chunk holds for k = 5; pool windows of 3, 2 and
+    a generic 4)."""
     g = synth.generator(700 + hw + cout)
     x = synth.normal(g, (n, cin, hw, hw), 1.0)
     wt = synth.normal(g, (cout, cin, k, k), 2.0 / (cin * k * k))
@@ -611,7 +616,7 @@ def test_conv_f32_pools_and_head(dev, n, cin, hw, cout, k, s, p):
     fw = synth.normal(g, (11, cout), 2.0 / cout)
     net = q.Net(cin, hw, hw)
     t1 = net.conv_f32(0, wt.to(dev), kk.to(dev), bb.to(dev), stride=s, pad=p, relu=True)
-    t2 = net.maxpool_f32(t1, 3, 2, 1)
+    t2 = net.maxpool_f32(t1, pk, ps, pp)
     t3 = net.avgpool(t2)
     net.fc_f32(t3, fw.to(dev))
     ws = torch.empty(max(net.workspace_bytes(n), 1), dtype=torch.uint8, device=dev)
@@ -626,7 +631,7 @@ def test_conv_f32_pools_and_head(dev, n, cin, hw, cout, k, s, p):
     y = oracle.conv_f32(x.numpy(), wt.numpy(), s, p)
     z = oracle.relu(oracle.bn_f32(y, kk.numpy(), bb.numpy()))
     np.testing.assert_array_equal(view(t1), z)
-    mp = oracle.maxpool_f32(z, 3, 2, 1)
+    mp = oracle.maxpool_f32(z, pk, ps, pp)
     np.testing.assert_array_equal(view(t2), mp)
     ap = oracle.avgpool_f32(mp)
     np.testing.assert_array_equal(logits.cpu().numpy(), oracle.fc_f32(ap, fw.numpy()))
