@@ -285,6 +285,60 @@ def main():
         })
         if not args.no_cpu:
             out["cpu_baseline"] = cpu_baseline_conv(case, mode)
+    elif wl == "aqe":
+        # the elementwise AQE work of one training step of ResNet-18 2W2A at
+        # batch 64: forward of 11.2 M weights (per-channel thresholds) and of
+        # one 64 x 64 x 56 x 56 activation tensor, their AQE gradients, and the
+        # SGD update + clip of the weights
+        g = synth.generator(1006)
+        wt = synth.normal(g, (2432, 512, 3, 3), 2.0 / 4608).to(dev)
+        act = synth.normal(g, (64, 64, 56, 56), 1.0).to(dev)
+        gact = synth.normal(g, (64, 64, 56, 56), 1e-3).to(dev)
+        gw = synth.normal(g, (2432, 512, 3, 3), 1e-3).to(dev)
+        _, s_c = q.pack_weight(wt, 2)
+        wh, ah, ga, gwx = torch.empty_like(wt), torch.empty_like(act), torch.empty_like(act), torch.empty_like(wt)
+        nw, na = wt.numel(), act.numel()
+
+        def aqe_step():
+            q.aqe_forward(wt, 2, 0.5, scale=s_c, group_size=4608, out=wh)
+            q.aqe_forward(act, 2, 0.5, out=ah)
+            q.aqe_backward(act, gact, 0.5, out=ga)
+            q.aqe_backward(wt, gw, 0.5, out=gwx)
+            q.aqe_sgd_clip(wt, gwx, 1e-3)
+
+        for _ in range(args.warmup):
+            aqe_step()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            aqe_step()
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / args.steps
+        step_bytes = 32 * nw + 20 * na  # reads + writes of the five passes
+        t_bwd = time_kernel(lambda: q.aqe_backward(act, gact, 0.5, out=ga), args.steps, stream)
+        gbs = step_bytes / dt / 1e9
+        bwd_gbs = 12 * na / t_bwd / 1e9
+        out.update({"metric": "AQE training elementwise throughput", "value": round(gbs, 1), "unit": "GB/s",
+                    "ms_per_step": round(dt * 1e3, 4), "dtype": "f32",
+                    "config": {"workload": "aqe_resnet18_2w2a_batch64", "weights": nw, "activations": na},
+                    "roofline": {"bound": "hbm", "kernel": "aqe_backward_kernel<4>", "achieved": round(bwd_gbs, 1),
+                                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(bwd_gbs / HBM_PEAK_GBS, 4),
+                                 "traffic": None, "algorithmic_bytes": 12 * na, "avg_us": round(t_bwd * 1e6, 2),
+                                 "step_achieved_gbs": round(gbs, 1)}})
+        if not args.no_cpu:
+            import oracle
+
+            m = 1 << 22
+            xs, gs = act.view(-1)[:m].cpu().numpy(), gact.view(-1)[:m].cpu().numpy()
+            t0 = time.perf_counter()
+            oracle.aqe_forward(xs, 2, 0.5)
+            oracle.aqe_backward(xs, gs, 0.5)
+            oracle.sgd_clip(xs, gs, 1e-3)
+            tc = time.perf_counter() - t0
+            out["cpu_baseline"] = {"value": round((8 + 12 + 12) * m / tc / 1e9, 2), "unit": "GB/s", "cores": 1,
+                                   "kind": "oracle",
+                                   "sample": f"forward + backward + update over {m} activations (numpy, one thread), "
+                                             f"{tc:.2f} s"}
     elif wl in ("convnet", "resnet18"):
         from paper_2003_04296_amd.nets import build_convnet, build_resnet18
 

@@ -205,6 +205,38 @@ int qconv_resolve_algo(const qconv_desc* d, const qconv_epilogue* epi);
 int qconv_kernel_name(const qconv_desc* d, const qconv_epilogue* epi, int packed_out, char* buf, int len);
 
 /* ------------------------------------------------------------------------ */
+/* Training with the asymptotic-quantized estimator (AQE): the elementwise   */
+/* steps of Algorithm 1's training branch (Sec. III-B, III-D; Eqs.           */
+/* activation and weight).  Device pointers, n values each, no allocation,   */
+/* enqueued on `stream`; n == 0 launches nothing.                            */
+/* ------------------------------------------------------------------------ */
+
+/* Forward: y = fl(fl(alpha * h(x)) + fl(fl(1 - alpha) * x)) elementwise,
+ * 0 <= alpha <= 1, where h(x) is the level (+-1, 0, +-1/2, +-1/4) that the
+ * packing quantizers give for `bits` (same compares, ties and readings).
+ *   group_size == 0: activation thresholds (host `thresholds`, NULL =
+ *     defaults); scale must be NULL.
+ *   group_size  > 0: weight thresholds: the base set (host `thresholds`,
+ *     NULL = defaults) times scale[i / group_size] (device, e.g. the s_c that
+ *     qconv_pack_weight writes; one group = one output channel's weights in
+ *     OIHW order), rounded as the weight packing rounds them; n must be a
+ *     multiple of group_size.
+ * alpha = 1 gives h(x) for finite x (0 * inf is NaN), alpha = 0 gives x.
+ * x and y may be the same buffer. */
+int aqe_forward(const float* x, int64_t n, int bits, float alpha, const float* thresholds, const float* scale,
+                int64_t group_size, float* y, void* stream);
+
+/* Backward: gx = fl(2 alpha * gy) where |x| <= 1, else 0 (a NaN x gives 0).
+ * alpha = 1/2 gives the straight-through estimator gy 1{|x| <= 1} (Eq. ste,
+ * Theorem 1).  gx may alias gy. */
+int aqe_backward(const float* x, const float* gy, int64_t n, float alpha, float* gx, void* stream);
+
+/* Weight update of Algorithm 1 with plain SGD, then the clip to [-1, 1]:
+ * w = fl(w - fl(lr * g)), then 1 if above 1, -1 if below -1 (a NaN stays).
+ * In place. */
+int aqe_sgd_clip(float* w, const float* g, int64_t n, float lr, void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Whole networks (Algorithm 1, inference branch, layer by layer)            */
 /* ------------------------------------------------------------------------ */
 

@@ -1,4 +1,5 @@
-"""Plain CPU oracle for the MINW-Net inference path.
+"""Plain CPU oracle for the MINW-Net inference path and the elementwise
+steps of its AQE training.
 
 TEST INFRASTRUCTURE ONLY: the test suite, the smoke check and the benchmark's
 CPU-baseline leg are its only callers.  It never imports the GPU package and
@@ -130,6 +131,81 @@ def quantize_weights(w, bits: int, base_thr=None):
     if rc != 0:
         raise ValueError(f"oracle_quantize_weights failed ({rc})")
     return out, s
+
+
+def quantize_weights_with_scale(w, bits: int, s, base_thr=None) -> np.ndarray:
+    """Integer level codes of the weights with given per-channel scales s_c."""
+    w = _f32(w)
+    cout = w.shape[0]
+    k = w.size // cout
+    s = _f32(s)
+    bt = WEIGHT_BASE_THRESHOLDS[bits] if base_thr is None else tuple(base_thr)
+    t = _f32(bt if len(bt) else (0.0,))
+    out = np.empty(w.shape, dtype=np.int8)
+    rc = lib().oracle_quantize_weights(_p(w), cout, ctypes.c_int64(k), bits, _p(s), _p(t), _p(out))
+    if rc != 0:
+        raise ValueError(f"oracle_quantize_weights failed ({rc})")
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Training with the asymptotic-quantized estimator (Sec. III-B and III-D,
+# Eqs. activation and weight; Algorithm 1, training branch).  Every float32
+# operation below is one rounded numpy float32 operation, in the order the
+# equations write them.
+# ---------------------------------------------------------------------------
+
+
+def levels_f32(codes, bits: int) -> np.ndarray:
+    """Level values of integer codes (3 bits: codes are 4x the level)."""
+    v = np.asarray(codes).astype(np.float32)
+    return v / np.float32(4) if bits == 3 else v
+
+
+def aqe_forward(x, bits: int, alpha: float, thr=None) -> np.ndarray:
+    """Activations: alpha h(x) + (1 - alpha) x with h the quantizer level."""
+    x = _f32(x)
+    h = levels_f32(quantize(x, bits, thr), bits)
+    a = np.float32(alpha)
+    om = np.float32(np.float32(1) - a)
+    with np.errstate(invalid="ignore"):  # 0 * inf is NaN, as on the GPU
+        return (a * h + om * x).astype(np.float32)
+
+
+def aqe_forward_weights(w, bits: int, alpha: float, s, base_thr=None) -> np.ndarray:
+    """Weights (OIHW, one group per output channel) with given s_c."""
+    w = _f32(w)
+    h = levels_f32(quantize_weights_with_scale(w, bits, s, base_thr), bits)
+    a = np.float32(alpha)
+    om = np.float32(np.float32(1) - a)
+    with np.errstate(invalid="ignore"):
+        return (a * h + om * w).astype(np.float32)
+
+
+def aqe_backward(x, gy, alpha: float) -> np.ndarray:
+    """2 alpha gy where |x| <= 1, else 0."""
+    x = _f32(x)
+    gy = _f32(gy)
+    twoa = np.float32(2) * np.float32(alpha)
+    with np.errstate(invalid="ignore"):
+        return np.where(np.abs(x) <= np.float32(1), twoa * gy, np.float32(0)).astype(np.float32)
+
+
+def ste_backward(x, gy) -> np.ndarray:
+    """The straight-through estimator of Sec. II-B: gy 1{|x| <= 1}."""
+    x = _f32(x)
+    gy = _f32(gy)
+    return np.where(np.abs(x) <= np.float32(1), gy, np.float32(0)).astype(np.float32)
+
+
+def sgd_clip(w, g, lr: float) -> np.ndarray:
+    """Algorithm 1's update with plain SGD, then the clip to [-1, 1]."""
+    w = _f32(w)
+    g = _f32(g)
+    v = (w - np.float32(lr) * g).astype(np.float32)
+    v = np.where(v > np.float32(1), np.float32(1), v)
+    v = np.where(v < np.float32(-1), np.float32(-1), v)
+    return v.astype(np.float32)
 
 
 # ---------------------------------------------------------------------------

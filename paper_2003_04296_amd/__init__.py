@@ -25,7 +25,7 @@ EXPORTED = (
     "qconv_out_size", "qconv_forward", "qnet_create", "qnet_destroy", "qnet_add_conv_f32",
     "qnet_add_maxpool_f32", "qnet_add_quantize", "qnet_add_qconv", "qnet_add_avgpool",
     "qnet_add_fc_f32", "qnet_workspace_bytes", "qnet_forward", "qnet_tensor_info", "qconv_resolve_algo",
-    "qconv_kernel_name",
+    "qconv_kernel_name", "aqe_forward", "aqe_backward", "aqe_sgd_clip",
 )
 
 
@@ -80,6 +80,11 @@ def lib() -> ctypes.CDLL:
     L.qconv_resolve_algo.argtypes = [ctypes.POINTER(qconv_desc), ctypes.POINTER(qconv_epilogue)]
     L.qconv_kernel_name.argtypes = [ctypes.POINTER(qconv_desc), ctypes.POINTER(qconv_epilogue), i32,
                                     ctypes.c_char_p, i32]
+    i64 = ctypes.c_int64
+    f32 = ctypes.c_float
+    L.aqe_forward.argtypes = [vp, i64, i32, f32, vp, vp, i64, vp, vp]
+    L.aqe_backward.argtypes = [vp, vp, i64, f32, vp, vp]
+    L.aqe_sgd_clip.argtypes = [vp, vp, i64, f32, vp]
     L.qnet_create.restype = vp
     L.qnet_create.argtypes = [i32, i32, i32]
     L.qnet_destroy.argtypes = [vp]
@@ -167,6 +172,33 @@ def pack_weight(w, bits: int, base_thresholds=None, stream=None):
     _check(lib().qconv_pack_weight(_ptr(w), cout, cin, kh, kw, bits, t, _ptr(out), _ptr(scale), _stream(stream)),
            "qconv_pack_weight")
     return out, scale
+
+
+def aqe_forward(x, bits: int, alpha: float, thresholds=None, scale=None, group_size: int = 0, out=None, stream=None):
+    """AQE forward y = alpha h(x) + (1 - alpha) x (device fp32 tensors);
+    weights: pass scale (s_c per group) and group_size (values per group)."""
+    import torch
+
+    y = torch.empty_like(x) if out is None else out
+    t = _host_f32(thresholds)
+    _check(lib().aqe_forward(_ptr(x), x.numel(), bits, float(alpha), t, _ptr(scale), int(group_size), _ptr(y),
+                             _stream(stream)), "aqe_forward")
+    return y
+
+
+def aqe_backward(x, gy, alpha: float, out=None, stream=None):
+    """AQE backward gx = 2 alpha gy 1{|x| <= 1}."""
+    import torch
+
+    gx = torch.empty_like(gy) if out is None else out
+    _check(lib().aqe_backward(_ptr(x), _ptr(gy), x.numel(), float(alpha), _ptr(gx), _stream(stream)), "aqe_backward")
+    return gx
+
+
+def aqe_sgd_clip(w, g, lr: float, stream=None):
+    """In place: w = clip(w - lr g, -1, 1)."""
+    _check(lib().aqe_sgd_clip(_ptr(w), _ptr(g), w.numel(), float(lr), _stream(stream)), "aqe_sgd_clip")
+    return w
 
 
 def fold_bn(gamma, beta, mean, var, eps):

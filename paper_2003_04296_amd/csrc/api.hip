@@ -235,6 +235,42 @@ int qconv_resolve_algo(const qconv_desc* d, const qconv_epilogue* epi) {
   return prepare_conv(d, nullptr, nullptr, epi, nullptr, nullptr, false, &a);
 }
 
+int aqe_forward(const float* x, int64_t n, int bits, float alpha, const float* thresholds, const float* scale,
+                int64_t group_size, float* y, void* stream) {
+  if (n < 0 || !bits_ok(bits) || !(alpha >= 0.0f && alpha <= 1.0f) || group_size < 0) return QCONV_EINVAL;
+  if (n > 0 && (!x || !y)) return QCONV_EINVAL;
+  Thr t = {0.0f, 0.0f, 0.0f};
+  if (group_size == 0) {
+    if (scale) return QCONV_EINVAL;
+    const int rc = act_thresholds(bits, thresholds, &t);
+    if (rc) return rc;
+  } else {
+    if (n % group_size != 0 || (n > 0 && !scale)) return QCONV_EINVAL;
+    if (bits == 2) t.t0 = thresholds ? thresholds[0] : kWgtThr2[0];
+    if (bits == 3) {
+      t.t0 = thresholds ? thresholds[0] : kWgtThr3[0];
+      t.t1 = thresholds ? thresholds[1] : kWgtThr3[1];
+      t.t2 = thresholds ? thresholds[2] : kWgtThr3[2];
+    }
+    if (bits == 2 && !(t.t0 >= 0.0f)) return QCONV_EINVAL;
+    if (bits == 3 && !(t.t0 >= 0.0f && t.t0 <= t.t1 && t.t1 <= t.t2)) return QCONV_EINVAL;
+  }
+  return launch_aqe_forward(x, n, bits, alpha, t, group_size ? scale : nullptr, group_size ? group_size : 1, y,
+                            (hipStream_t)stream);
+}
+
+int aqe_backward(const float* x, const float* gy, int64_t n, float alpha, float* gx, void* stream) {
+  if (n < 0 || !(alpha >= 0.0f && alpha <= 1.0f)) return QCONV_EINVAL;
+  if (n > 0 && (!x || !gy || !gx)) return QCONV_EINVAL;
+  return launch_aqe_backward(x, gy, n, alpha, gx, (hipStream_t)stream);
+}
+
+int aqe_sgd_clip(float* w, const float* g, int64_t n, float lr, void* stream) {
+  if (n < 0 || !(lr == lr)) return QCONV_EINVAL;
+  if (n > 0 && (!w || !g)) return QCONV_EINVAL;
+  return launch_aqe_sgd_clip(w, g, n, lr, (hipStream_t)stream);
+}
+
 int qconv_kernel_name(const qconv_desc* d, const qconv_epilogue* epi, int packed_out, char* buf, int len) {
   ConvArgs a;
   static uint32_t marker;  // stands for a packed output buffer; never accessed

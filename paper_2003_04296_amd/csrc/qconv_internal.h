@@ -186,6 +186,11 @@ int launch_avgpool_f32(const float* x, int n, int c, int h, int w, float* y, hip
 int launch_fc_f32(const void* x, int x_bits, int n, int in, const float* w, const float* bias,
                   int out, float* y, hipStream_t s);
 
+int launch_aqe_forward(const float* x, int64_t n, int bits, float alpha, Thr base, const float* scale,
+                       int64_t group, float* y, hipStream_t s);
+int launch_aqe_backward(const float* x, const float* gy, int64_t n, float alpha, float* gx, hipStream_t s);
+int launch_aqe_sgd_clip(float* w, const float* g, int64_t n, float lr, hipStream_t s);
+
 inline int hip_status() {
   return hipGetLastError() == hipSuccess ? QCONV_OK : QCONV_EHIP;
 }

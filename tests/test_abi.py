@@ -20,7 +20,7 @@ GOLDEN = os.path.join(ROOT, "tests", "golden", "dispatch_table1.txt")
 def _declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    names = re.findall(r"\b((?:qconv|qnet)_[a-z0-9_]+)\s*\(", text)
+    names = re.findall(r"\b((?:qconv|qnet|aqe)_[a-z0-9_]+)\s*\(", text)
     return sorted(set(names))
 
 
