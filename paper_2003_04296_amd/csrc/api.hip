@@ -348,7 +348,7 @@ size_t plan(const qnet* net, int batch, std::vector<size_t>* toff, std::vector<s
     if (l.kind != L_CONV_F32) continue;
     if (woff) (*woff)[i] = off;
     const int cin = net->t[l.src].c;
-    off = align256(off + (size_t)cin * l.k * l.k * ceil_div(l.cout, 32) * 32 * sizeof(float));
+    off = align256(off + (size_t)cin * l.k * l.k * ceil_div(l.cout, 64) * 64 * sizeof(float));
   }
   return off;
 }

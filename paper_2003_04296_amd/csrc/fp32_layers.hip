@@ -12,9 +12,13 @@ namespace qc {
 
 namespace {
 
-constexpr int CONV_TN = 32;  // output channels per wave (weights via the scalar cache)
+// Output channels per thread: 32 when the output is packed (one word per
+// plane), 64 for fp32 outputs (each tap's scalar weight loads then feed 64
+// fmaf).  The transposed weights are padded to a multiple of CONV_PAD.
+constexpr int CONV_TN = 32;
+constexpr int CONV_PAD = 64;
 
-// OIHW -> [cin][k][k][cout_pad32] so that the TN weights of one tap are one
+// OIHW -> [cin][k][k][cout_pad64] so that the TN weights of one tap are one
 // contiguous, wave-uniform run.
 __global__ void transpose_weight_kernel(const float* __restrict__ w, int cout, int cin, int kk,
                                         int cop, float* __restrict__ wt) {
@@ -26,7 +30,7 @@ __global__ void transpose_weight_kernel(const float* __restrict__ w, int cout, i
   wt[i] = (co < cout) ? w[(int64_t)co * cin * kk + tap] : 0.0f;
 }
 
-template <int OUT_BITS>
+template <int OUT_BITS, int TN>
 __global__ __launch_bounds__(256) void conv_f32_kernel(const float* __restrict__ x,
                                                        const float* __restrict__ wt, int n, int cin,
                                                        int h, int w, int cout, int cop, int k,
@@ -38,14 +42,14 @@ __global__ __launch_bounds__(256) void conv_f32_kernel(const float* __restrict__
   const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t total = (int64_t)n * ho * wo;
   if (g >= total) return;
-  const int co0 = blockIdx.y * CONV_TN;
+  const int co0 = blockIdx.y * TN;
   const int ow = (int)(g % wo);
   const int64_t r = g / wo;
   const int oh = (int)(r % ho);
   const int b = (int)(r / ho);
-  float acc[CONV_TN];
+  float acc[TN];
 #pragma unroll
-  for (int j = 0; j < CONV_TN; ++j) acc[j] = 0.0f;
+  for (int j = 0; j < TN; ++j) acc[j] = 0.0f;
   const float* xb = x + (int64_t)b * cin * h * w;
   for (int ci = 0; ci < cin; ++ci) {
     for (int ky = 0; ky < k; ++ky) {
@@ -57,14 +61,14 @@ __global__ __launch_bounds__(256) void conv_f32_kernel(const float* __restrict__
         const float xv = xb[((int64_t)ci * h + ih) * w + iw];
         const float* wp = wt + ((int64_t)(ci * k + ky) * k + kx) * cop + co0;
 #pragma unroll
-        for (int j = 0; j < CONV_TN; ++j) acc[j] = fmaf(xv, wp[j], acc[j]);
+        for (int j = 0; j < TN; ++j) acc[j] = fmaf(xv, wp[j], acc[j]);
       }
     }
   }
   const int64_t plane = (int64_t)ho * wo;
   uint32_t words[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
-  for (int j = 0; j < CONV_TN; ++j) {
+  for (int j = 0; j < TN; ++j) {
     const int co = co0 + j;
     if (co >= cout) break;
     float z = fmaf(bn_k[co], acc[j], bn_b[co]);
@@ -257,7 +261,7 @@ __global__ __launch_bounds__(256) void fc_f32_kernel(const void* __restrict__ xi
 
 int launch_transpose_conv_weight(const float* w, int cout, int cin, int k, float* wt,
                                  hipStream_t s) {
-  const int cop = ceil_div(cout, CONV_TN) * CONV_TN;
+  const int cop = ceil_div(cout, CONV_PAD) * CONV_PAD;
   const int64_t total = (int64_t)cin * k * k * cop;
   transpose_weight_kernel<<<(unsigned)((total + 255) / 256), 256, 0, s>>>(w, cout, cin, k * k, cop,
                                                                            wt);
@@ -268,18 +272,20 @@ int launch_conv_f32(const float* x, const float* wt, int n, int cin, int h, int 
                     int stride, int pad, const float* bn_k, const float* bn_b, int relu,
                     int out_bits, Thr othr, float* out_f32, uint32_t* out_packed, hipStream_t s) {
   const int ho = (h + 2 * pad - k) / stride + 1, wo = (w + 2 * pad - k) / stride + 1;
-  const int cop = ceil_div(cout, CONV_TN) * CONV_TN;
+  const int cop = ceil_div(cout, CONV_PAD) * CONV_PAD;
   const int64_t total = (int64_t)n * ho * wo;
   if (total == 0) return QCONV_OK;
-  const dim3 grid((unsigned)((total + 255) / 256), (unsigned)(cop / CONV_TN));
-#define QC_F32(B)                                                                              \
-  conv_f32_kernel<B><<<grid, 256, 0, s>>>(x, wt, n, cin, h, w, cout, cop, k, stride, pad, ho, \
-                                          wo, bn_k, bn_b, relu, othr, out_f32, out_packed)
+  const unsigned gx = (unsigned)((total + 255) / 256);
+#define QC_F32(B, TN)                                                                                        \
+  conv_f32_kernel<B, TN><<<dim3(gx, (unsigned)ceil_div(cout, TN)), 256, 0, s>>>(                            \
+      x, wt, n, cin, h, w, cout, cop, k, stride, pad, ho, wo, bn_k, bn_b, relu, othr, out_f32, out_packed)
   switch (out_bits) {
-    case 0: QC_F32(0); break;
-    case 1: QC_F32(1); break;
-    case 2: QC_F32(2); break;
-    default: QC_F32(3); break;
+    case 0:
+      if (cout > CONV_TN) QC_F32(0, 64); else QC_F32(0, 32);
+      break;
+    case 1: QC_F32(1, 32); break;
+    case 2: QC_F32(2, 32); break;
+    default: QC_F32(3, 32); break;
   }
 #undef QC_F32
   return hip_status();

@@ -174,7 +174,7 @@ bool mfma_supports(const ConvArgs& a);
 int bitplane_kernel_name(const ConvArgs& a, char* buf, int len);
 int mfma_kernel_name(const ConvArgs& a, char* buf, int len);
 
-int launch_conv_f32(const float* x, const float* wt_t /* [cin][k][k][cout_pad32] */, int n, int cin,
+int launch_conv_f32(const float* x, const float* wt_t /* [cin][k][k][cout_pad64] */, int n, int cin,
                     int h, int w, int cout, int k, int stride, int pad, const float* bn_k,
                     const float* bn_b, int relu, int out_bits, Thr othr, float* out_f32,
                     uint32_t* out_packed, hipStream_t s);
