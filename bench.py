@@ -12,7 +12,8 @@ time, plus the roofline of the dominant kernel (measured with HIP events on
 the launch stream) and the CPU oracle timed on a bounded sample.
 
 Other workloads: --workload 1w1a | 1w2a (default) | 3w3a-L{0..3} |
-convnet | resnet18 (the last two report images/s).
+a16w{1,2,3} (fp16 inputs, same layer shape; the step converts fp32 -> fp16) |
+aqe | convnet | resnet18 (the last two report images/s).
 """
 from __future__ import annotations
 
@@ -36,8 +37,8 @@ METRIC = "quantized-conv GOPS (1W1A, 2W2A, 3W3A) + images/sec fwd; % of roofline
 # MI355X figures: 256 CUs x 64 lanes x 2.4 GHz of 32-bit VALU issue.
 VALU_LANE_OPS = 256 * 64 * 2.4e9
 HBM_PEAK_GBS = 8000.0
-# dense matrix-core peaks (ops = 2 per MAC), in G: int8 5.0 POP/s, fp4 10.1 PFLOP/s
-MFMA_PEAK_GOPS = {"mfma_i8": 5.0e6, "mfma_fp4": 10.1e6}
+# dense matrix-core peaks (ops = 2 per MAC), in G: int8 5.0 POP/s, fp4 10.1 PFLOP/s, fp16 2.5 PFLOP/s
+MFMA_PEAK_GOPS = {"mfma_i8": 5.0e6, "mfma_fp4": 10.1e6, "mfma_f16": 2.5e6}
 # Minimal VALU recipe (lane-ops per 32-channel word pair) of the bitplane
 # product on gfx950, where v_bitop3_b32 fuses any 3-input bit function:
 #   1W1A: xor, bcnt                         -> 2
@@ -98,11 +99,14 @@ class ConvWorkload:
         self.pack()
         self.conv()
 
-    def conv_bytes(self):
-        """Algorithmic HBM bytes of one conv launch: packed input + packed weights + output."""
+    def conv_bytes(self, used):
+        """Algorithmic HBM bytes of one conv launch: packed (or fp16) input + the
+        part of the packed weights the algorithm reads + output."""
         n, c, h, w = self.shape
         a = q.packed_act_words(n, c, h, w, self.case.a_bits) * 4
-        wb = q.packed_weight_words(self.cout, c, self.k, self.k, self.case.w_bits) * 4
+        taps, cw, cop = self.k * self.k, (c + 31) // 32, (self.cout + 127) // 128 * 128
+        wb = {"bitplane": taps * cw * cop * q.planes(self.case.w_bits) * 4, "mfma_i8": taps * cw * cop * 32,
+              "mfma_fp4": taps * ((cw + 1) // 2) * cop * 32, "mfma_f16": taps * 2 * cw * cop * 32}[used]
         return a + wb + int(np.prod(self.out_shape)) * 4
 
     def pack_bytes(self):
@@ -155,6 +159,12 @@ def cpu_baseline_conv(case, mode, budget_s=12.0):
 
     def run(m):
         t0 = time.perf_counter()
+        if case.a_bits == 16:
+            lw, _ = oracle.quantize_weights(case.w.numpy(), case.w_bits)
+            kk, bb = oracle.bn_fold({key: (v.numpy() if hasattr(v, "numpy") else v) for key, v in case.bn.items()})
+            oracle.qconv16_layer(oracle.to_f16(case.x[:m].numpy()), lw, case.w_bits, case.stride, case.pad, "bn",
+                                 k=kk, b=bb)
+            return time.perf_counter() - t0
         la = oracle.quantize(case.x[:m].numpy(), case.a_bits)
         lw, s = oracle.quantize_weights(case.w.numpy(), case.w_bits)
         acc = oracle.qconv_acc(la, lw, case.a_bits, case.stride, case.pad)
@@ -203,7 +213,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="1w2a")
-    ap.add_argument("--algo", default="auto", choices=["auto", "bitplane", "mfma_i8", "mfma_fp4"])
+    ap.add_argument("--algo", default="auto", choices=["auto", "bitplane", "mfma_i8", "mfma_fp4", "mfma_f16"])
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--copy-ref-mib", type=int, default=0,
                     help="after timing, run one device copy of this many MiB (HBM counter calibration)")
@@ -219,16 +229,18 @@ def main():
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
     algo = {"auto": q.ALGO_AUTO, "bitplane": q.ALGO_BITPLANE, "mfma_i8": q.ALGO_MFMA_I8,
-            "mfma_fp4": q.ALGO_MFMA_FP4}[args.algo]
+            "mfma_fp4": q.ALGO_MFMA_FP4, "mfma_f16": q.ALGO_MFMA_F16}[args.algo]
     wl = args.workload
     out = {"metric": METRIC, "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "higher_is_better": True,
            "scaling": "weak", "vs_baseline": None, "data": "synthetic"}
 
-    if wl in ("1w1a", "1w2a") or wl.startswith("3w3a"):
+    if wl in ("1w1a", "1w2a", "a16w1", "a16w2", "a16w3") or wl.startswith("3w3a"):
         if wl == "1w1a":
             case, mode = synth.workload1(), q.EPI_SCALE_F32
         elif wl == "1w2a":
             case, mode = synth.workload2(), q.EPI_BN_F32
+        elif wl.startswith("a16"):
+            case, mode = synth.workload7(int(wl[-1])), q.EPI_BN_F32
         else:
             case, mode = synth.workload5(int(wl.split("L")[1])), q.EPI_INT32
         W = ConvWorkload(case, dev, mode, algo)
@@ -254,13 +266,13 @@ def main():
             peak, cbound = valu_peak_gops(case.a_bits, case.w_bits), "alu"
         else:
             peak, cbound = MFMA_PEAK_GOPS[used], "mfma"
-        hbm_gbs = W.conv_bytes() / t_conv / 1e9
+        hbm_gbs = W.conv_bytes(used) / t_conv / 1e9
         frac_c = gops_conv / peak if peak else 0.0
         frac_h = hbm_gbs / HBM_PEAK_GBS
         n, c, h, w = W.shape
         out.update({
             "value": round(gops_step, 1), "unit": "GOPS", "ms_per_step": round(dt * 1e3, 4),
-            "dtype": "int32",
+            "dtype": "f16" if case.a_bits == 16 else "int32",
             "config": {"workload": case.name, "batch": n, "cin": c, "hw": h, "cout": W.cout, "k": W.k,
                        "a_bits": case.a_bits, "w_bits": case.w_bits,
                        "epilogue": {q.EPI_INT32: "int32", q.EPI_SCALE_F32: "scale_f32",
@@ -278,7 +290,7 @@ def main():
         })
         out["roofline"].update({
             "traffic": measured_traffic(case.name, kname), "traffic_unit": "HBM bytes per launch",
-            "algorithmic_bytes": W.conv_bytes(), "avg_us": round(t_conv * 1e6, 2)})
+            "algorithmic_bytes": W.conv_bytes(used), "avg_us": round(t_conv * 1e6, 2)})
         out.update({
             "pack_act": {"avg_us": round(t_pack * 1e6, 2), "achieved_gbs": round(W.pack_bytes() / t_pack / 1e9, 1),
                          "peak_gbs": HBM_PEAK_GBS},

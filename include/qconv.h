@@ -50,14 +50,25 @@
  *   activations: [n][h][w][cw][P],              cw = ceil(c / 32)
  *   weights    : [kh][kw][cw][cout_pad][P],     cout_pad = ceil(cout / 128) * 128
  *                (rows of padding channels are 0), followed in the same
- *                buffer by two matrix-core operand copies of the same levels,
- *                expanded from those bitplanes (channels past cin are 0):
- *                int8 codes [kh][kw][cw][cout_pad][32 B] and E2M1 (fp4)
+ *                buffer by three matrix-core operand copies of the same
+ *                levels, expanded from those bitplanes (channels past cin
+ *                and padding output channels are 0): int8 codes [kh][kw][cw][cout_pad][32 B], E2M1 (fp4)
  *                codes [kh][kw][ceil(cw/2)][cout_pad][32 B] (64 channels,
- *                two per byte, low nibble first; the codes 0, +-1, +-2, +-4
- *                are exact in both formats).
+ *                two per byte, low nibble first) and IEEE fp16 codes
+ *                [kh][kw][2 cw][cout_pad][16 x 2 B] (16 channels per
+ *                record); the codes 0, +-1, +-2, +-4 are exact in all three.
  *   An all-zero activation word reads as level -1 for 1 bit and 0 for 2/3
  *   bits, i.e. Q(0): the value padding taps take in the product.
+ *
+ * 16-bit inputs (Table I / Table IV: 16-bit floating inputs with 1..3-bit
+ * weights, the "XNOR ADDER" / "SHIFT ADDER" rows): bits = 16 stands for an
+ * unquantized IEEE fp16 activation tensor [n][h][w][cw * 32] (channel-last,
+ * channels past c hold +0; viewed as uint32 words, channel 2i in the low
+ * half of word i).  The product sums fp16 activation x weight code exactly
+ * and accumulates in fp32 (padding taps hold 0); its real value is
+ * acc * 2^-(2[w_bits==3]).  Only the fp32 accumulation rounds, so results
+ * match the exact product within K * 2^-24 * sum|x * code| (in code units),
+ * and exactly when every partial sum is an integer below 2^24.
  */
 #ifndef QCONV_H
 #define QCONV_H
@@ -105,17 +116,21 @@ int qconv_inference_op(int m_bits, int n_bits, int* op, int* precision_bits);
 /* Quantize + pack (Sec. III-C, Eq. 20)                                      */
 /* ------------------------------------------------------------------------ */
 
-/* Bytes of the packed activation tensor [n][h][w][ceil(c/32)][P]. */
+/* Bytes of the packed activation tensor [n][h][w][ceil(c/32)][P]
+ * (bits = 16: the fp16 tensor [n][h][w][ceil(c/32) * 32]). */
 size_t qconv_packed_act_bytes(int n, int c, int h, int w, int bits);
 
 /* Quantize fp32 NCHW activations x[n][c][h][w] with h(.) of `bits` and pack
  * them into out_packed.  thresholds (host, may be NULL for the defaults):
- * 2 bits {delta}; 3 bits {t1, t2, t3} increasing; ignored for 1 bit. */
+ * 2 bits {delta}; 3 bits {t1, t2, t3} increasing; ignored for 1 bit.
+ * bits = 16: convert to the fp16 channel-last layout above instead (round to
+ * nearest, ties to even; beyond the fp16 range -> +-inf; NaN stays NaN;
+ * thresholds ignored). */
 int qconv_pack_act(const float* x, int n, int c, int h, int w, int bits,
                    const float* thresholds, uint32_t* out_packed, void* stream);
 
 /* Bytes of the packed weight buffer: the bitplanes [kh][kw][ceil(cin/32)][cout_pad][P]
- * plus the int8 and fp4 operand copies described above. */
+ * plus the int8, fp4 and fp16 operand copies described above. */
 size_t qconv_packed_weight_bytes(int cout, int cin, int kh, int kw, int bits);
 
 /* Quantize fp32 OIHW weights w[cout][cin][kh][kw] (Eq. 20) and pack them.
@@ -138,14 +153,15 @@ typedef enum {
   QCONV_ALGO_AUTO = 0,     /* library choice (matrix cores where supported)   */
   QCONV_ALGO_BITPLANE = 1, /* VALU XNOR/AND + popcount over bitplanes         */
   QCONV_ALGO_MFMA_I8 = 2,  /* int8 matrix cores on the expanded level codes   */
-  QCONV_ALGO_MFMA_FP4 = 3  /* fp4 (E2M1) matrix cores on the same codes        */
+  QCONV_ALGO_MFMA_FP4 = 3, /* fp4 (E2M1) matrix cores on the same codes        */
+  QCONV_ALGO_MFMA_F16 = 4  /* fp16 matrix cores: the only one for a_bits = 16   */
 } qconv_algo;
 
 typedef struct {
   int n, cin, h, w;     /* input activations (packed with a_bits)         */
   int cout, kh, kw;     /* weights (packed with w_bits)                   */
   int stride, pad;      /* same stride / padding on both axes             */
-  int a_bits, w_bits;   /* 1..3 each                                      */
+  int a_bits, w_bits;   /* a_bits 1..3 or 16 (fp16 inputs), w_bits 1..3  */
   int algo;             /* qconv_algo                                     */
 } qconv_desc;
 
@@ -186,7 +202,15 @@ int qconv_out_size(int in, int k, int stride, int pad);
  * staging buffer (at least one input row of 64 output pixels' receptive
  * field); asked for explicitly otherwise they return QCONV_EUNSUPPORTED,
  * and AUTO falls back to the bitplane kernels.  Every algorithm returns the
- * same bits. */
+ * same bits.  a_bits = 16: act_packed is the fp16 tensor above, the
+ * algorithm is QCONV_ALGO_MFMA_F16 (AUTO picks it; any other returns
+ * QCONV_EUNSUPPORTED, as does QCONV_ALGO_MFMA_F16 for a_bits <= 3), the
+ * epilogue runs on the fp32 accumulator (QCONV_EPI_INT32 returns
+ * QCONV_EUNSUPPORTED) and the overflow check does not apply.  There is no
+ * bitplane fallback for 16-bit inputs: a layer whose input tile does not
+ * fit the fp16 staging buffer (80 bytes per pixel per 32 channels; e.g. 2x2
+ * pooling after a stride-2 conv over rows of 30 or more pixels) returns
+ * QCONV_EUNSUPPORTED. */
 int qconv_forward(const qconv_desc* d, const uint32_t* act_packed, const uint32_t* w_packed,
                   const qconv_epilogue* epi, void* out, uint32_t* out_packed, void* stream);
 

@@ -26,6 +26,9 @@ Readings taken where the paper is silent (each also listed in the design notes):
   sits before BN (Sec. III-E); HardTanh is applied before requantization.
 * fp32 layers accumulate each output as one fmaf chain in (ci, kh, kw)
   order from +0.
+* "16-bit floating" inputs (Tables I and IV) are IEEE binary16; their
+  product with weight codes is the exact sum rounded once to fp32, and the
+  fp32 epilogue of the quantized layers follows.
 """
 from __future__ import annotations
 
@@ -469,3 +472,76 @@ def resnet18_forward(p: dict, a_bits: int = 2, w_bits: int = 2, return_acts: boo
     feat = avgpool_f32(x)
     logits = fc_f32(feat, _np(p["fc"]["w"]), _np(p["fc"]["b"]))
     return (logits, acts) if return_acts else logits
+
+
+# ---------------------------------------------------------------------------
+# 16-bit inputs with 1..3-bit weights (Table I rows with 16-bit inputs;
+# Table IV "reduce weights" rows): the "XNOR ADDER" / "SHIFT ADDER" product
+# at 16-bit floating precision
+# ---------------------------------------------------------------------------
+
+
+def to_f16(x) -> np.ndarray:
+    """A 16-bit floating input: fp32 rounded to IEEE binary16 (nearest, ties
+    to even, beyond the range to +-inf, NaN stays NaN) by numpy's conversion."""
+    with np.errstate(over="ignore"):
+        return np.asarray(x, dtype=np.float32).astype(np.float16)
+
+
+def conv16_acc(x16, w_levels, stride: int = 1, pad: int = 0) -> np.ndarray:
+    """The product of 16-bit inputs and weight level codes, in code units,
+    summed in fp64 (plain loops in qoracle.c).  Padding taps hold 0: the
+    quantizer of a 16-bit input is the identity.  Every term x * code is a
+    multiple of 2^-24 (the fp16 grid) times a code of at most 4, so each
+    partial sum is exact in fp64 while the sum of |terms| stays below 2^29."""
+    x = np.asarray(x16, dtype=np.float16).astype(np.float64)
+    return conv_f64(x, np.asarray(w_levels).astype(np.float64), stride, pad)
+
+
+def conv16_acc_at(x16, w_levels, idx, stride: int = 1, pad: int = 0) -> np.ndarray:
+    """conv16_acc at flat NCHW output indices ``idx`` only (one fp64 dot
+    product per output over its zero-padded receptive field)."""
+    x = np.asarray(x16, dtype=np.float16).astype(np.float64)
+    w = np.asarray(w_levels).astype(np.float64)
+    n, cin, h, wd = x.shape
+    cout, _, kh, kw = w.shape
+    ho, wo = out_size(h, kh, stride, pad), out_size(wd, kw, stride, pad)
+    xp = np.zeros((n, cin, h + 2 * pad + stride * kh, wd + 2 * pad + stride * kw), np.float64)
+    xp[:, :, pad:pad + h, pad:pad + wd] = x
+    idx = np.asarray(idx, dtype=np.int64).reshape(-1)
+    out = np.empty(idx.size, np.float64)
+    for t, f in enumerate(idx):
+        b, rem = divmod(int(f), cout * ho * wo)
+        co, rem = divmod(rem, ho * wo)
+        oy, ox = divmod(rem, wo)
+        patch = xp[b, :, oy * stride:oy * stride + kh, ox * stride:ox * stride + kw]
+        out[t] = float(np.sum(patch * w[co]))
+    return out
+
+
+def qconv16_layer(x16, w_levels, w_bits: int, stride: int, pad: int, mode: str, s=None, k=None, b=None,
+                  residual=None, pool: bool = False, out_bits: int = 0, acc=None):
+    """One layer on 16-bit inputs.  The accumulator is the exact product
+    rounded once to fp32; the rest is the fp32 epilogue of the quantized
+    layers (Sec. III-E): 2x2 max pooling of the accumulators, acc * 2^-shift
+    (3-bit weight codes are 4 x level), then
+      mode "scale": s_c * acc_real;  "bn": fmaf(k_c, acc_real, b_c) [+ residual];
+    out_bits > 0 also returns Q(HardTanh(z)) with the activation quantizer.
+    ``acc``: conv16_acc(x16, w_levels, stride, pad) when already computed.
+    Returns (z, levels or None)."""
+    if acc is None:
+        acc = conv16_acc(x16, w_levels, stride, pad)
+    acc = np.asarray(acc, np.float64).astype(np.float32)
+    if pool:
+        acc = maxpool_f32(acc, 2, 2, 0)
+    a = (acc * np.float32(2.0 ** -level_shift(w_bits))).astype(np.float32)
+    if mode == "scale":
+        z = (_f32(s)[None, :, None, None] * a).astype(np.float32)
+    elif mode == "bn":
+        z = bn_f32(a, k, b)
+        if residual is not None:
+            z = add(z, residual)
+    else:
+        raise ValueError(mode)
+    lv = quantize(hardtanh(z), out_bits) if out_bits else None
+    return z, lv

@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libqconv.so")
 
 QCONV_OK, QCONV_EINVAL, QCONV_EUNSUPPORTED, QCONV_EWORKSPACE, QCONV_EOVERFLOW, QCONV_EHIP = 0, -1, -2, -3, -4, -5
-ALGO_AUTO, ALGO_BITPLANE, ALGO_MFMA_I8, ALGO_MFMA_FP4 = 0, 1, 2, 3
+ALGO_AUTO, ALGO_BITPLANE, ALGO_MFMA_I8, ALGO_MFMA_FP4, ALGO_MFMA_F16 = 0, 1, 2, 3, 4
 EPI_INT32, EPI_SCALE_F32, EPI_BN_F32, EPI_BN_PACK = 0, 1, 2, 3
 EPI_POOL2, EPI_RESIDUAL = 1, 2
 OP_NAMES = {1: "XNOR", 2: "SHIFT", 3: "XNOR-ADDER", 4: "SHIFT-ADDER", 5: "MAC"}
@@ -150,7 +150,8 @@ def packed_weight_words(cout, cin, kh, kw, bits) -> int:
 
 
 def pack_act(x, bits: int, thresholds=None, out=None, stream=None):
-    """fp32 NCHW device tensor -> packed bitplanes [n][h][w][cw][P] (int32 view)."""
+    """fp32 NCHW device tensor -> packed bitplanes [n][h][w][cw][P] (int32 view);
+    bits = 16: the fp16 channel-last tensor [n][h][w][cw * 32] (int32 view)."""
     import torch
 
     n, c, h, w = x.shape
@@ -238,7 +239,7 @@ def conv(act_packed, w_packed, n, cin, h, w, cout, k, stride, pad, a_bits, w_bit
     return out, out_packed
 
 
-ALGO_NAMES = {ALGO_BITPLANE: "bitplane", ALGO_MFMA_I8: "mfma_i8", ALGO_MFMA_FP4: "mfma_fp4"}
+ALGO_NAMES = {ALGO_BITPLANE: "bitplane", ALGO_MFMA_I8: "mfma_i8", ALGO_MFMA_FP4: "mfma_fp4", ALGO_MFMA_F16: "mfma_f16"}
 
 
 def resolve_algo(n, cin, h, w, cout, k, stride, pad, a_bits, w_bits, mode=EPI_INT32, flags=0, out_bits=0,

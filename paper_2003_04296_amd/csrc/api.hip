@@ -20,6 +20,7 @@ constexpr float kWgtThr2[1] = {0.7f};
 constexpr float kWgtThr3[3] = {0.125f, 0.375f, 0.75f};
 
 bool bits_ok(int b) { return b >= 1 && b <= 3; }
+bool act_bits_ok(int b) { return bits_ok(b) || b == 16; }
 int max_code(int bits) { return bits == 3 ? 4 : 1; }
 int code_shift(int bits) { return bits == 3 ? 2 : 0; }
 
@@ -41,7 +42,7 @@ int act_thresholds(int bits, const float* user, Thr* t) {
 }
 
 size_t packed_bytes(int64_t n, int c, int64_t h, int64_t w, int bits) {
-  return (size_t)(n * h * w * ceil_div(c, 32) * planes_of(bits)) * sizeof(uint32_t);
+  return (size_t)(n * h * w * ceil_div(c, 32) * act_words(bits)) * sizeof(uint32_t);
 }
 
 }  // namespace
@@ -60,7 +61,7 @@ const char* qconv_error_string(int status) {
   }
 }
 
-int qconv_version(void) { return 100; }
+int qconv_version(void) { return 101; }
 
 int qconv_inference_op(int m, int n, int* op, int* precision_bits) {
   auto valid = [](int b) { return b == 1 || b == 2 || b == 3 || b == 16 || b == 32; };
@@ -81,14 +82,15 @@ int qconv_inference_op(int m, int n, int* op, int* precision_bits) {
 }
 
 size_t qconv_packed_act_bytes(int n, int c, int h, int w, int bits) {
-  if (n < 0 || c < 1 || h < 1 || w < 1 || !bits_ok(bits)) return 0;
+  if (n < 0 || c < 1 || h < 1 || w < 1 || !act_bits_ok(bits)) return 0;
   return packed_bytes(n, c, h, w, bits);
 }
 
 int qconv_pack_act(const float* x, int n, int c, int h, int w, int bits, const float* thresholds,
                    uint32_t* out_packed, void* stream) {
-  if (n < 0 || c < 1 || h < 1 || w < 1 || !bits_ok(bits)) return QCONV_EINVAL;
+  if (n < 0 || c < 1 || h < 1 || w < 1 || !act_bits_ok(bits)) return QCONV_EINVAL;
   if (n > 0 && (!x || !out_packed)) return QCONV_EINVAL;
+  if (bits == 16) return launch_pack_act_f16(x, n, c, h, w, out_packed, (hipStream_t)stream);
   Thr t;
   const int rc = act_thresholds(bits, thresholds, &t);
   if (rc) return rc;
@@ -98,7 +100,7 @@ int qconv_pack_act(const float* x, int n, int c, int h, int w, int bits, const f
 size_t qconv_packed_weight_bytes(int cout, int cin, int kh, int kw, int bits) {
   if (cout < 1 || cin < 1 || kh < 1 || kw < 1 || !bits_ok(bits)) return 0;
   return wbytes_planes(cout, cin, kh, kw, bits) + wbytes_i8(cout, cin, kh, kw) +
-         wbytes_fp4(cout, cin, kh, kw);
+         wbytes_fp4(cout, cin, kh, kw) + wbytes_f16(cout, cin, kh, kw);
 }
 
 int qconv_pack_weight(const float* w, int cout, int cin, int kh, int kw, int bits,
@@ -145,15 +147,20 @@ int prepare_conv(const qconv_desc* d, const uint32_t* act_packed, const uint32_t
                  ConvArgs* args) {
   if (!d || !epi) return QCONV_EINVAL;
   if (d->n < 0 || d->cin < 1 || d->h < 1 || d->w < 1 || d->cout < 1 || d->kh < 1 || d->kw < 1 ||
-      d->stride < 1 || d->pad < 0 || !bits_ok(d->a_bits) || !bits_ok(d->w_bits))
+      d->stride < 1 || d->pad < 0 || !act_bits_ok(d->a_bits) || !bits_ok(d->w_bits))
     return QCONV_EINVAL;
-  if (d->algo < QCONV_ALGO_AUTO || d->algo > QCONV_ALGO_MFMA_FP4) return QCONV_EINVAL;
+  if (d->algo < QCONV_ALGO_AUTO || d->algo > QCONV_ALGO_MFMA_F16) return QCONV_EINVAL;
+  const bool a16 = d->a_bits == 16;
+  // 16-bit inputs run on the fp16 matrix cores only, and only they do
+  if (a16 ? (d->algo != QCONV_ALGO_AUTO && d->algo != QCONV_ALGO_MFMA_F16) : d->algo == QCONV_ALGO_MFMA_F16)
+    return QCONV_EUNSUPPORTED;
   const int ho = qconv_out_size(d->h, d->kh, d->stride, d->pad);
   const int wo = qconv_out_size(d->w, d->kw, d->stride, d->pad);
   if (ho < 1 || wo < 1) return QCONV_EINVAL;
   const int64_t K = (int64_t)d->cin * d->kh * d->kw;
-  if (K * max_code(d->a_bits) * max_code(d->w_bits) >= (int64_t)1 << 31) return QCONV_EOVERFLOW;
+  if (!a16 && K * max_code(d->a_bits) * max_code(d->w_bits) >= (int64_t)1 << 31) return QCONV_EOVERFLOW;
   if (epi->mode < QCONV_EPI_INT32 || epi->mode > QCONV_EPI_BN_PACK) return QCONV_EINVAL;
+  if (a16 && epi->mode == QCONV_EPI_INT32) return QCONV_EUNSUPPORTED;  // the accumulator is fp32
   if (epi->flags & ~(QCONV_EPI_POOL2 | QCONV_EPI_RESIDUAL)) return QCONV_EINVAL;
   const bool pool = (epi->flags & QCONV_EPI_POOL2) != 0;
   const bool resid = (epi->flags & QCONV_EPI_RESIDUAL) != 0;
@@ -213,14 +220,20 @@ int prepare_conv(const qconv_desc* d, const uint32_t* act_packed, const uint32_t
     const uint8_t* wb = reinterpret_cast<const uint8_t*>(w_packed);
     a.w_i8 = wb ? wb + wbytes_planes(d->cout, d->cin, d->kh, d->kw, d->w_bits) : nullptr;
     a.w_fp4 = wb ? a.w_i8 + wbytes_i8(d->cout, d->cin, d->kh, d->kw) : nullptr;
+    a.w_f16 = wb ? a.w_fp4 + wbytes_fp4(d->cout, d->cin, d->kh, d->kw) : nullptr;
+  }
+  if (a16) {
+    a.mfma_op = OP_F16;
+    if (d->n > 0 && !mfma_supports(a)) return QCONV_EUNSUPPORTED;
+    return QCONV_ALGO_MFMA_F16;
   }
   if (d->algo == QCONV_ALGO_MFMA_I8 || d->algo == QCONV_ALGO_MFMA_FP4) {
-    a.mfma_fp4 = d->algo == QCONV_ALGO_MFMA_FP4 ? 1 : 0;
+    a.mfma_op = d->algo == QCONV_ALGO_MFMA_FP4 ? OP_FP4 : OP_I8;
     if (d->n > 0 && !mfma_supports(a)) return QCONV_EUNSUPPORTED;
     return d->algo;
   }
   if (d->algo == QCONV_ALGO_AUTO && d->n > 0) {
-    a.mfma_fp4 = 1;
+    a.mfma_op = OP_FP4;
     if (mfma_supports(a)) return QCONV_ALGO_MFMA_FP4;
   }
   return QCONV_ALGO_BITPLANE;

@@ -6,6 +6,14 @@
 //   v_mfma_scale_f32_32x32x64_f8f6f4  (fp4 operands, unit scales, fp32 accumulate)
 // give the exact integer accumulator of the bitplane kernel.
 //
+// 16-bit inputs (Table I, rows with 16-bit inputs and 1..3-bit weights: the
+// "XNOR ADDER" / "SHIFT ADDER" operation at 16-bit floating precision): the
+// activations stay fp16 and the weight codes are exact in fp16, so
+//   v_mfma_f32_32x32x16_f16           (fp32 accumulate)
+// sums exact products; only the fp32 accumulation rounds.  The halo is
+// staged in LDS as it is stored (64 bytes per 32 channels), with the same
+// fragment addressing (32 bytes per k-step, 16 per lane half).
+//
 // Work unit.  The block's M dimension is a list of "units": output pixels, or
 // with 2x2 pooling whole pooling windows (the pooled output pixels), each of
 // which occupies four consecutive M rows.  A block owns a run of units of one
@@ -46,6 +54,7 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 typedef float v16f __attribute__((ext_vector_type(16)));
+typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 
 constexpr int MAX_LDS = 38 * 1024;  // one halo buffer (two per block, two blocks per CU)
 #ifndef QC_BRING
@@ -54,7 +63,7 @@ constexpr int MAX_LDS = 38 * 1024;  // one halo buffer (two per block, two block
 // Packed words of the next stage held per thread in registers (bounded by
 // the registers left next to the accumulators); items past 256 times this
 // are loaded when the stage is expanded.
-__host__ __device__ constexpr int halo_items_per_thread(int planes) { return planes == 1 ? 4 : 8 / planes; }  // one halo buffer (two per block, two blocks per CU)
+__host__ __device__ constexpr int halo_items_per_thread(int words) { return words == 1 ? 4 : words == 16 ? 1 : 8 / words; }
 
 // n / d by a multiply-high, exact whenever n * d < 2^32 (checked on the host
 // against the largest dividend of each use).
@@ -69,20 +78,29 @@ FastDiv make_fastdiv(uint32_t d) {
 }
 __device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv f) { return f.m ? __umulhi(n, f.m) : n; }
 
-template <int FP4>
+// Operand formats (MfmaOp): what one 32-channel word of a pixel becomes in
+// LDS and how many channels one k-step of the MFMA consumes.
+template <int OPK>
 struct OpT;
 template <>
-struct OpT<0> {
+struct OpT<OP_I8> {
   static constexpr int CHUNK_WORDS = 4;  // 32-channel words staged per chunk
   static constexpr int WORD_BYTES = 32;  // LDS bytes per word per pixel
-  static constexpr int WORDS_PER_STEP = 1;
+  static constexpr int K_PER_STEP = 32;  // channels per k-step
   using acc_t = v16i;
 };
 template <>
-struct OpT<1> {
+struct OpT<OP_FP4> {
   static constexpr int CHUNK_WORDS = 8;
   static constexpr int WORD_BYTES = 16;
-  static constexpr int WORDS_PER_STEP = 2;
+  static constexpr int K_PER_STEP = 64;
+  using acc_t = v16f;
+};
+template <>
+struct OpT<OP_F16> {
+  static constexpr int CHUNK_WORDS = 2;
+  static constexpr int WORD_BYTES = 64;
+  static constexpr int K_PER_STEP = 16;
   using acc_t = v16f;
 };
 
@@ -124,7 +142,7 @@ struct MfmaArgs {
   FastDiv fd_slot, fd_hc, fd_cwc;
   int pix_bytes;      // LDS bytes per halo pixel
   int chunk_words;    // words staged per chunk
-  int ksteps;         // k-steps per tap over all words (int8: cw, fp4: ceil(cw/2))
+  int ksteps;         // k-steps per tap over all words (int8: cw, fp4: ceil(cw/2), fp16: 2 cw)
   int nchunks;
   int vec;            // upi % 4 == 0: four consecutive units are one aligned 16-byte run
   int tiles_px, tiles_co;
@@ -136,14 +154,20 @@ struct MfmaArgs {
   int act_bytes;      // byte size of the packed activations (buffer-resource bound; 0 if >= 2^31)
 };
 
-__device__ __forceinline__ v16i mfma(v4i a, v4i b, v16i c) {
-  return __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, c, 0, 0, 0);
-}
-__device__ __forceinline__ v16f mfma(v4i a, v4i b, v16f c) {
-  v8i a8 = {a[0], a[1], a[2], a[3], 0, 0, 0, 0};
-  v8i b8 = {b[0], b[1], b[2], b[3], 0, 0, 0, 0};
-  // operand format 4 = E2M1 for both; scales 127 = 2^0
-  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, c, 4, 4, 0, 127, 0, 127);
+// One 32 x 32 MFMA of operand format OPK on 16-byte fragments.
+template <int OPK, class AccT>
+__device__ __forceinline__ AccT mfma(v4i a, v4i b, AccT c) {
+  if constexpr (OPK == OP_I8) {
+    return __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, c, 0, 0, 0);
+  } else if constexpr (OPK == OP_FP4) {
+    v8i a8 = {a[0], a[1], a[2], a[3], 0, 0, 0, 0};
+    v8i b8 = {b[0], b[1], b[2], b[3], 0, 0, 0, 0};
+    // operand format 4 = E2M1 for both; scales 127 = 2^0
+    return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, c, 4, 4, 0, 127, 0, 127);
+  } else {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(v8h, a), __builtin_bit_cast(v8h, b), c, 0,
+                                                  0, 0);
+  }
 }
 // Accumulator register as an exact float / int.
 __device__ __forceinline__ float acc_f(const v16i& a, int v) { return (float)a[v]; }
@@ -151,9 +175,15 @@ __device__ __forceinline__ float acc_f(const v16f& a, int v) { return a[v]; }
 __device__ __forceinline__ int acc_i(const v16i& a, int v) { return a[v]; }
 __device__ __forceinline__ int acc_i(const v16f& a, int v) { return (int)a[v]; }
 
-template <int FP4, int PA>
+// One word of a halo pixel into LDS in operand format OPK (fp16 words are
+// already operands: 64 bytes copied as they are).
+template <int OPK, int PA>
 __device__ __forceinline__ void expand_to_lds(const uint32_t* pl, uint8_t* dst) {
-  if constexpr (FP4) {
+  if constexpr (OPK == OP_F16) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      reinterpret_cast<uint4*>(dst)[q] = make_uint4(pl[4 * q], pl[4 * q + 1], pl[4 * q + 2], pl[4 * q + 3]);
+  } else if constexpr (OPK == OP_FP4) {
     uint32_t o[4];
     expand_fp4_word<PA>(pl, 0xFFFFFFFFu, o);
     *reinterpret_cast<uint4*>(dst) = make_uint4(o[0], o[1], o[2], o[3]);
@@ -634,11 +664,14 @@ __device__ __forceinline__ void load_halo(const MfmaArgs& m, int img0, int iy0, 
           raw[u][0] = v.x;
           raw[u][1] = v.y;
         } else {
-          const uint4 v = *reinterpret_cast<const uint4*>(src);
-          raw[u][0] = v.x;
-          raw[u][1] = v.y;
-          raw[u][2] = v.z;
-          raw[u][3] = v.w;
+#pragma unroll
+          for (int q = 0; q < PA / 4; ++q) {
+            const uint4 v = reinterpret_cast<const uint4*>(src)[q];
+            raw[u][4 * q] = v.x;
+            raw[u][4 * q + 1] = v.y;
+            raw[u][4 * q + 2] = v.z;
+            raw[u][4 * q + 3] = v.w;
+          }
         }
       }
     }
@@ -647,7 +680,7 @@ __device__ __forceinline__ void load_halo(const MfmaArgs& m, int img0, int iy0, 
 
 // Expands this thread's share of a halo tile into an LDS buffer: the items
 // already held in raw, then any items past NI * 256 loaded here directly.
-template <int FP4, int PA, int NI>
+template <int OPK, int PA, int NI>
 __device__ __forceinline__ void store_halo(const MfmaArgs& m, int img0, int iy0, int chunk, int tid,
                                            const uint32_t (&raw)[NI][PA], uint8_t* buf) {
   const int items = m.ipb * m.slot_pix * m.chunk_words;
@@ -657,7 +690,7 @@ __device__ __forceinline__ void store_halo(const MfmaArgs& m, int img0, int iy0,
     if (it < items) {
       const int hp = (int)fdiv((uint32_t)it, m.fd_cwc);
       const int cwl = it - hp * m.chunk_words;
-      expand_to_lds<FP4, PA>(raw[u], buf + hp * m.pix_bytes + cwl * OpT<FP4>::WORD_BYTES);
+      expand_to_lds<OPK, PA>(raw[u], buf + hp * m.pix_bytes + cwl * OpT<OPK>::WORD_BYTES);
     }
   }
   for (int it = NI * 256 + tid; it < items; it += 256) {
@@ -665,7 +698,7 @@ __device__ __forceinline__ void store_halo(const MfmaArgs& m, int img0, int iy0,
     load_halo<PA, 1>(m, img0, iy0, chunk, it, one);
     const int hp = (int)fdiv((uint32_t)it, m.fd_cwc);
     const int cwl = it - hp * m.chunk_words;
-    expand_to_lds<FP4, PA>(one[0], buf + hp * m.pix_bytes + cwl * OpT<FP4>::WORD_BYTES);
+    expand_to_lds<OPK, PA>(one[0], buf + hp * m.pix_bytes + cwl * OpT<OPK>::WORD_BYTES);
   }
 }
 
@@ -688,9 +721,9 @@ __device__ __forceinline__ void load_params(const ConvArgs& a, int co_blk, int t
 // the MFMAs of stage s and expanded into the other of two LDS halo buffers
 // after them, so that global latency, the expansion and the epilogue's
 // stores overlap the matrix work.  Split-K shapes run one item per block.
-template <int FP4, int PA, int CFG, int SWAP>
+template <int OPK, int PA, int CFG, int SWAP>
 __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
-  using O = OpT<FP4>;
+  using O = OpT<OPK>;
   using acc_t = typename O::acc_t;
   using C = Cfg<CFG>;
   constexpr int MT = C::MT, NT = C::NT, WN = C::WN, SK = C::SK;
@@ -717,7 +750,7 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
   uint32_t raw[NI][PA];
   load_halo<PA, NI>(m, cur.img0, cur.iy0, 0, tid, raw);
   if constexpr (SWAP) load_params<BCO>(a, cur.co_blk, tid, prm_base);
-  store_halo<FP4, PA, NI>(m, cur.img0, cur.iy0, 0, tid, raw, halo_base);
+  store_halo<OPK, PA, NI>(m, cur.img0, cur.iy0, 0, tid, raw, halo_base);
   __syncthreads();
 
   acc_t acc[MT][NT];
@@ -735,7 +768,7 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
       __builtin_amdgcn_make_buffer_rsrc((void*)m.wx, (short)0, m.wx_bytes, 0x00020000);
   const int bstride = a.cop * 32;  // bytes between consecutive k-steps
   const int taps = a.kh * a.kw;
-  const int steps_per_chunk = m.chunk_words / O::WORDS_PER_STEP;
+  const int steps_per_chunk = m.chunk_words * 32 / O::K_PER_STEP;
   int chunk = 0, sbuf = 0, ipar = 0;
 
   for (;;) {
@@ -806,9 +839,9 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
 #pragma unroll
             for (int j = 0; j < NT; ++j) {
               if constexpr (SWAP)
-                acc[i][j] = mfma(bf[j], Acur[i], acc[i][j]);
+                acc[i][j] = mfma<OPK>(bf[j], Acur[i], acc[i][j]);
               else
-                acc[i][j] = mfma(Acur[i], bf[j], acc[i][j]);
+                acc[i][j] = mfma<OPK>(Acur[i], bf[j], acc[i][j]);
             }
         };
 #if QC_BRING == 3
@@ -844,7 +877,7 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
     // ---- the next stage's halo into the other buffer (the epilogue below
     // reads no halo buffer; a split-K block never has a next stage) ----
     if (has_next)
-      store_halo<FP4, PA, NI>(m, nimg0, niy0, nchunk, tid, raw, halo_base + (sbuf ^ 1) * buf_bytes);
+      store_halo<OPK, PA, NI>(m, nimg0, niy0, nchunk, tid, raw, halo_base + (sbuf ^ 1) * buf_bytes);
 
     // ---- epilogue of a finished item ----
     if (chunk == m.nchunks - 1) {
@@ -1011,7 +1044,7 @@ __device__ __forceinline__ void load_halo_rsrc(const MfmaArgs& m, __amdgpu_buffe
 
 // Expands a thread's share of a halo tile into LDS: the NI items held in raw,
 // then the items past NI * STRIDE, loaded here one at a time.
-template <int FP4, int PA, int NI, int STRIDE>
+template <int OPK, int PA, int NI, int STRIDE>
 __device__ __forceinline__ void expand_halo(const MfmaArgs& m, __amdgpu_buffer_rsrc_t rsrc, int img0, int iy0,
                                             int tid, const uint32_t (&raw)[NI][PA], uint8_t* buf) {
   const int items = m.ipb * m.slot_pix * m.chunk_words;
@@ -1020,7 +1053,7 @@ __device__ __forceinline__ void expand_halo(const MfmaArgs& m, __amdgpu_buffer_r
     const int it = tid + STRIDE * u;
     if (it < items) {
       const int hp = (int)fdiv((uint32_t)it, m.fd_cwc);
-      expand_to_lds<FP4, PA>(raw[u], buf + hp * m.pix_bytes + (it - hp * m.chunk_words) * OpT<FP4>::WORD_BYTES);
+      expand_to_lds<OPK, PA>(raw[u], buf + hp * m.pix_bytes + (it - hp * m.chunk_words) * OpT<OPK>::WORD_BYTES);
     }
   }
   for (int it0 = NI * STRIDE; it0 < items; it0 += STRIDE) {
@@ -1029,7 +1062,7 @@ __device__ __forceinline__ void expand_halo(const MfmaArgs& m, __amdgpu_buffer_r
     const int it = it0 + tid;
     if (it < items) {
       const int hp = (int)fdiv((uint32_t)it, m.fd_cwc);
-      expand_to_lds<FP4, PA>(one[0], buf + hp * m.pix_bytes + (it - hp * m.chunk_words) * OpT<FP4>::WORD_BYTES);
+      expand_to_lds<OPK, PA>(one[0], buf + hp * m.pix_bytes + (it - hp * m.chunk_words) * OpT<OPK>::WORD_BYTES);
     }
   }
 }
@@ -1069,9 +1102,9 @@ constexpr int PP_GROUP = 512;  // threads per wave group
 // buffer per group.  Serves unpacked, unpooled outputs (pixels as the A
 // operand, so that a lane holds one channel); needs a single channel chunk
 // and packed activations below 2 GiB.
-template <int FP4, int PA, int CFG>
+template <int OPK, int PA, int CFG>
 __global__ __launch_bounds__(1024, 1) void conv_mfma_pp_kernel(const MfmaArgs m) {
-  using O = OpT<FP4>;
+  using O = OpT<OPK>;
   using acc_t = typename O::acc_t;
   using C = PCfg<CFG>;
   constexpr int MT = C::MT, NT = C::NT, WN = C::WN;
@@ -1133,7 +1166,7 @@ __global__ __launch_bounds__(1024, 1) void conv_mfma_pp_kernel(const MfmaArgs m)
     }
     load_params<BCO>(a, co_blk, gtid0, prm);
   } else {
-    expand_halo<FP4, PA, NI, PP_GROUP>(m, arsrc, img0, iy0, gtid0, raw, halo);
+    expand_halo<OPK, PA, NI, PP_GROUP>(m, arsrc, img0, iy0, gtid0, raw, halo);
   }
   // Explicit waits for every outstanding global access where that costs
   // nothing (here, and at the start of each store phase, where the only ones
@@ -1196,7 +1229,7 @@ __global__ __launch_bounds__(1024, 1) void conv_mfma_pp_kernel(const MfmaArgs m)
 #pragma unroll
       for (int i = 0; i < MT; ++i)
 #pragma unroll
-        for (int j = 0; j < NT; ++j) acc[i][j] = mfma(B[j], A[i], acc[i][j]);
+        for (int j = 0; j < NT; ++j) acc[i][j] = mfma<OPK>(B[j], A[i], acc[i][j]);
     };
     v4i AX[MT], BX[NT], AY[MT], BY[NT];
     fetch(AX, BX);                  // step 0
@@ -1206,7 +1239,7 @@ __global__ __launch_bounds__(1024, 1) void conv_mfma_pp_kernel(const MfmaArgs m)
 #pragma unroll
       for (int i = 0; i < MT; ++i)
 #pragma unroll
-        for (int j = 0; j < NT; ++j) acc[i][j] = mfma(BX[j], AX[i], zero);
+        for (int j = 0; j < NT; ++j) acc[i][j] = mfma<OPK>(BX[j], AX[i], zero);
     }
     // steps 1 .. nsteps - 1 in pairs (Y, X); reads run one step ahead
     int st = 1;
@@ -1239,7 +1272,7 @@ __global__ __launch_bounds__(1024, 1) void conv_mfma_pp_kernel(const MfmaArgs m)
       const int it = gt + PP_GROUP * U;
       if (stage && it < items) {
         const int hp = (int)fdiv((uint32_t)it, m.fd_cwc);
-        expand_to_lds<FP4, PA>(raw[U], halo + hp * m.pix_bytes + (it - hp * m.chunk_words) * O::WORD_BYTES);
+        expand_to_lds<OPK, PA>(raw[U], halo + hp * m.pix_bytes + (it - hp * m.chunk_words) * O::WORD_BYTES);
       }
     };
     const bool st = k >= 1 && co_w < a.cout;
@@ -1292,7 +1325,7 @@ __global__ __launch_bounds__(1024, 1) void conv_mfma_pp_kernel(const MfmaArgs m)
         const int it = it0 + gt;
         if (it < items) {
           const int hp = (int)fdiv((uint32_t)it, m.fd_cwc);
-          expand_to_lds<FP4, PA>(one[0], halo + hp * m.pix_bytes + (it - hp * m.chunk_words) * O::WORD_BYTES);
+          expand_to_lds<OPK, PA>(one[0], halo + hp * m.pix_bytes + (it - hp * m.chunk_words) * O::WORD_BYTES);
         }
       }
     }
@@ -1324,13 +1357,18 @@ __global__ __launch_bounds__(1024, 1) void conv_mfma_pp_kernel(const MfmaArgs m)
 bool plan(const ConvArgs& a, int cfg, MfmaArgs* m) {
   memset(m, 0, sizeof(*m));
   m->c = a;
-  const int fp4 = a.mfma_fp4;
-  const int chunk_max = fp4 ? OpT<1>::CHUNK_WORDS : OpT<0>::CHUNK_WORDS;
-  const int wpstep = fp4 ? 2 : 1;
-  const int word_bytes = fp4 ? 16 : 32;
+  const int op = a.mfma_op;
+  if ((op == OP_F16) != (a.a_bits == 16)) return false;  // fp16 operands exactly for 16-bit inputs
+  const int chunk_max = op == OP_FP4 ? OpT<OP_FP4>::CHUNK_WORDS
+                                     : (op == OP_F16 ? OpT<OP_F16>::CHUNK_WORDS : OpT<OP_I8>::CHUNK_WORDS);
+  const int wpstep = op == OP_FP4 ? 2 : 1;  // words per k-step, rounded up to whole words
+  const int word_bytes = op == OP_FP4 ? OpT<OP_FP4>::WORD_BYTES
+                                      : (op == OP_F16 ? OpT<OP_F16>::WORD_BYTES : OpT<OP_I8>::WORD_BYTES);
+  const int k_per_step = op == OP_FP4 ? OpT<OP_FP4>::K_PER_STEP
+                                      : (op == OP_F16 ? OpT<OP_F16>::K_PER_STEP : OpT<OP_I8>::K_PER_STEP);
   const int cw_round = ceil_div(a.cw, wpstep) * wpstep;
-  m->ksteps = ceil_div(a.cw, wpstep);
-  m->wx = fp4 ? a.w_fp4 : a.w_i8;
+  m->ksteps = ceil_div(a.cw * 32, k_per_step);
+  m->wx = op == OP_FP4 ? a.w_fp4 : (op == OP_F16 ? a.w_f16 : a.w_i8);
   const int64_t wxb = (int64_t)a.kh * a.kw * m->ksteps * a.cop * 32;
   if (wxb >= ((int64_t)1 << 31)) return false;
   m->wx_bytes = (int)wxb;
@@ -1404,7 +1442,7 @@ bool plan(const ConvArgs& a, int cfg, MfmaArgs* m) {
     const Thr& t = a.othr;
     m->ht_needed = (a.out_bits == 2 && t.t0 >= 1.0f) || (a.out_bits == 3 && t.t2 >= 1.0f);
   }
-  const int64_t ab = (int64_t)a.n * a.h * a.w * a.cw * planes_of(a.a_bits) * 4;
+  const int64_t ab = (int64_t)a.n * a.h * a.w * a.cw * act_words(a.a_bits) * 4;
   m->act_bytes = ab < ((int64_t)1 << 31) ? (int)ab : 0;
   const int64_t ob = (int64_t)a.n * a.cout * m->upi * 4;
   m->out_bytes = ob < ((int64_t)1 << 31) ? (int)ob : 0;
@@ -1474,22 +1512,22 @@ size_t pp_lds(const MfmaArgs& m, int cfg) {
 // whose channels fit one stage and whose weights fit next to two halo
 // buffers, when every block gets at least one item per group.
 bool use_pp(const MfmaArgs& m, int cfg, int cus) {
-  if (cfg == 2 || !use_swap(m) || m.nchunks != 1 || m.act_bytes == 0) return false;
+  if (cfg == 2 || m.c.mfma_op == OP_F16 || !use_swap(m) || m.nchunks != 1 || m.act_bytes == 0) return false;
   if (pp_lds(m, cfg) > (size_t)LDS_PER_CU) return false;
   return (int64_t)m.tiles_px * m.tiles_co >= 2 * (int64_t)cus;
 }
 
-template <int FP4, int PA, int CFG>
+template <int OPK, int PA, int CFG>
 int launch_cfg(MfmaArgs m, hipStream_t s) {
   const size_t lds = block_lds(m);
   const int total = m.tiles_px * m.tiles_co;
   const int cus = device_cus();
-  if constexpr (CFG != 2) {
+  if constexpr (CFG != 2 && OPK != OP_F16) {
     if (use_pp(m, CFG, cus)) {
       const size_t plds = pp_lds(m, CFG);
       // every block keeps one output-channel tile: a multiple of tiles_co blocks
       m.grid = max(m.tiles_co, (min(total, cus) / m.tiles_co) * m.tiles_co);
-      auto kern = conv_mfma_pp_kernel<FP4, PA, CFG>;
+      auto kern = conv_mfma_pp_kernel<OPK, PA, CFG>;
       // the dynamic-LDS limit of this instantiation, raised once per device
       static std::atomic<int> lds_set[MAX_DEVICES];
       int dev = 0;
@@ -1512,25 +1550,25 @@ int launch_cfg(MfmaArgs m, hipStream_t s) {
     m.grid = min(total, per_cu * cus);
   }
   if (use_swap(m))
-    conv_mfma_kernel<FP4, PA, CFG, 1><<<dim3((unsigned)m.grid), 256, lds, s>>>(m);
+    conv_mfma_kernel<OPK, PA, CFG, 1><<<dim3((unsigned)m.grid), 256, lds, s>>>(m);
   else
-    conv_mfma_kernel<FP4, PA, CFG, 0><<<dim3((unsigned)m.grid), 256, lds, s>>>(m);
+    conv_mfma_kernel<OPK, PA, CFG, 0><<<dim3((unsigned)m.grid), 256, lds, s>>>(m);
   return hip_status();
 }
 
-template <int FP4, int PA>
+template <int OPK, int PA>
 int launch_fp(const MfmaArgs& m, int cfg, hipStream_t s) {
 #ifdef QC_ONLY_ONE
-  if constexpr (!(FP4 == QC_ONLY_FP4 && PA == QC_ONLY_PA)) {
+  if constexpr (!(OPK == QC_ONLY_OPK && PA == QC_ONLY_PA)) {
     return QCONV_EUNSUPPORTED;
   } else {
-    return launch_cfg<FP4, PA, 0>(m, s);
+    return launch_cfg<OPK, PA, 0>(m, s);
     (void)cfg;
   }
 #else
-  if (cfg == 0) return launch_cfg<FP4, PA, 0>(m, s);
-  if (cfg == 1) return launch_cfg<FP4, PA, 1>(m, s);
-  return launch_cfg<FP4, PA, 2>(m, s);
+  if (cfg == 0) return launch_cfg<OPK, PA, 0>(m, s);
+  if (cfg == 1) return launch_cfg<OPK, PA, 1>(m, s);
+  return launch_cfg<OPK, PA, 2>(m, s);
 #endif
 }
 
@@ -1548,9 +1586,9 @@ int mfma_kernel_name(const ConvArgs& a, char* buf, int len) {
   if (!plan(a, cfg, &m)) return QCONV_EUNSUPPORTED;
   char name[96];
   if (use_pp(m, cfg, device_cus()))
-    snprintf(name, sizeof(name), "conv_mfma_pp_kernel<%d, %d, %d>", a.mfma_fp4, planes_of(a.a_bits), cfg);
+    snprintf(name, sizeof(name), "conv_mfma_pp_kernel<%d, %d, %d>", a.mfma_op, act_words(a.a_bits), cfg);
   else
-    snprintf(name, sizeof(name), "conv_mfma_kernel<%d, %d, %d, %d>", a.mfma_fp4, planes_of(a.a_bits), cfg,
+    snprintf(name, sizeof(name), "conv_mfma_kernel<%d, %d, %d, %d>", a.mfma_op, act_words(a.a_bits), cfg,
              use_swap(m) ? 1 : 0);
   if (buf && len > 0) snprintf(buf, (size_t)len, "%s", name);
   return (int)strlen(name);
@@ -1560,15 +1598,16 @@ int launch_conv_mfma(const ConvArgs& a, hipStream_t s) {
   MfmaArgs m;
   const int cfg = pick_cfg(a);
   if (!plan(a, cfg, &m)) return QCONV_EUNSUPPORTED;
-  const int pa = planes_of(a.a_bits);
-  if (a.mfma_fp4) {
-    if (pa == 1) return launch_fp<1, 1>(m, cfg, s);
-    if (pa == 2) return launch_fp<1, 2>(m, cfg, s);
-    return launch_fp<1, 4>(m, cfg, s);
+  const int pa = act_words(a.a_bits);
+  if (a.mfma_op == OP_F16) return launch_fp<OP_F16, 16>(m, cfg, s);
+  if (a.mfma_op == OP_FP4) {
+    if (pa == 1) return launch_fp<OP_FP4, 1>(m, cfg, s);
+    if (pa == 2) return launch_fp<OP_FP4, 2>(m, cfg, s);
+    return launch_fp<OP_FP4, 4>(m, cfg, s);
   }
-  if (pa == 1) return launch_fp<0, 1>(m, cfg, s);
-  if (pa == 2) return launch_fp<0, 2>(m, cfg, s);
-  return launch_fp<0, 4>(m, cfg, s);
+  if (pa == 1) return launch_fp<OP_I8, 1>(m, cfg, s);
+  if (pa == 2) return launch_fp<OP_I8, 2>(m, cfg, s);
+  return launch_fp<OP_I8, 4>(m, cfg, s);
 }
 
 }  // namespace qc

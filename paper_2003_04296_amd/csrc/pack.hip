@@ -6,8 +6,12 @@
 // so each of the 32 channel reads of a wave is one contiguous 256-byte run
 // (HBM-bound: 4 bytes read per channel, P/8 bytes written).
 //
+// 16-bit inputs: fp32 NCHW -> fp16 [n][h][w][cw * 32] (round to nearest
+// even; channels past c are +0), with the same thread mapping.
+//
 // Weights: fp32 OIHW -> per-channel scale s_c = mean|W_c| (double, storage
-// order) -> thresholds scaled by s_c -> bitplanes [kh][kw][cw][cout_pad][P].
+// order) -> thresholds scaled by s_c -> bitplanes [kh][kw][cw][cout_pad][P],
+// then the int8, fp4 and fp16 matrix-core operand copies of the same codes.
 #include "qconv_internal.h"
 
 namespace qc {
@@ -48,6 +52,39 @@ __global__ __launch_bounds__(256) void pack_act_kernel(const float* __restrict__
   uint32_t* dst = out + ((b * hw + pix) * cwn + cw) * P;
 #pragma unroll
   for (int p = 0; p < P; ++p) dst[p] = word[p];
+}
+
+__device__ __forceinline__ uint32_t f16_bits(float v) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v);
+}
+
+__global__ __launch_bounds__(256) void pack_act_f16_kernel(const float* __restrict__ x, int c, int hw, int cwn,
+                                                           int64_t total, uint32_t* __restrict__ out) {
+  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (tid >= total) return;
+  const int pix = (int)(tid % hw);
+  const int64_t r = tid / hw;
+  const int cw = (int)(r % cwn);
+  const int64_t b = r / cwn;
+  const int c0 = cw * 32;
+  const int nch = min(32, c - c0);
+  const float* src = x + (b * c + c0) * (int64_t)hw + pix;
+  uint32_t h[16];
+  if (nch == 32) {
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+      h[j] = f16_bits(src[(int64_t)(2 * j) * hw]) | (f16_bits(src[(int64_t)(2 * j + 1) * hw]) << 16);
+  } else {
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const uint32_t lo = 2 * j < nch ? f16_bits(src[(int64_t)(2 * j) * hw]) : 0u;
+      const uint32_t hi = 2 * j + 1 < nch ? f16_bits(src[(int64_t)(2 * j + 1) * hw]) : 0u;
+      h[j] = lo | (hi << 16);
+    }
+  }
+  uint4* dst = reinterpret_cast<uint4*>(out + ((b * hw + pix) * cwn + cw) * 16);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) dst[q] = make_uint4(h[4 * q], h[4 * q + 1], h[4 * q + 2], h[4 * q + 3]);
 }
 
 // s_c = (float)(sum_k |W_ck| / K), the sum in double in storage order.
@@ -102,26 +139,64 @@ __global__ __launch_bounds__(256) void pack_weight_kernel(const float* __restric
   for (int p = 0; p < P; ++p) dst[p] = word[p];
 }
 
+// Channels of a 32-channel word that exist, given how many remain (>= 1).
+__device__ __forceinline__ uint32_t chan_mask(int remaining) {
+  return remaining >= 32 ? 0xFFFFFFFFu : ((1u << remaining) - 1u);
+}
+
+// int8 code byte -> fp16 bits (exact: the codes are 0, +-1, +-2, +-4).
+__device__ __forceinline__ uint32_t code_f16(uint32_t word, int byte) {
+  return f16_bits((float)(int8_t)(word >> (8 * byte)));
+}
+
 // Matrix-core operand copies of packed weights: one thread per
 // (tap, word, output channel) for int8 (32 bytes), per (tap, word pair,
-// output channel) for fp4 (32 bytes = 64 nibbles).
+// output channel) for fp4 (32 bytes = 64 nibbles), per (tap, 16-channel
+// k-step, output channel) for fp16 (32 bytes = 16 halves).  Channels past
+// cin and padding output channels get code 0 (a 1-bit sign plane alone
+// would read as -1 there).
 template <int P>
 __global__ __launch_bounds__(256) void expand_weight_kernel(const uint32_t* __restrict__ planes,
-                                                            int taps, int cwn, int cop, int cin,
+                                                            int taps, int cwn, int cout, int cop, int cin,
                                                             uint8_t* __restrict__ w_i8,
-                                                            uint8_t* __restrict__ w_fp4) {
+                                                            uint8_t* __restrict__ w_fp4,
+                                                            uint8_t* __restrict__ w_f16) {
   const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int cwp = (cwn + 1) / 2;
   const int64_t n_i8 = (int64_t)taps * cwn * cop;
   const int64_t n_fp4 = (int64_t)taps * cwp * cop;
-  if (tid < n_i8) {
+  const int64_t n_f16 = (int64_t)taps * 2 * cwn * cop;
+  if (tid >= n_i8 + n_fp4 && tid < n_i8 + n_fp4 + n_f16) {
+    const int64_t u = tid - n_i8 - n_fp4;
+    const int co = (int)(u % cop);
+    const int64_t r = u / cop;
+    const int ks = (int)(r % (2 * cwn));
+    const int tap = (int)(r / (2 * cwn));
+    const int cw = ks >> 1, half = ks & 1;
+    const uint32_t* src = planes + (((int64_t)tap * cwn + cw) * cop + co) * P;
+    const uint32_t valid = co < cout ? chan_mask(cin - cw * 32) : 0u;
+    uint32_t pl[P];
+#pragma unroll
+    for (int p = 0; p < P; ++p) pl[p] = src[p];
+    uint32_t o[8];
+    expand_i8_word<P>(pl, valid, o);
+    uint32_t hv[8];  // channels 16 half .. 16 half + 15 as fp16 pairs
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t wd = o[4 * half + q];
+      hv[2 * q] = code_f16(wd, 0) | (code_f16(wd, 1) << 16);
+      hv[2 * q + 1] = code_f16(wd, 2) | (code_f16(wd, 3) << 16);
+    }
+    uint4* dst = reinterpret_cast<uint4*>(w_f16 + u * 32);
+    dst[0] = make_uint4(hv[0], hv[1], hv[2], hv[3]);
+    dst[1] = make_uint4(hv[4], hv[5], hv[6], hv[7]);
+  } else if (tid < n_i8) {
     const int co = (int)(tid % cop);
     const int64_t r = tid / cop;
     const int cw = (int)(r % cwn);
     const int tap = (int)(r / cwn);
     const uint32_t* src = planes + (((int64_t)tap * cwn + cw) * cop + co) * P;
-    const int nvalid = min(32, cin - cw * 32);
-    const uint32_t valid = nvalid >= 32 ? 0xFFFFFFFFu : ((1u << nvalid) - 1u);
+    const uint32_t valid = co < cout ? chan_mask(cin - cw * 32) : 0u;
     uint32_t pl[P];
 #pragma unroll
     for (int p = 0; p < P; ++p) pl[p] = src[p];
@@ -148,8 +223,7 @@ __global__ __launch_bounds__(256) void expand_weight_kernel(const uint32_t* __re
         const uint32_t* src = planes + (((int64_t)tap * cwn + cw) * cop + co) * P;
 #pragma unroll
         for (int p = 0; p < P; ++p) pl[p] = src[p];
-        const int nvalid = min(32, cin - cw * 32);
-        valid = nvalid >= 32 ? 0xFFFFFFFFu : ((1u << nvalid) - 1u);
+        valid = co < cout ? chan_mask(cin - cw * 32) : 0u;
       }
       expand_fp4_word<P>(pl, valid, o + 4 * half);
     }
@@ -176,6 +250,15 @@ int launch_pack_act(const float* x, int n, int c, int h, int w, int bits, Thr t,
   return hip_status();
 }
 
+int launch_pack_act_f16(const float* x, int n, int c, int h, int w, uint32_t* out, hipStream_t s) {
+  const int hw = h * w;
+  const int cwn = ceil_div(c, 32);
+  const int64_t total = (int64_t)n * cwn * hw;
+  if (total == 0) return QCONV_OK;
+  pack_act_f16_kernel<<<dim3((unsigned)((total + 255) / 256)), 256, 0, s>>>(x, c, hw, cwn, total, out);
+  return hip_status();
+}
+
 int launch_pack_weight(const float* w, int cout, int cin, int kh, int kw, int bits,
                        const float* base_thr, uint32_t* out, float* scale, hipStream_t s) {
   const int k = cin * kh * kw;
@@ -192,13 +275,15 @@ int launch_pack_weight(const float* w, int cout, int cin, int kh, int kw, int bi
   }
   uint8_t* w_i8 = reinterpret_cast<uint8_t*>(out) + wbytes_planes(cout, cin, kh, kw, bits);
   uint8_t* w_fp4 = w_i8 + wbytes_i8(cout, cin, kh, kw);
+  uint8_t* w_f16 = w_fp4 + wbytes_fp4(cout, cin, kh, kw);
   const int taps = kh * kw;
-  const int64_t items = (int64_t)taps * cwn * cop + (int64_t)taps * ((cwn + 1) / 2) * cop;
+  const int64_t items =
+      (int64_t)taps * cwn * cop + (int64_t)taps * ((cwn + 1) / 2) * cop + (int64_t)taps * 2 * cwn * cop;
   const dim3 g2((unsigned)((items + 255) / 256));
   switch (bits) {
-    case 1: expand_weight_kernel<1><<<g2, 256, 0, s>>>(out, taps, cwn, cop, cin, w_i8, w_fp4); break;
-    case 2: expand_weight_kernel<2><<<g2, 256, 0, s>>>(out, taps, cwn, cop, cin, w_i8, w_fp4); break;
-    default: expand_weight_kernel<4><<<g2, 256, 0, s>>>(out, taps, cwn, cop, cin, w_i8, w_fp4); break;
+    case 1: expand_weight_kernel<1><<<g2, 256, 0, s>>>(out, taps, cwn, cout, cop, cin, w_i8, w_fp4, w_f16); break;
+    case 2: expand_weight_kernel<2><<<g2, 256, 0, s>>>(out, taps, cwn, cout, cop, cin, w_i8, w_fp4, w_f16); break;
+    default: expand_weight_kernel<4><<<g2, 256, 0, s>>>(out, taps, cwn, cout, cop, cin, w_i8, w_fp4, w_f16); break;
   }
   return hip_status();
 }

@@ -120,7 +120,7 @@ __device__ __forceinline__ void expand_fp4_word(const uint32_t* pl, uint32_t val
   }
 }
 
-// Byte sizes / offsets of the three parts of a packed weight buffer.
+// Byte sizes of the four parts of a packed weight buffer.
 inline size_t wbytes_planes(int cout, int cin, int kh, int kw, int bits) {
   return (size_t)kh * kw * ceil_div(cin, 32) * cout_pad(cout) * planes_of(bits) * 4;
 }
@@ -130,12 +130,21 @@ inline size_t wbytes_i8(int cout, int cin, int kh, int kw) {
 inline size_t wbytes_fp4(int cout, int cin, int kh, int kw) {
   return (size_t)kh * kw * ceil_div(ceil_div(cin, 32), 2) * cout_pad(cout) * 32;
 }
+// fp16 codes, 16 channels (32 bytes) per (tap, k-step, output channel).
+inline size_t wbytes_f16(int cout, int cin, int kh, int kw) {
+  return (size_t)kh * kw * 2 * ceil_div(cin, 32) * cout_pad(cout) * 32;
+}
+
+// 32-bit words per (pixel, 32-channel word) of an activation tensor: the
+// bitplanes of 1..3-bit levels, or 32 fp16 values of a 16-bit input.
+__host__ __device__ constexpr int act_words(int bits) { return bits == 16 ? 16 : planes_of(bits); }
 
 // ---------------------------------------------------------------------------
 // Launchers (each returns a qconv_status; inputs already validated).
 // ---------------------------------------------------------------------------
 int launch_pack_act(const float* x, int n, int c, int h, int w, int bits, Thr t, uint32_t* out,
                     hipStream_t s);
+int launch_pack_act_f16(const float* x, int n, int c, int h, int w, uint32_t* out, hipStream_t s);
 int launch_pack_weight(const float* w, int cout, int cin, int kh, int kw, int bits,
                        const float* base_thr, uint32_t* out, float* scale, hipStream_t s);
 
@@ -149,7 +158,7 @@ struct ConvArgs {
   int oh_out, ow_out;     // output size after optional 2x2 pooling
   int kreal;              // cin * kh * kw
   int shift;              // acc_real = acc * 2^-shift
-  int a_bits, w_bits;
+  int a_bits, w_bits;     // a_bits 16: fp16 activations [n][h][w][cw * 32]
   // epilogue
   int mode, pool, residual_on;
   const float* scale;
@@ -164,8 +173,10 @@ struct ConvArgs {
   int cin;
   const uint8_t* w_i8;
   const uint8_t* w_fp4;
-  int mfma_fp4;  // 1: fp4 operands, 0: int8
+  const uint8_t* w_f16;
+  int mfma_op;  // MfmaOp: the operand format of the matrix-core kernel
 };
+enum MfmaOp { OP_I8 = 0, OP_FP4 = 1, OP_F16 = 2 };
 int launch_conv_bitplane(const ConvArgs& a, hipStream_t s);
 int launch_conv_mfma(const ConvArgs& a, hipStream_t s);
 bool mfma_supports(const ConvArgs& a);

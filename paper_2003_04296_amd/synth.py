@@ -116,6 +116,14 @@ def workload2(n: int = 256, c: int = 128, hw: int = 32) -> ConvLayerCase:
                      f"1w2a_conv_bn_{n}x{c}x{hw}x{hw}")
 
 
+def workload7(w_bits: int = 1, n: int = 256, c: int = 128, hw: int = 32) -> ConvLayerCase:
+    """16-bit (fp16) inputs with ``w_bits``-bit weights (Table I / Table IV
+    rows with 16-bit floating inputs), the 3x3 layer shape of workload 2 with
+    an fp32 BN epilogue; seed 1007 + w_bits."""
+    return conv_case(1007 + w_bits, n, c, hw, hw, c, 3, 1, 1, 16, w_bits, "normal", "normal", True,
+                     f"a16w{w_bits}_conv_bn_{n}x{c}x{hw}x{hw}")
+
+
 WORKLOAD5_LAYERS = ((64, 56), (128, 28), (256, 14), (512, 7))
 
 

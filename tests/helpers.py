@@ -84,3 +84,27 @@ def weight_copies(words, cout, cin, kh, kw, bits):
     lv4 = np.moveaxis(val, 2, 3).reshape(kh, kw, cop, cwp * 64)[:, :, :cout, :cin]
     to_oihw = lambda a: np.ascontiguousarray(np.transpose(a, (2, 3, 0, 1))).astype(np.int8)
     return to_oihw(lv8), to_oihw(lv4)
+
+
+def weight_copy_f16(words, cout, cin, kh, kw, bits) -> np.ndarray:
+    """Decode the fp16 operand copy (the fourth part of a packed weight
+    buffer, [kh][kw][2 cw][cout_pad][16 halves]) -> int8 levels [cout][cin][kh][kw]."""
+    P = PLANES[bits]
+    cw = (cin + 31) // 32
+    cwp = (cw + 1) // 2
+    cop = (cout + 127) // 128 * 128
+    raw = np.asarray(words).view(np.uint8)
+    off = kh * kw * cw * cop * (P * 4 + 32) + kh * kw * cwp * cop * 32
+    h = raw[off:off + kh * kw * 2 * cw * cop * 32].view(np.float16).reshape(kh, kw, 2 * cw, cop, 16)
+    lv = np.moveaxis(h, 2, 3).reshape(kh, kw, cop, 2 * cw * 16)[:, :, :cout, :cin].astype(np.float64)
+    assert np.all(lv == np.round(lv))
+    return np.ascontiguousarray(np.transpose(lv, (2, 3, 0, 1))).astype(np.int8)
+
+
+def unpack_act16(words, n, c, h, w) -> np.ndarray:
+    """fp16 [n][h][w][cw * 32] (int32 view) -> fp16 [n][c][h][w], and whether
+    the padding channels are +0."""
+    cw = (c + 31) // 32
+    a = np.asarray(words).view(np.float16).reshape(n, h, w, cw * 32)
+    pad_ok = bool(np.all(a[..., c:].view(np.uint16) == 0))
+    return np.ascontiguousarray(np.transpose(a[..., :c], (0, 3, 1, 2))), pad_ok

@@ -56,9 +56,10 @@ def test_inference_op_rejects_other_widths():
     assert q.lib().qconv_inference_op(4, 1, ctypes.byref(op), ctypes.byref(prec)) == q.QCONV_EINVAL
 
 
-@pytest.mark.parametrize("n,c,h,w,bits", [(1, 1, 1, 1, 1), (2, 33, 5, 7, 2), (256, 128, 32, 32, 2), (3, 64, 4, 4, 3)])
+@pytest.mark.parametrize("n,c,h,w,bits", [(1, 1, 1, 1, 1), (2, 33, 5, 7, 2), (256, 128, 32, 32, 2), (3, 64, 4, 4, 3),
+                                         (2, 33, 5, 7, 16), (256, 128, 32, 32, 16)])
 def test_packed_act_size(n, c, h, w, bits):
-    want = n * h * w * ((c + 31) // 32) * {1: 1, 2: 2, 3: 4}[bits] * 4
+    want = n * h * w * ((c + 31) // 32) * {1: 1, 2: 2, 3: 4, 16: 16}[bits] * 4
     assert q.lib().qconv_packed_act_bytes(n, c, h, w, bits) == want
 
 
@@ -68,7 +69,8 @@ def test_packed_weight_size(cout, cin, k, bits):
     planes = k * k * cw * cop * {1: 1, 2: 2, 3: 4}[bits] * 4
     i8 = k * k * cw * cop * 32
     fp4 = k * k * ((cw + 1) // 2) * cop * 32
-    assert q.lib().qconv_packed_weight_bytes(cout, cin, k, k, bits) == planes + i8 + fp4
+    f16 = k * k * 2 * cw * cop * 32
+    assert q.lib().qconv_packed_weight_bytes(cout, cin, k, k, bits) == planes + i8 + fp4 + f16
 
 
 def test_size_queries_reject_bad_input():
@@ -128,6 +130,24 @@ def _fwd(d, e, out=FAKE, out_packed=None):
 def test_forward_rejects_bad_desc(bad):
     e = q.qconv_epilogue(q.EPI_INT32, 0, None, None, None, None, 0, None)
     assert _fwd(_desc(**bad), e) == q.QCONV_EINVAL
+
+
+def test_sixteen_bit_input_rules():
+    """16-bit inputs run on the fp16 matrix cores only, with an fp32 epilogue;
+    the int32 overflow rule does not apply to them."""
+    sc = q.qconv_epilogue(q.EPI_SCALE_F32, 0, FAKE, None, None, None, 0, None)
+    assert q.resolve_algo(2, 128, 32, 32, 128, 3, 1, 1, 16, 1, mode=q.EPI_SCALE_F32) == q.ALGO_MFMA_F16
+    assert q.resolve_algo(2, 128, 32, 32, 128, 3, 1, 1, 16, 3, mode=q.EPI_BN_F32, flags=q.EPI_POOL2) == q.ALGO_MFMA_F16
+    assert q.lib().qconv_resolve_algo(ctypes.byref(_desc(a_bits=16, algo=q.ALGO_MFMA_F16)), ctypes.byref(sc)) == 4
+    for algo in (q.ALGO_BITPLANE, q.ALGO_MFMA_I8, q.ALGO_MFMA_FP4):
+        assert _fwd(_desc(a_bits=16, algo=algo), sc) == q.QCONV_EUNSUPPORTED
+    assert _fwd(_desc(a_bits=2, algo=q.ALGO_MFMA_F16), sc) == q.QCONV_EUNSUPPORTED
+    assert _fwd(_desc(a_bits=16, algo=5), sc) == q.QCONV_EINVAL
+    assert _fwd(_desc(a_bits=8), sc) == q.QCONV_EINVAL
+    e32 = q.qconv_epilogue(q.EPI_INT32, 0, None, None, None, None, 0, None)
+    assert _fwd(_desc(a_bits=16), e32) == q.QCONV_EUNSUPPORTED
+    assert _fwd(_desc(cin=134218000, kh=1, kw=1, pad=0, a_bits=16, w_bits=3), sc) != q.QCONV_EOVERFLOW
+    assert q.kernel_name(2, 128, 32, 32, 128, 3, 1, 1, 16, 1, mode=q.EPI_BN_F32).startswith("conv_mfma_kernel<2, 16, ")
 
 
 def test_forward_rejects_overflowing_k():

@@ -82,6 +82,13 @@ def test_pack_weight_matches_oracle(dev, bits, shape):
     lv8, lv4 = weight_copies(words.cpu().numpy(), cout, cin, kh, kw, bits)
     np.testing.assert_array_equal(lv8, lv)
     np.testing.assert_array_equal(lv4, lv)
+    # ... and 0 in the rows of padding output channels
+    raw = words.cpu().numpy().view(np.uint8)
+    cw = (cin + 31) // 32
+    off = kh * kw * cw * cop * P * 4
+    i8 = raw[off:off + kh * kw * cw * cop * 32].reshape(kh, kw, cw, cop, 32)
+    f4 = raw[off + i8.size:off + i8.size + kh * kw * ((cw + 1) // 2) * cop * 32].reshape(kh, kw, -1, cop, 32)
+    assert np.all(i8[:, :, :, cout:, :] == 0) and np.all(f4[:, :, :, cout:, :] == 0)
 
 
 # ---------------------------------------------------------------------------
