@@ -63,7 +63,13 @@ constexpr int MAX_LDS = 38 * 1024;  // one halo buffer (two per block, two block
 // Packed words of the next stage held per thread in registers (bounded by
 // the registers left next to the accumulators); items past 256 times this
 // are loaded when the stage is expanded.
-__host__ __device__ constexpr int halo_items_per_thread(int words) { return words == 1 ? 4 : words == 16 ? 1 : 8 / words; }
+// fp16 halo words (64 bytes each) are not held across the MFMAs: they are
+// loaded at the end of the stage instead (two per thread in flight), so
+// that no weight-fragment load of the MFMA loop waits behind them (loads of
+// a wave complete in order) and the registers stay free.
+__host__ __device__ constexpr int halo_items_per_thread(int words) {
+  return words == 1 ? 4 : words == 16 ? 0 : 8 / words;
+}
 
 // n / d by a multiply-high, exact whenever n * d < 2^32 (checked on the host
 // against the largest dividend of each use).
@@ -634,9 +640,10 @@ __device__ __forceinline__ void decode_item(const MfmaArgs& m, int w, int wm, in
 // Packed words of this thread's share of a halo tile: item it = tid + 256 u
 // is (halo pixel it / chunk_words, word it % chunk_words).  Pixels outside
 // the image and words past the last channel read as 0 (= Q(0)).
-template <int PA, int NI>
+template <int PA, int NI, int NR>
 __device__ __forceinline__ void load_halo(const MfmaArgs& m, int img0, int iy0, int chunk, int tid,
-                                          uint32_t (&raw)[NI][PA]) {
+                                          uint32_t (&raw)[NR][PA]) {
+  static_assert(NI <= NR, "items past the register array");
   const ConvArgs& a = m.c;
   const int items = m.ipb * m.slot_pix * m.chunk_words;
   const int apix = a.cw * PA;
@@ -680,9 +687,9 @@ __device__ __forceinline__ void load_halo(const MfmaArgs& m, int img0, int iy0, 
 
 // Expands this thread's share of a halo tile into an LDS buffer: the items
 // already held in raw, then any items past NI * 256 loaded here directly.
-template <int OPK, int PA, int NI>
+template <int OPK, int PA, int NI, int NR>
 __device__ __forceinline__ void store_halo(const MfmaArgs& m, int img0, int iy0, int chunk, int tid,
-                                           const uint32_t (&raw)[NI][PA], uint8_t* buf) {
+                                           const uint32_t (&raw)[NR][PA], uint8_t* buf) {
   const int items = m.ipb * m.slot_pix * m.chunk_words;
 #pragma unroll
   for (int u = 0; u < NI; ++u) {
@@ -693,12 +700,19 @@ __device__ __forceinline__ void store_halo(const MfmaArgs& m, int img0, int iy0,
       expand_to_lds<OPK, PA>(raw[u], buf + hp * m.pix_bytes + cwl * OpT<OPK>::WORD_BYTES);
     }
   }
-  for (int it = NI * 256 + tid; it < items; it += 256) {
-    uint32_t one[1][PA];
-    load_halo<PA, 1>(m, img0, iy0, chunk, it, one);
-    const int hp = (int)fdiv((uint32_t)it, m.fd_cwc);
-    const int cwl = it - hp * m.chunk_words;
-    expand_to_lds<OPK, PA>(one[0], buf + hp * m.pix_bytes + cwl * OpT<OPK>::WORD_BYTES);
+  // the rest two at a time: both loads in flight before the first store
+  for (int it = NI * 256 + tid; it < items; it += 512) {
+    uint32_t two[2][PA];
+    load_halo<PA, 2>(m, img0, iy0, chunk, it, two);
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int iu = it + 256 * u;
+      if (iu < items) {
+        const int hp = (int)fdiv((uint32_t)iu, m.fd_cwc);
+        const int cwl = iu - hp * m.chunk_words;
+        expand_to_lds<OPK, PA>(two[u], buf + hp * m.pix_bytes + cwl * OpT<OPK>::WORD_BYTES);
+      }
+    }
   }
 }
 
@@ -729,6 +743,7 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
   constexpr int MT = C::MT, NT = C::NT, WN = C::WN, SK = C::SK;
   constexpr int BCO = 32 * NT * WN;
   constexpr int NI = halo_items_per_thread(PA);  // halo items per thread and stage
+  constexpr int BRING = QC_BRING;
   static_assert(SK == 1 || SK == MT * NT, "a split-K block has one tile per wave");
   extern __shared__ __attribute__((aligned(16))) uint8_t lds_raw[];
   const ConvArgs& a = m.c;
@@ -747,7 +762,7 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
   if (w >= total) return;
   Item<MT> cur;
   decode_item<MT, NT, WN>(m, w, wm, r32, g, &cur);
-  uint32_t raw[NI][PA];
+  uint32_t raw[NI > 0 ? NI : 1][PA];
   load_halo<PA, NI>(m, cur.img0, cur.iy0, 0, tid, raw);
   if constexpr (SWAP) load_params<BCO>(a, cur.co_blk, tid, prm_base);
   store_halo<OPK, PA, NI>(m, cur.img0, cur.iy0, 0, tid, raw, halo_base);
@@ -786,8 +801,9 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
     }
 
     // ---- MFMA over this wave's share of the (tap, k-step) steps of the stage ----
-    // B fragments come from a ring of three register sets, each loaded two
-    // steps before its MFMAs; A fragments are read from LDS one step ahead.
+    // B fragments come from a ring of BRING register sets, each loaded
+    // BRING - 1 steps before its MFMAs; A fragments are read from LDS one
+    // step ahead.
     {
       const uint8_t* lds = halo_base + sbuf * buf_bytes;
       const int co_w = cur.co_blk + 32 * NT * wn;
@@ -844,33 +860,20 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
                 acc[i][j] = mfma<OPK>(Acur[i], bf[j], acc[i][j]);
             }
         };
-#if QC_BRING == 3
-        v4i B0[NT], B1[NT], B2[NT];
-        bload(B0);
-        bload(B1);
+        // ring of BRING register sets: the set of step st + BRING - 1 is
+        // loaded just before the MFMAs of step st
+        v4i Bq[BRING][NT];
+        Unroll<0, BRING - 1>::run([&](auto D) { bload(Bq[decltype(D)::value]); });
         aload(Anext);
-        for (int st = 0; st < nsteps; st += 3) {
-          bload(B2);
-          step(B0);
-          if (st + 1 >= nsteps) break;
-          bload(B0);
-          step(B1);
-          if (st + 2 >= nsteps) break;
-          bload(B1);
-          step(B2);
+        for (int st = 0; st < nsteps; st += BRING) {
+          Unroll<0, BRING>::run([&](auto D) {
+            constexpr int d = decltype(D)::value;
+            if (st + d < nsteps) {
+              bload(Bq[(d + BRING - 1) % BRING]);
+              step(Bq[d]);
+            }
+          });
         }
-#else
-        v4i B0[NT], B1[NT];
-        bload(B0);
-        aload(Anext);
-        for (int st = 0; st < nsteps; st += 2) {
-          bload(B1);
-          step(B0);
-          if (st + 1 >= nsteps) break;
-          bload(B0);
-          step(B1);
-        }
-#endif
       }
     }
 
