@@ -1357,6 +1357,8 @@ __global__ __launch_bounds__(1024, 1) void conv_mfma_pp_kernel(const MfmaArgs m)
   }
 }
 
+int device_cus();
+
 bool plan(const ConvArgs& a, int cfg, MfmaArgs* m) {
   memset(m, 0, sizeof(*m));
   m->c = a;
@@ -1403,8 +1405,16 @@ bool plan(const ConvArgs& a, int cfg, MfmaArgs* m) {
       const size_t slot = (size_t)t.hr * t.hc * t.pix_bytes;
       const int fit = (int)(MAX_LDS / slot);
       t.ipb = min(units_pb / m->upi, fit);
-      t.bpi = 0;
+      if (cfg == 2) {
+        // split-K items of whole images (fully connected layers): no more
+        // images per item than leaves one item per CU, so that every CU
+        // works and the largest channel chunk fits (fewer serial stages)
+        const int64_t per_cu = (int64_t)a.n * ceil_div(a.cout, cfg_block_co(cfg)) / device_cus();
+        if (per_cu < t.ipb) t.ipb = per_cu < 1 ? 1 : (int)per_cu;
+      }
       if (t.ipb < 1) continue;
+      // one image per item is the single-image mode: one block per image
+      t.bpi = t.ipb == 1 ? 1 : 0;
       units = t.ipb * m->upi;
     } else {
       t.ipb = 1;
@@ -1439,6 +1449,7 @@ bool plan(const ConvArgs& a, int cfg, MfmaArgs* m) {
     return false;
   m->tiles_px = (m->ipb == 1) ? a.n * m->bpi : ceil_div(a.n, m->ipb);
   m->tiles_co = ceil_div(a.cout, cfg_block_co(cfg));
+  if (m->tiles_px < 1 || m->tiles_co < 1) return false;  // never an empty launch
   m->halo_bytes = m->slot_pix * m->pix_bytes * m->ipb;
   m->ht_needed = 0;
   if (a.out_packed) {
@@ -1457,9 +1468,13 @@ bool plan(const ConvArgs& a, int cfg, MfmaArgs* m) {
 // LDS bytes of one block: two parameter sets and two halo buffers.
 size_t block_lds(const MfmaArgs& m) { return 2 * PARAM_BYTES + (size_t)m.buf_bytes * 2; }
 
-// Block shape: 64-row split-K blocks when the 256-row shapes would leave the
-// chip under-filled (fewer than two blocks per CU) or their input tile does
-// not fit the staging buffer; otherwise 128 or 64 output channels per block.
+int device_cus();
+
+// Block shape: 64-row split-K blocks when the 256-row shapes would leave
+// compute units without a block (measured on the ConvNet and ResNet-18
+// layers: with one or more 256-row items per CU the unsplit shape is faster,
+// with fewer the split one) or their input tile does not fit the staging
+// buffer; otherwise 128 or 64 output channels per block.
 int pick_cfg(const ConvArgs& a) {
   const int big = a.cout <= 64 ? 1 : 0;
   MfmaArgs m;
@@ -1470,7 +1485,7 @@ int pick_cfg(const ConvArgs& a) {
   }
   const int64_t blocks = (int64_t)m.tiles_px * m.tiles_co;
   const int steps = a.kh * a.kw * m.ksteps;
-  if (blocks < 512 && steps >= 8) {
+  if (blocks < device_cus() && steps >= 8) {
     MfmaArgs s;
     if (plan(a, 2, &s)) return 2;
   }
