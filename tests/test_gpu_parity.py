@@ -385,6 +385,19 @@ def test_pooled_conv_bn_pack_and_residual(dev, case, algo):
                                   oracle.quantize(oracle.hardtanh(zz), 2))
 
 
+@pytest.mark.parametrize("algo", [q.ALGO_MFMA_FP4, q.ALGO_MFMA_I8])
+def test_one_whole_image_per_item(dev, algo):
+    """Images small enough for several per 256-row item (128 output pixels)
+    whose input tile leaves room for only one: each item is one image, one
+    block per image (this plan once produced an empty launch)."""
+    n, cin, h, w, cout, k, s, p = 300, 64, 15, 31, 64, 3, 2, 1
+    assert q.kernel_name(n, cin, h, w, cout, k, s, p, 2, 1, algo=algo).startswith("conv_mfma_kernel<")
+    x, wt = _inputs(31, n, cin, h, w, cout, k)
+    out, _, _ = _gpu_conv(dev, x, wt, 2, 1, s, p, algo=algo)
+    want, _ = _oracle_acc(x, wt, 2, 1, s, p)
+    np.testing.assert_array_equal(out.cpu().numpy(), want)
+
+
 def test_empty_batch_is_a_no_op(dev):
     x = torch.zeros((0, 32, 4, 4), device=dev)
     act = q.pack_act(x, 1)
