@@ -150,7 +150,8 @@ int qconv_fold_bn(const float* gamma, const float* beta, const float* mean, cons
 /* Quantized convolution with fused epilogue (Algorithm 1 + Sec. III-E)      */
 /* ------------------------------------------------------------------------ */
 typedef enum {
-  QCONV_ALGO_AUTO = 0,     /* library choice (matrix cores where supported)   */
+  QCONV_ALGO_AUTO = 0,     /* library choice: fp4 matrix cores where supported,
+                              the bitplane kernel for K = cin*kh*kw <= 256     */
   QCONV_ALGO_BITPLANE = 1, /* VALU XNOR/AND + popcount over bitplanes         */
   QCONV_ALGO_MFMA_I8 = 2,  /* int8 matrix cores on the expanded level codes   */
   QCONV_ALGO_MFMA_FP4 = 3, /* fp4 (E2M1) matrix cores on the same codes        */

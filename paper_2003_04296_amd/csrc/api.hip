@@ -232,7 +232,11 @@ int prepare_conv(const qconv_desc* d, const uint32_t* act_packed, const uint32_t
     if (d->n > 0 && !mfma_supports(a)) return QCONV_EUNSUPPORTED;
     return d->algo;
   }
-  if (d->algo == QCONV_ALGO_AUTO && d->n > 0) {
+  // AUTO: the fp4 matrix cores, except for tiny contractions (K <= 256, the
+  // 1x1 shortcut convolutions of ResNet-18), where staging an input tile in
+  // LDS costs more than the whole bitplane product (measured 18-19 us on the
+  // bitplane kernel against 21-29 us on the matrix cores for those layers)
+  if (d->algo == QCONV_ALGO_AUTO && d->n > 0 && K > 256) {
     a.mfma_op = OP_FP4;
     if (mfma_supports(a)) return QCONV_ALGO_MFMA_FP4;
   }

@@ -112,6 +112,17 @@ def test_pooled_resolution():
     assert q.resolve_algo(1, 128, 8, 4096, 128, 3, 1, 1, 1, 1) == q.ALGO_BITPLANE
 
 
+def test_auto_takes_the_bitplane_kernel_for_tiny_contractions():
+    """AUTO: fp4 matrix cores for K = cin*kh*kw > 256, the bitplane kernel at
+    or below (the ResNet-18 1x1 shortcut convolutions)."""
+    for cin in (64, 128, 256):
+        assert q.resolve_algo(64, cin, 28, 28, 2 * cin, 1, 2, 0, 2, 2, mode=q.EPI_BN_F32) == q.ALGO_BITPLANE
+    assert q.resolve_algo(64, 257, 28, 28, 512, 1, 2, 0, 2, 2, mode=q.EPI_BN_F32) == q.ALGO_MFMA_FP4
+    assert q.resolve_algo(64, 29, 28, 28, 64, 3, 1, 1, 2, 2, mode=q.EPI_BN_F32) == q.ALGO_MFMA_FP4  # K = 261
+    # explicit requests are honoured
+    assert q.resolve_algo(64, 64, 28, 28, 128, 1, 2, 0, 2, 2, algo=q.ALGO_MFMA_FP4) == q.ALGO_MFMA_FP4
+
+
 FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails validation first
 
 
