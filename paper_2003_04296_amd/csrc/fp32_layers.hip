@@ -138,6 +138,49 @@ __global__ __launch_bounds__(256) void maxpool_f32_kernel(const float* __restric
   }
 }
 
+// 3 x 3 / 2 max pooling with padding 1 over rows of even width (the stem of
+// ResNet-18): the lane holding output column ow reads input columns 2ow and
+// 2ow + 1 of each window row as one aligned 8-byte load and takes column
+// 2ow - 1 from the lane holding ow - 1 (the previous lane, in the same output
+// row whenever ow > 0; a wave's first lane loads it itself), so a wave
+// issues three loads per output instead of nine.  The scan order and the
+// compares are those of maxpool_f32_kernel, so the results are identical.
+__global__ __launch_bounds__(256) void maxpool3s2_f32_kernel(const float* __restrict__ x, int64_t planes, int h,
+                                                            int w, int ho, int wo, float* __restrict__ y) {
+  const int pos = blockIdx.x * blockDim.x + threadIdx.x;
+  const bool live = pos < ho * wo;
+  const int p = live ? pos : ho * wo - 1;  // every lane takes part in the exchange
+  const int oh = p / wo, ow = p - (p / wo) * wo;
+  const bool first_lane = (threadIdx.x & 63) == 0;
+  for (int64_t bc = blockIdx.y; bc < planes; bc += gridDim.y) {
+    const float* pl = x + bc * h * w;
+    float2 v[3];
+    float left[3];
+    bool rok[3];
+#pragma unroll
+    for (int dy = 0; dy < 3; ++dy) {
+      const int ih = 2 * oh - 1 + dy;
+      rok[dy] = ih >= 0 && ih < h;
+      const int row = rok[dy] ? ih : 0;
+      v[dy] = *reinterpret_cast<const float2*>(pl + row * w + 2 * ow);
+    }
+#pragma unroll
+    for (int dy = 0; dy < 3; ++dy) {
+      left[dy] = __shfl_up(v[dy].y, 1);
+      if (first_lane && ow > 0) left[dy] = pl[(rok[dy] ? 2 * oh - 1 + dy : 0) * w + 2 * ow - 1];
+    }
+    float m = -INFINITY;
+#pragma unroll
+    for (int dy = 0; dy < 3; ++dy) {
+      if (!rok[dy]) continue;
+      if (ow > 0 && left[dy] > m) m = left[dy];
+      if (v[dy].x > m) m = v[dy].x;
+      if (v[dy].y > m) m = v[dy].y;
+    }
+    if (live) y[bc * ho * wo + pos] = m;
+  }
+}
+
 __global__ __launch_bounds__(256) void avgpool_f32_kernel(const float* __restrict__ x,
                                                           int64_t nc, int hw,
                                                           float* __restrict__ y) {
@@ -298,7 +341,9 @@ int launch_maxpool_f32(const float* x, int n, int c, int h, int w, int k, int st
   if ((int64_t)h * w >= ((int64_t)1 << 31)) return QCONV_EUNSUPPORTED;
   if (planes == 0 || ho < 1 || wo < 1) return QCONV_OK;
   const dim3 grid((unsigned)ceil_div(ho * wo, 256), (unsigned)(planes < 65535 ? planes : 65535));
-  if (k == 3)
+  if (k == 3 && stride == 2 && pad == 1 && w % 2 == 0 && ((uintptr_t)x & 7u) == 0)
+    maxpool3s2_f32_kernel<<<grid, 256, 0, s>>>(x, planes, h, w, ho, wo, y);
+  else if (k == 3)
     maxpool_f32_kernel<3><<<grid, 256, 0, s>>>(x, planes, h, w, k, stride, pad, ho, wo, y);
   else if (k == 2)
     maxpool_f32_kernel<2><<<grid, 256, 0, s>>>(x, planes, h, w, k, stride, pad, ho, wo, y);
