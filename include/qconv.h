@@ -208,9 +208,10 @@ int qconv_out_size(int in, int k, int stride, int pad);
  * QCONV_EUNSUPPORTED, as does QCONV_ALGO_MFMA_F16 for a_bits <= 3), the
  * epilogue runs on the fp32 accumulator (QCONV_EPI_INT32 returns
  * QCONV_EUNSUPPORTED) and the overflow check does not apply.  There is no
- * bitplane fallback for 16-bit inputs: a layer whose input tile does not
- * fit the fp16 staging buffer (80 bytes per pixel per 32 channels; e.g. 2x2
- * pooling after a stride-2 conv over rows of 30 or more pixels) returns
+ * bitplane fallback for 16-bit inputs: input tiles that do not fit the
+ * usual staging buffer are staged in one of up to 76 KB (one block per
+ * compute unit), and a layer whose tile exceeds even that (80 bytes per
+ * pixel per 32 channels; rows of several hundred pixels) returns
  * QCONV_EUNSUPPORTED. */
 int qconv_forward(const qconv_desc* d, const uint32_t* act_packed, const uint32_t* w_packed,
                   const qconv_epilogue* epi, void* out, uint32_t* out_packed, void* stream);

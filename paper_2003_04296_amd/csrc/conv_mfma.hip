@@ -57,6 +57,9 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 
 constexpr int MAX_LDS = 38 * 1024;  // one halo buffer (two per block, two blocks per CU)
+// fp16 operands have no bitplane fallback: input tiles up to twice that size
+// are staged with one block per CU instead
+constexpr int MAX_LDS_WIDE = 76 * 1024;
 #ifndef QC_BRING
 #define QC_BRING 2  // weight-fragment register sets in flight
 #endif
@@ -1392,6 +1395,9 @@ bool plan(const ConvArgs& a, int cfg, MfmaArgs* m) {
   // that more small images fit in one block.
   int best_units = -1;
   MfmaArgs best = *m;
+  for (int wide = 0; wide < 2 && best_units < 0; ++wide) {
+  if (wide && op != OP_F16) break;
+  const size_t lim = wide ? (size_t)MAX_LDS_WIDE : (size_t)MAX_LDS;
   for (int cwc = min(chunk_max, cw_round); cwc >= wpstep; cwc /= 2) {
     if (cwc % wpstep) break;
     MfmaArgs t = *m;
@@ -1403,7 +1409,7 @@ bool plan(const ConvArgs& a, int cfg, MfmaArgs* m) {
     if (m->upi * 2 <= units_pb) {
       t.hr = (conv_rows_img - 1) * a.stride + a.kh;
       const size_t slot = (size_t)t.hr * t.hc * t.pix_bytes;
-      const int fit = (int)(MAX_LDS / slot);
+      const int fit = (int)(lim / slot);
       t.ipb = min(units_pb / m->upi, fit);
       if (cfg == 2) {
         // split-K items of whole images (fully connected layers): no more
@@ -1423,7 +1429,7 @@ bool plan(const ConvArgs& a, int cfg, MfmaArgs* m) {
       const int urows = min(uh, ceil_div(units_pb, m->uw) + 1);
       const int crows = a.pool ? 2 * urows : urows;
       t.hr = (crows - 1) * a.stride + a.kh;
-      if ((size_t)t.hr * t.hc * t.pix_bytes > (size_t)MAX_LDS) continue;
+      if ((size_t)t.hr * t.hc * t.pix_bytes > lim) continue;
       units = units_pb;
     }
     if (units > best_units) {
@@ -1431,6 +1437,7 @@ bool plan(const ConvArgs& a, int cfg, MfmaArgs* m) {
       best = t;
     }
     if (units == units_pb || (m->upi * 2 <= units_pb && t.ipb == units_pb / m->upi)) break;
+  }
   }
   if (best_units < 0) return false;
   *m = best;
@@ -1535,6 +1542,22 @@ bool use_pp(const MfmaArgs& m, int cfg, int cus) {
   return (int64_t)m.tiles_px * m.tiles_co >= 2 * (int64_t)cus;
 }
 
+// Raises the dynamic-LDS limit of one kernel instantiation to `bytes`, once
+// per device and size (the pointer identifies the instantiation).
+template <void (*K)(const MfmaArgs)>
+bool raise_lds_limit_of(size_t bytes) {
+  static std::atomic<int> done[MAX_DEVICES];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return false;
+  std::atomic<int>* d = (dev >= 0 && dev < MAX_DEVICES) ? &done[dev] : nullptr;
+  if (d && d->load(std::memory_order_relaxed) >= (int)bytes) return true;
+  if (hipFuncSetAttribute(reinterpret_cast<const void*>(K), hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes) !=
+      hipSuccess)
+    return false;
+  if (d) d->store((int)bytes, std::memory_order_relaxed);
+  return true;
+}
+
 template <int OPK, int PA, int CFG>
 int launch_cfg(MfmaArgs m, hipStream_t s) {
   const size_t lds = block_lds(m);
@@ -1567,10 +1590,13 @@ int launch_cfg(MfmaArgs m, hipStream_t s) {
     const int per_cu = max(1, min(2, (int)(LDS_PER_CU / lds)));
     m.grid = min(total, per_cu * cus);
   }
-  if (use_swap(m))
+  if (use_swap(m)) {
+    if (lds > 64 * 1024 && !raise_lds_limit_of<conv_mfma_kernel<OPK, PA, CFG, 1>>(lds)) return QCONV_EHIP;
     conv_mfma_kernel<OPK, PA, CFG, 1><<<dim3((unsigned)m.grid), 256, lds, s>>>(m);
-  else
+  } else {
+    if (lds > 64 * 1024 && !raise_lds_limit_of<conv_mfma_kernel<OPK, PA, CFG, 0>>(lds)) return QCONV_EHIP;
     conv_mfma_kernel<OPK, PA, CFG, 0><<<dim3((unsigned)m.grid), 256, lds, s>>>(m);
+  }
   return hip_status();
 }
 

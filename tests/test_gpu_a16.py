@@ -140,9 +140,10 @@ def _dev(t, dev):
 
 
 def _supported(case, w_bits, mode, flags=0, out_bits=0):
-    """Whether the library takes this 16-bit layer; the only refusal is an
-    input tile too large for the fp16 staging buffer (wide rows with
-    pooling after a stride-2 conv), which has no fallback."""
+    """Whether the library takes this 16-bit layer.  Tiles too large for the
+    usual staging buffers use wide ones, so every case here must be taken;
+    the only refusal the library may give is for an input tile beyond those
+    (wide rows with pooling after a stride-2 conv)."""
     n, cin, h, w, cout, k, stride, pad = case
     try:
         algo = q.resolve_algo(n, cin, h, w, cout, k, stride, pad, 16, w_bits, mode, flags, out_bits)
