@@ -13,6 +13,7 @@ the launch stream) and the CPU oracle timed on a bounded sample.
 
 Other workloads: --workload 1w1a | 1w2a (default) | 3w3a-L{0..3} |
 a16w{1,2,3} (fp16 inputs, same layer shape; the step converts fp32 -> fp16) |
+a{1,2,3}w16 (quantized inputs with fp16 weights, same layer shape) |
 aqe | convnet | resnet18 (the last two report images/s).
 """
 from __future__ import annotations
@@ -105,8 +106,11 @@ class ConvWorkload:
         n, c, h, w = self.shape
         a = q.packed_act_words(n, c, h, w, self.case.a_bits) * 4
         taps, cw, cop = self.k * self.k, (c + 31) // 32, (self.cout + 127) // 128 * 128
-        wb = {"bitplane": taps * cw * cop * q.planes(self.case.w_bits) * 4, "mfma_i8": taps * cw * cop * 32,
-              "mfma_fp4": taps * ((cw + 1) // 2) * cop * 32, "mfma_f16": taps * 2 * cw * cop * 32}[used]
+        if used == "bitplane":
+            wb = taps * cw * cop * q.planes(self.case.w_bits) * 4
+        else:
+            wb = {"mfma_i8": taps * cw * cop * 32, "mfma_fp4": taps * ((cw + 1) // 2) * cop * 32,
+                  "mfma_f16": taps * 2 * cw * cop * 32}[used]
         return a + wb + int(np.prod(self.out_shape)) * 4
 
     def pack_bytes(self):
@@ -159,6 +163,11 @@ def cpu_baseline_conv(case, mode, budget_s=12.0):
 
     def run(m):
         t0 = time.perf_counter()
+        if case.w_bits == 16:
+            kk, bb = oracle.bn_fold({key: (v.numpy() if hasattr(v, "numpy") else v) for key, v in case.bn.items()})
+            oracle.qconv16w_layer(oracle.quantize(case.x[:m].numpy(), case.a_bits), oracle.to_f16(case.w.numpy()),
+                                  case.a_bits, case.stride, case.pad, "bn", k=kk, b=bb)
+            return time.perf_counter() - t0
         if case.a_bits == 16:
             lw, _ = oracle.quantize_weights(case.w.numpy(), case.w_bits)
             kk, bb = oracle.bn_fold({key: (v.numpy() if hasattr(v, "numpy") else v) for key, v in case.bn.items()})
@@ -234,13 +243,15 @@ def main():
     out = {"metric": METRIC, "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "higher_is_better": True,
            "scaling": "weak", "vs_baseline": None, "data": "synthetic"}
 
-    if wl in ("1w1a", "1w2a", "a16w1", "a16w2", "a16w3") or wl.startswith("3w3a"):
+    if wl in ("1w1a", "1w2a", "a16w1", "a16w2", "a16w3", "a1w16", "a2w16", "a3w16") or wl.startswith("3w3a"):
         if wl == "1w1a":
             case, mode = synth.workload1(), q.EPI_SCALE_F32
         elif wl == "1w2a":
             case, mode = synth.workload2(), q.EPI_BN_F32
         elif wl.startswith("a16"):
             case, mode = synth.workload7(int(wl[-1])), q.EPI_BN_F32
+        elif wl.endswith("w16"):
+            case, mode = synth.workload8(int(wl[1])), q.EPI_BN_F32
         else:
             case, mode = synth.workload5(int(wl.split("L")[1])), q.EPI_INT32
         W = ConvWorkload(case, dev, mode, algo)
@@ -272,7 +283,7 @@ def main():
         n, c, h, w = W.shape
         out.update({
             "value": round(gops_step, 1), "unit": "GOPS", "ms_per_step": round(dt * 1e3, 4),
-            "dtype": "f16" if case.a_bits == 16 else "int32",
+            "dtype": "f16" if 16 in (case.a_bits, case.w_bits) else "int32",
             "config": {"workload": case.name, "batch": n, "cin": c, "hw": h, "cout": W.cout, "k": W.k,
                        "a_bits": case.a_bits, "w_bits": case.w_bits,
                        "epilogue": {q.EPI_INT32: "int32", q.EPI_SCALE_F32: "scale_f32",

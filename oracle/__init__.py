@@ -519,22 +519,28 @@ def conv16_acc_at(x16, w_levels, idx, stride: int = 1, pad: int = 0) -> np.ndarr
     return out
 
 
-def qconv16_layer(x16, w_levels, w_bits: int, stride: int, pad: int, mode: str, s=None, k=None, b=None,
-                  residual=None, pool: bool = False, out_bits: int = 0, acc=None):
-    """One layer on 16-bit inputs.  The accumulator is the exact product
-    rounded once to fp32; the rest is the fp32 epilogue of the quantized
-    layers (Sec. III-E): 2x2 max pooling of the accumulators, acc * 2^-shift
-    (3-bit weight codes are 4 x level), then
+def conv16w_acc(a_levels, w16, a_bits: int, stride: int = 1, pad: int = 0) -> np.ndarray:
+    """The product of M-bit input level codes and 16-bit weights (Table I
+    rows with 1..3-bit inputs and 16-bit weights), in code units, summed in
+    fp64: padding taps hold Q(0), the level an all-zero packed word encodes
+    (-1 for 1 bit).  Exact on the same grounds as conv16_acc."""
+    a = np.asarray(a_levels, dtype=np.float64)
+    if pad:
+        a = np.pad(a, ((0, 0), (0, 0), (pad, pad), (pad, pad)), constant_values=float(pad_level(a_bits)))
+    return conv_f64(a, np.asarray(w16, dtype=np.float16).astype(np.float64), stride, 0)
+
+
+def f32_acc_epilogue(acc, shift: int, mode: str, s=None, k=None, b=None, residual=None, pool: bool = False,
+                     out_bits: int = 0):
+    """The layer epilogue on an exact product rounded once to fp32 (the
+    16-bit rows): 2x2 max pooling of the accumulators, acc * 2^-shift, then
       mode "scale": s_c * acc_real;  "bn": fmaf(k_c, acc_real, b_c) [+ residual];
     out_bits > 0 also returns Q(HardTanh(z)) with the activation quantizer.
-    ``acc``: conv16_acc(x16, w_levels, stride, pad) when already computed.
     Returns (z, levels or None)."""
-    if acc is None:
-        acc = conv16_acc(x16, w_levels, stride, pad)
     acc = np.asarray(acc, np.float64).astype(np.float32)
     if pool:
         acc = maxpool_f32(acc, 2, 2, 0)
-    a = (acc * np.float32(2.0 ** -level_shift(w_bits))).astype(np.float32)
+    a = (acc * np.float32(2.0 ** -shift)).astype(np.float32)
     if mode == "scale":
         z = (_f32(s)[None, :, None, None] * a).astype(np.float32)
     elif mode == "bn":
@@ -545,3 +551,23 @@ def qconv16_layer(x16, w_levels, w_bits: int, stride: int, pad: int, mode: str, 
         raise ValueError(mode)
     lv = quantize(hardtanh(z), out_bits) if out_bits else None
     return z, lv
+
+
+def qconv16_layer(x16, w_levels, w_bits: int, stride: int, pad: int, mode: str, s=None, k=None, b=None,
+                  residual=None, pool: bool = False, out_bits: int = 0, acc=None):
+    """One layer on 16-bit inputs (Sec. III-E layer constructs): the exact
+    product rounded once to fp32, then f32_acc_epilogue with the weights'
+    code shift (3-bit codes are 4 x level).  ``acc``: conv16_acc(x16,
+    w_levels, stride, pad) when already computed."""
+    if acc is None:
+        acc = conv16_acc(x16, w_levels, stride, pad)
+    return f32_acc_epilogue(acc, level_shift(w_bits), mode, s, k, b, residual, pool, out_bits)
+
+
+def qconv16w_layer(a_levels, w16, a_bits: int, stride: int, pad: int, mode: str, s=None, k=None, b=None,
+                   residual=None, pool: bool = False, out_bits: int = 0, acc=None):
+    """One layer on M-bit inputs with 16-bit weights: conv16w_acc rounded
+    once to fp32, then f32_acc_epilogue with the inputs' code shift."""
+    if acc is None:
+        acc = conv16w_acc(a_levels, w16, a_bits, stride, pad)
+    return f32_acc_epilogue(acc, level_shift(a_bits), mode, s, k, b, residual, pool, out_bits)

@@ -98,7 +98,8 @@ int qconv_pack_act(const float* x, int n, int c, int h, int w, int bits, const f
 }
 
 size_t qconv_packed_weight_bytes(int cout, int cin, int kh, int kw, int bits) {
-  if (cout < 1 || cin < 1 || kh < 1 || kw < 1 || !bits_ok(bits)) return 0;
+  if (cout < 1 || cin < 1 || kh < 1 || kw < 1 || !act_bits_ok(bits)) return 0;
+  if (bits == 16) return wbytes_f16(cout, cin, kh, kw);
   return wbytes_planes(cout, cin, kh, kw, bits) + wbytes_i8(cout, cin, kh, kw) +
          wbytes_fp4(cout, cin, kh, kw) + wbytes_f16(cout, cin, kh, kw);
 }
@@ -106,8 +107,9 @@ size_t qconv_packed_weight_bytes(int cout, int cin, int kh, int kw, int bits) {
 int qconv_pack_weight(const float* w, int cout, int cin, int kh, int kw, int bits,
                       const float* base_thresholds, uint32_t* out_packed, float* out_scale,
                       void* stream) {
-  if (!w || !out_packed || !out_scale || cout < 1 || cin < 1 || kh < 1 || kw < 1 || !bits_ok(bits))
+  if (!w || !out_packed || !out_scale || cout < 1 || cin < 1 || kh < 1 || kw < 1 || !act_bits_ok(bits))
     return QCONV_EINVAL;
+  if (bits == 16) return launch_pack_weight_f16(w, cout, cin, kh, kw, out_packed, out_scale, (hipStream_t)stream);
   float base[3] = {0.0f, 0.0f, 0.0f};
   if (bits == 2) base[0] = base_thresholds ? base_thresholds[0] : kWgtThr2[0];
   if (bits == 3)
@@ -147,20 +149,23 @@ int prepare_conv(const qconv_desc* d, const uint32_t* act_packed, const uint32_t
                  ConvArgs* args) {
   if (!d || !epi) return QCONV_EINVAL;
   if (d->n < 0 || d->cin < 1 || d->h < 1 || d->w < 1 || d->cout < 1 || d->kh < 1 || d->kw < 1 ||
-      d->stride < 1 || d->pad < 0 || !act_bits_ok(d->a_bits) || !bits_ok(d->w_bits))
+      d->stride < 1 || d->pad < 0 || !act_bits_ok(d->a_bits) || !act_bits_ok(d->w_bits))
     return QCONV_EINVAL;
   if (d->algo < QCONV_ALGO_AUTO || d->algo > QCONV_ALGO_MFMA_F16) return QCONV_EINVAL;
-  const bool a16 = d->a_bits == 16;
-  // 16-bit inputs run on the fp16 matrix cores only, and only they do
-  if (a16 ? (d->algo != QCONV_ALGO_AUTO && d->algo != QCONV_ALGO_MFMA_F16) : d->algo == QCONV_ALGO_MFMA_F16)
+  // one side 16-bit (Table I: 16-bit inputs with 1..3-bit weights, or
+  // 1..3-bit inputs with 16-bit weights) runs on the fp16 matrix cores only,
+  // and only such layers do; 16 x 16 is not a row of the tables
+  const bool f16 = d->a_bits == 16 || d->w_bits == 16;
+  if (d->a_bits == 16 && d->w_bits == 16) return QCONV_EUNSUPPORTED;
+  if (f16 ? (d->algo != QCONV_ALGO_AUTO && d->algo != QCONV_ALGO_MFMA_F16) : d->algo == QCONV_ALGO_MFMA_F16)
     return QCONV_EUNSUPPORTED;
   const int ho = qconv_out_size(d->h, d->kh, d->stride, d->pad);
   const int wo = qconv_out_size(d->w, d->kw, d->stride, d->pad);
   if (ho < 1 || wo < 1) return QCONV_EINVAL;
   const int64_t K = (int64_t)d->cin * d->kh * d->kw;
-  if (!a16 && K * max_code(d->a_bits) * max_code(d->w_bits) >= (int64_t)1 << 31) return QCONV_EOVERFLOW;
+  if (!f16 && K * max_code(d->a_bits) * max_code(d->w_bits) >= (int64_t)1 << 31) return QCONV_EOVERFLOW;
   if (epi->mode < QCONV_EPI_INT32 || epi->mode > QCONV_EPI_BN_PACK) return QCONV_EINVAL;
-  if (a16 && epi->mode == QCONV_EPI_INT32) return QCONV_EUNSUPPORTED;  // the accumulator is fp32
+  if (f16 && epi->mode == QCONV_EPI_INT32) return QCONV_EUNSUPPORTED;  // the accumulator is fp32
   if (epi->flags & ~(QCONV_EPI_POOL2 | QCONV_EPI_RESIDUAL)) return QCONV_EINVAL;
   const bool pool = (epi->flags & QCONV_EPI_POOL2) != 0;
   const bool resid = (epi->flags & QCONV_EPI_RESIDUAL) != 0;
@@ -216,13 +221,16 @@ int prepare_conv(const qconv_desc* d, const uint32_t* act_packed, const uint32_t
     if (rc) return rc;
   }
   a.cin = d->cin;
-  {
+  if (d->w_bits == 16) {
+    // the whole buffer is the fp16 operand copy
+    a.w_f16 = reinterpret_cast<const uint8_t*>(w_packed);
+  } else {
     const uint8_t* wb = reinterpret_cast<const uint8_t*>(w_packed);
     a.w_i8 = wb ? wb + wbytes_planes(d->cout, d->cin, d->kh, d->kw, d->w_bits) : nullptr;
     a.w_fp4 = wb ? a.w_i8 + wbytes_i8(d->cout, d->cin, d->kh, d->kw) : nullptr;
     a.w_f16 = wb ? a.w_fp4 + wbytes_fp4(d->cout, d->cin, d->kh, d->kw) : nullptr;
   }
-  if (a16) {
+  if (f16) {
     a.mfma_op = OP_F16;
     if (d->n > 0 && !mfma_supports(a)) return QCONV_EUNSUPPORTED;
     return QCONV_ALGO_MFMA_F16;

@@ -12,7 +12,10 @@
 //   v_mfma_f32_32x32x16_f16           (fp32 accumulate)
 // sums exact products; only the fp32 accumulation rounds.  The halo is
 // staged in LDS as it is stored (64 bytes per 32 channels), with the same
-// fragment addressing (32 bytes per k-step, 16 per lane half).
+// fragment addressing (32 bytes per k-step, 16 per lane half).  The rows
+// with 1..3-bit inputs and 16-bit weights use the same kernel with the roles
+// of the formats swapped: the activation bitplanes are expanded into the
+// fp16 codes of their levels in LDS and the weights are fp16.
 //
 // Work unit.  The block's M dimension is a list of "units": output pixels, or
 // with 2x2 pooling whole pooling windows (the pooled output pixels), each of
@@ -184,14 +187,24 @@ __device__ __forceinline__ float acc_f(const v16f& a, int v) { return a[v]; }
 __device__ __forceinline__ int acc_i(const v16i& a, int v) { return a[v]; }
 __device__ __forceinline__ int acc_i(const v16f& a, int v) { return (int)a[v]; }
 
-// One word of a halo pixel into LDS in operand format OPK (fp16 words are
-// already operands: 64 bytes copied as they are).
+// One word of a halo pixel into LDS in operand format OPK.  fp16: a word of
+// 16-bit inputs is already an operand (64 bytes copied as they are); the
+// bitplanes of 1..3-bit inputs (against 16-bit weights) become the fp16
+// codes of their levels.
 template <int OPK, int PA>
 __device__ __forceinline__ void expand_to_lds(const uint32_t* pl, uint8_t* dst) {
-  if constexpr (OPK == OP_F16) {
+  if constexpr (OPK == OP_F16 && PA == 16) {
 #pragma unroll
     for (int q = 0; q < 4; ++q)
       reinterpret_cast<uint4*>(dst)[q] = make_uint4(pl[4 * q], pl[4 * q + 1], pl[4 * q + 2], pl[4 * q + 3]);
+  } else if constexpr (OPK == OP_F16) {
+    uint32_t o[8], h[16];
+    expand_i8_word<PA>(pl, 0xFFFFFFFFu, o);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) i8_word_to_f16(o[q], &h[2 * q], &h[2 * q + 1]);
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      reinterpret_cast<uint4*>(dst)[q] = make_uint4(h[4 * q], h[4 * q + 1], h[4 * q + 2], h[4 * q + 3]);
   } else if constexpr (OPK == OP_FP4) {
     uint32_t o[4];
     expand_fp4_word<PA>(pl, 0xFFFFFFFFu, o);
@@ -1366,7 +1379,8 @@ bool plan(const ConvArgs& a, int cfg, MfmaArgs* m) {
   memset(m, 0, sizeof(*m));
   m->c = a;
   const int op = a.mfma_op;
-  if ((op == OP_F16) != (a.a_bits == 16)) return false;  // fp16 operands exactly for 16-bit inputs
+  // fp16 operands exactly for 16-bit inputs or 16-bit weights
+  if ((op == OP_F16) != (a.a_bits == 16 || a.w_bits == 16)) return false;
   const int chunk_max = op == OP_FP4 ? OpT<OP_FP4>::CHUNK_WORDS
                                      : (op == OP_F16 ? OpT<OP_F16>::CHUNK_WORDS : OpT<OP_I8>::CHUNK_WORDS);
   const int wpstep = op == OP_FP4 ? 2 : 1;  // words per k-step, rounded up to whole words
@@ -1643,7 +1657,12 @@ int launch_conv_mfma(const ConvArgs& a, hipStream_t s) {
   const int cfg = pick_cfg(a);
   if (!plan(a, cfg, &m)) return QCONV_EUNSUPPORTED;
   const int pa = act_words(a.a_bits);
-  if (a.mfma_op == OP_F16) return launch_fp<OP_F16, 16>(m, cfg, s);
+  if (a.mfma_op == OP_F16) {
+    if (pa == 16) return launch_fp<OP_F16, 16>(m, cfg, s);
+    if (pa == 1) return launch_fp<OP_F16, 1>(m, cfg, s);
+    if (pa == 2) return launch_fp<OP_F16, 2>(m, cfg, s);
+    return launch_fp<OP_F16, 4>(m, cfg, s);
+  }
   if (a.mfma_op == OP_FP4) {
     if (pa == 1) return launch_fp<OP_FP4, 1>(m, cfg, s);
     if (pa == 2) return launch_fp<OP_FP4, 2>(m, cfg, s);

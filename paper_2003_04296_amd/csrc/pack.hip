@@ -54,10 +54,6 @@ __global__ __launch_bounds__(256) void pack_act_kernel(const float* __restrict__
   for (int p = 0; p < P; ++p) dst[p] = word[p];
 }
 
-__device__ __forceinline__ uint32_t f16_bits(float v) {
-  return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v);
-}
-
 __global__ __launch_bounds__(256) void pack_act_f16_kernel(const float* __restrict__ x, int c, int hw, int cwn,
                                                            int64_t total, uint32_t* __restrict__ out) {
   const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -144,11 +140,6 @@ __device__ __forceinline__ uint32_t chan_mask(int remaining) {
   return remaining >= 32 ? 0xFFFFFFFFu : ((1u << remaining) - 1u);
 }
 
-// int8 code byte -> fp16 bits (exact: the codes are 0, +-1, +-2, +-4).
-__device__ __forceinline__ uint32_t code_f16(uint32_t word, int byte) {
-  return f16_bits((float)(int8_t)(word >> (8 * byte)));
-}
-
 // Matrix-core operand copies of packed weights: one thread per
 // (tap, word, output channel) for int8 (32 bytes), per (tap, word pair,
 // output channel) for fp4 (32 bytes = 64 nibbles), per (tap, 16-channel
@@ -182,11 +173,7 @@ __global__ __launch_bounds__(256) void expand_weight_kernel(const uint32_t* __re
     expand_i8_word<P>(pl, valid, o);
     uint32_t hv[8];  // channels 16 half .. 16 half + 15 as fp16 pairs
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint32_t wd = o[4 * half + q];
-      hv[2 * q] = code_f16(wd, 0) | (code_f16(wd, 1) << 16);
-      hv[2 * q + 1] = code_f16(wd, 2) | (code_f16(wd, 3) << 16);
-    }
+    for (int q = 0; q < 4; ++q) i8_word_to_f16(o[4 * half + q], &hv[2 * q], &hv[2 * q + 1]);
     uint4* dst = reinterpret_cast<uint4*>(w_f16 + u * 32);
     dst[0] = make_uint4(hv[0], hv[1], hv[2], hv[3]);
     dst[1] = make_uint4(hv[4], hv[5], hv[6], hv[7]);
@@ -233,6 +220,37 @@ __global__ __launch_bounds__(256) void expand_weight_kernel(const uint32_t* __re
   }
 }
 
+// 16-bit weights (Table I rows with 1..3-bit inputs and 16-bit weights):
+// fp32 OIHW -> fp16 [kh][kw][2 cw][cout_pad][16 halves], the layout of the
+// fp16 operand copy, rounded to nearest even; channels past cin and padding
+// output channels are +0.  One thread per 32-byte record.
+__global__ __launch_bounds__(256) void pack_weight_f16_kernel(const float* __restrict__ w, int cout, int cin,
+                                                              int kh, int kw, int cwn, int cop,
+                                                              uint32_t* __restrict__ out) {
+  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t total = (int64_t)kh * kw * 2 * cwn * cop;
+  if (tid >= total) return;
+  const int co = (int)(tid % cop);
+  const int64_t r = tid / cop;
+  const int ks = (int)(r % (2 * cwn));
+  const int tap = (int)(r / (2 * cwn));
+  const int y = tap / kw, x = tap - (tap / kw) * kw;
+  uint32_t hv[8];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    uint32_t pair = 0u;
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int ci = 16 * ks + 2 * q + e;
+      if (co < cout && ci < cin) pair |= f16_bits(w[(((int64_t)co * cin + ci) * kh + y) * kw + x]) << (16 * e);
+    }
+    hv[q] = pair;
+  }
+  uint4* dst = reinterpret_cast<uint4*>(out + tid * 8);
+  dst[0] = make_uint4(hv[0], hv[1], hv[2], hv[3]);
+  dst[1] = make_uint4(hv[4], hv[5], hv[6], hv[7]);
+}
+
 }  // namespace
 
 int launch_pack_act(const float* x, int n, int c, int h, int w, int bits, Thr t, uint32_t* out,
@@ -256,6 +274,16 @@ int launch_pack_act_f16(const float* x, int n, int c, int h, int w, uint32_t* ou
   const int64_t total = (int64_t)n * cwn * hw;
   if (total == 0) return QCONV_OK;
   pack_act_f16_kernel<<<dim3((unsigned)((total + 255) / 256)), 256, 0, s>>>(x, c, hw, cwn, total, out);
+  return hip_status();
+}
+
+int launch_pack_weight_f16(const float* w, int cout, int cin, int kh, int kw, uint32_t* out, float* scale,
+                           hipStream_t s) {
+  weight_scale_kernel<<<ceil_div(cout, 64), 64, 0, s>>>(w, cout, cin * kh * kw, scale);
+  const int cwn = ceil_div(cin, 32);
+  const int64_t total = (int64_t)kh * kw * 2 * cwn * cout_pad(cout);
+  pack_weight_f16_kernel<<<dim3((unsigned)((total + 255) / 256)), 256, 0, s>>>(w, cout, cin, kh, kw, cwn,
+                                                                                cout_pad(cout), out);
   return hip_status();
 }
 

@@ -120,6 +120,18 @@ __device__ __forceinline__ void expand_fp4_word(const uint32_t* pl, uint32_t val
   }
 }
 
+// fp16 bits of a float, rounded to nearest even.
+__device__ __forceinline__ uint32_t f16_bits(float v) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v);
+}
+
+// fp16 codes of the four int8 codes of `word` as two words (channel 2i in
+// the low half; exact: the codes are 0, +-1, +-2, +-4).
+__device__ __forceinline__ void i8_word_to_f16(uint32_t word, uint32_t* lo, uint32_t* hi) {
+  *lo = f16_bits((float)(int8_t)word) | (f16_bits((float)(int8_t)(word >> 8)) << 16);
+  *hi = f16_bits((float)(int8_t)(word >> 16)) | (f16_bits((float)(int8_t)(word >> 24)) << 16);
+}
+
 // Byte sizes of the four parts of a packed weight buffer.
 inline size_t wbytes_planes(int cout, int cin, int kh, int kw, int bits) {
   return (size_t)kh * kw * ceil_div(cin, 32) * cout_pad(cout) * planes_of(bits) * 4;
@@ -147,6 +159,8 @@ int launch_pack_act(const float* x, int n, int c, int h, int w, int bits, Thr t,
 int launch_pack_act_f16(const float* x, int n, int c, int h, int w, uint32_t* out, hipStream_t s);
 int launch_pack_weight(const float* w, int cout, int cin, int kh, int kw, int bits,
                        const float* base_thr, uint32_t* out, float* scale, hipStream_t s);
+int launch_pack_weight_f16(const float* w, int cout, int cin, int kh, int kw, uint32_t* out, float* scale,
+                           hipStream_t s);
 
 struct ConvArgs {
   const uint32_t* act;
@@ -158,7 +172,7 @@ struct ConvArgs {
   int oh_out, ow_out;     // output size after optional 2x2 pooling
   int kreal;              // cin * kh * kw
   int shift;              // acc_real = acc * 2^-shift
-  int a_bits, w_bits;     // a_bits 16: fp16 activations [n][h][w][cw * 32]
+  int a_bits, w_bits;     // a_bits 16: fp16 activations [n][h][w][cw * 32]; w_bits 16: fp16 weights
   // epilogue
   int mode, pool, residual_on;
   const float* scale;

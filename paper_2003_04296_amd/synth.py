@@ -124,6 +124,14 @@ def workload7(w_bits: int = 1, n: int = 256, c: int = 128, hw: int = 32) -> Conv
                      f"a16w{w_bits}_conv_bn_{n}x{c}x{hw}x{hw}")
 
 
+def workload8(a_bits: int = 2, n: int = 256, c: int = 128, hw: int = 32) -> ConvLayerCase:
+    """``a_bits``-bit inputs with 16-bit (fp16) weights (Table I rows with
+    16-bit weights), the 3x3 layer shape of workload 2 with an fp32 BN
+    epilogue; seed 1010 + a_bits."""
+    return conv_case(1010 + a_bits, n, c, hw, hw, c, 3, 1, 1, a_bits, 16, "normal", "normal", True,
+                     f"a{a_bits}w16_conv_bn_{n}x{c}x{hw}x{hw}")
+
+
 WORKLOAD5_LAYERS = ((64, 56), (128, 28), (256, 14), (512, 7))
 
 

@@ -161,6 +161,22 @@ def test_sixteen_bit_input_rules():
     assert q.kernel_name(2, 128, 32, 32, 128, 3, 1, 1, 16, 1, mode=q.EPI_BN_F32).startswith("conv_mfma_kernel<2, 16, ")
 
 
+def test_sixteen_bit_weight_rules():
+    """Table I's rows with 1..3-bit inputs and 16-bit weights: the packed
+    weight buffer is the fp16 copy alone; the fp16 matrix cores only; 16 x 16
+    is not a row of the tables."""
+    cw, cop = (128 + 31) // 32, 256
+    assert q.lib().qconv_packed_weight_bytes(130, 128, 3, 3, 16) == 9 * 2 * cw * cop * 32
+    sc = q.qconv_epilogue(q.EPI_SCALE_F32, 0, FAKE, None, None, None, 0, None)
+    for ab in (1, 2, 3):
+        assert q.resolve_algo(2, 128, 32, 32, 128, 3, 1, 1, ab, 16, mode=q.EPI_BN_F32) == q.ALGO_MFMA_F16
+        assert _fwd(_desc(a_bits=ab, w_bits=16, algo=q.ALGO_BITPLANE), sc) == q.QCONV_EUNSUPPORTED
+    assert _fwd(_desc(a_bits=16, w_bits=16), sc) == q.QCONV_EUNSUPPORTED
+    e32 = q.qconv_epilogue(q.EPI_INT32, 0, None, None, None, None, 0, None)
+    assert _fwd(_desc(a_bits=2, w_bits=16), e32) == q.QCONV_EUNSUPPORTED
+    assert _fwd(_desc(a_bits=2, w_bits=8), sc) == q.QCONV_EINVAL
+
+
 def test_forward_rejects_overflowing_k():
     e = q.qconv_epilogue(q.EPI_INT32, 0, None, None, None, None, 0, None)
     # K = 134218000 * 1 * 1 with 3-bit codes (max 4*4) exceeds 2^31

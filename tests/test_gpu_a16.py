@@ -328,3 +328,107 @@ def test_api_rules(dev):
     q.conv(e, wq, 0, cin, h, w, cout, k, 1, 1, 16, 2, mode=q.EPI_SCALE_F32, scale=scale,
            out=torch.empty(0, dtype=torch.float32, device=dev))
     torch.cuda.synchronize()
+
+
+# ---------------------------------------------------------------------------
+# 1..3-bit inputs with 16-bit weights (Table I rows M x 16)
+# ---------------------------------------------------------------------------
+
+def _w16_decode(words, cout, cin, kh, kw):
+    """fp16 weights [kh][kw][2 cw][cout_pad][16] -> ([cout][cin][kh][kw], padding all +0)."""
+    cw = (cin + 31) // 32
+    cop = (cout + 127) // 128 * 128
+    h = np.asarray(words).view(np.float16).reshape(kh, kw, 2 * cw, cop, 16)
+    full = np.moveaxis(h, 2, 3).reshape(kh, kw, cop, 2 * cw * 16)
+    pad_ok = bool((full[:, :, cout:, :].view(np.uint16) == 0).all() and (full[:, :, :, cin:].view(np.uint16) == 0).all())
+    return np.ascontiguousarray(np.transpose(full[:, :, :cout, :cin], (2, 3, 0, 1))), pad_ok
+
+
+@pytest.mark.parametrize("shape", [(1, 1, 1, 1), (70, 40, 3, 3), (130, 33, 1, 1), (16, 512, 4, 4)])
+def test_pack_weight_16_is_binary16(dev, shape):
+    cout, cin, kh, kw = shape
+    w = _w(20, cout, cin, kh)
+    words, _ = q.pack_weight(w.to(dev), 16)
+    torch.cuda.synchronize()
+    assert words.numel() * 4 == kh * kw * 2 * ((cin + 31) // 32) * ((cout + 127) // 128 * 128) * 32
+    got, pad_ok = _w16_decode(words.cpu().numpy(), cout, cin, kh, kw)
+    assert pad_ok
+    np.testing.assert_array_equal(got.view(np.uint16), oracle.to_f16(w.numpy()).view(np.uint16))
+
+
+def _layer_w16(dev, x, w16f, a_bits, case, **epi):
+    n, cin, h, ww, cout, k, stride, pad = case
+    act = q.pack_act(x.to(dev), a_bits)
+    wq, _ = q.pack_weight(w16f.to(dev), 16)
+    out, outp = q.conv(act, wq, n, cin, h, ww, cout, k, stride, pad, a_bits, 16, **epi)
+    torch.cuda.synchronize()
+    return out, outp
+
+
+@pytest.mark.parametrize("a_bits", [1, 2, 3])
+@pytest.mark.parametrize("case", CASES)
+def test_w16_integer_weights_bit_exact(dev, case, a_bits):
+    """Integer-valued 16-bit weights: every partial sum is an integer, so the
+    fp32 accumulator is exact and every epilogue matches bit for bit."""
+    n, cin, h, w, cout, k, stride, pad = case
+    x = _x(600 + cin + a_bits, (n, cin, h, w))
+    wi = torch.floor(synth.uniform(synth.generator(601 + cout), (cout, cin, k, k), -4.0, 5.0))
+    la = oracle.quantize(x.numpy(), a_bits)
+    w16 = oracle.to_f16(wi.numpy())
+    A = oracle.conv16w_acc(la, w16, a_bits, stride, pad)
+    kk, bb = _bn(cout + 2, cout)
+    zb, _ = oracle.qconv16w_layer(la, w16, a_bits, stride, pad, "bn", k=kk.numpy(), b=bb.numpy(), acc=A)
+    out, _ = _layer_w16(dev, x, wi, a_bits, case, mode=q.EPI_BN_F32, bn_k=_dev(kk, dev), bn_b=_dev(bb, dev))
+    np.testing.assert_array_equal(out.cpu().numpy(), zb)
+    ho, wo = zb.shape[2], zb.shape[3]
+    for pool in ([False, True] if ho >= 2 and wo >= 2 else [False]):
+        ob = 1 + (cin + a_bits) % 3
+        hp, wp = (ho // 2, wo // 2) if pool else (ho, wo)
+        out, outp = _layer_w16(dev, x, wi, a_bits, case, mode=q.EPI_BN_F32, flags=q.EPI_POOL2 if pool else 0,
+                               bn_k=_dev(kk, dev), bn_b=_dev(bb, dev), out_bits=ob,
+                               out_packed=torch.empty(q.packed_act_words(n, cout, hp, wp, ob), dtype=torch.int32,
+                                                      device=dev))
+        zp, lv = oracle.qconv16w_layer(la, w16, a_bits, stride, pad, "bn", k=kk.numpy(), b=bb.numpy(), pool=pool,
+                                       out_bits=ob, acc=A)
+        np.testing.assert_array_equal(out.cpu().numpy(), zp)
+        np.testing.assert_array_equal(unpack_act(outp.cpu().numpy(), n, cout, hp, wp, ob), lv)
+
+
+@pytest.mark.parametrize("a_bits", [1, 2, 3])
+@pytest.mark.parametrize("case", CASES[::2])
+def test_w16_random_weights_within_the_accumulation_bound(dev, case, a_bits):
+    n, cin, h, w, cout, k, stride, pad = case
+    x = _x(700 + cin + a_bits, (n, cin, h, w))
+    wt = _w(701 + cout, cout, cin, k)
+    la = oracle.quantize(x.numpy(), a_bits)
+    w16 = oracle.to_f16(wt.numpy())
+    kk, bb = _bn(cout + 3, cout)
+    zb, _ = oracle.qconv16w_layer(la, w16, a_bits, stride, pad, "bn", k=kk.numpy(), b=bb.numpy())
+    out, _ = _layer_w16(dev, x, wt, a_bits, case, mode=q.EPI_BN_F32, bn_k=_dev(kk, dev), bn_b=_dev(bb, dev))
+    K = cin * k * k
+    pl = abs(oracle.pad_level(a_bits))
+    ap = np.pad(np.abs(la.astype(np.float64)), ((0, 0), (0, 0), (pad, pad), (pad, pad)), constant_values=float(pl))
+    S = oracle.conv_f64(ap, np.abs(w16.astype(np.float64)), stride, 0)
+    bound = (K * U / (1 - K * U) + U) * S * (np.abs(kk.numpy())[None, :, None, None] *
+                                              2.0 ** -oracle.level_shift(a_bits))
+    _close(out.cpu().numpy(), zb, bound)
+
+
+def test_w16_api_rules(dev):
+    n, cin, h, w, cout, k = 2, 32, 8, 8, 32, 3
+    x = _x(800, (n, cin, h, w))
+    wq, _ = q.pack_weight(_w(801, cout, cin, k).to(dev), 16)
+    act = q.pack_act(x.to(dev), 2)
+    assert q.resolve_algo(n, cin, h, w, cout, k, 1, 1, 2, 16, mode=q.EPI_BN_F32) == q.ALGO_MFMA_F16
+    assert q.kernel_name(n, cin, h, w, cout, k, 1, 1, 2, 16, mode=q.EPI_BN_F32).startswith("conv_mfma_kernel<2, 2,")
+    bad = [
+        lambda: q.conv(act, wq, n, cin, h, w, cout, k, 1, 1, 2, 16, mode=q.EPI_INT32),
+        lambda: q.conv(act, wq, n, cin, h, w, cout, k, 1, 1, 2, 16, mode=q.EPI_SCALE_F32,
+                       scale=torch.ones(cout, device=dev), algo=q.ALGO_MFMA_FP4),
+        lambda: q.conv(q.pack_act(x.to(dev), 16), wq, n, cin, h, w, cout, k, 1, 1, 16, 16, mode=q.EPI_SCALE_F32,
+                       scale=torch.ones(cout, device=dev)),
+    ]
+    for f in bad:
+        with pytest.raises(q.QconvError) as ei:
+            f()
+        assert ei.value.status == q.QCONV_EUNSUPPORTED

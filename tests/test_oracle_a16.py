@@ -156,3 +156,52 @@ def test_layer_epilogue_on_integer_inputs_is_the_quantized_epilogue():
     r = rng.normal(0, 1, z.shape).astype(np.float32)
     z2, _ = oracle.qconv16_layer(x16, w, 3, 1, 1, "bn", k=k, b=b, pool=True, residual=r)
     np.testing.assert_array_equal(z2, oracle.add(z, r))
+
+
+# ---------------------------------------------------------------------------
+# 1..3-bit inputs with 16-bit weights (Table I rows M x 16)
+# ---------------------------------------------------------------------------
+
+def _brute_w16(a, w16, a_bits, stride, pad):
+    """Exact rational sums with padding taps at Q(0) (-1 for 1 bit), by loops."""
+    n, cin, h, wd = a.shape
+    cout, _, kh, kw = w16.shape
+    pl = oracle.pad_level(a_bits)
+    ho, wo = (h + 2 * pad - kh) // stride + 1, (wd + 2 * pad - kw) // stride + 1
+    out = np.empty((n, cout, ho, wo), dtype=object)
+    for b in range(n):
+        for co in range(cout):
+            for oy in range(ho):
+                for ox in range(wo):
+                    acc = Fraction(0)
+                    for ci in range(cin):
+                        for ky in range(kh):
+                            for kx in range(kw):
+                                iy, ix = oy * stride - pad + ky, ox * stride - pad + kx
+                                lv = int(a[b, ci, iy, ix]) if 0 <= iy < h and 0 <= ix < wd else pl
+                                acc += lv * Fraction(float(w16[co, ci, ky, kx]))
+                    out[b, co, oy, ox] = acc
+    return out
+
+
+@pytest.mark.parametrize("a_bits", [1, 2, 3])
+@pytest.mark.parametrize("stride,pad", [(1, 1), (2, 1), (1, 0)])
+def test_conv16w_acc_is_the_exact_sum(a_bits, stride, pad):
+    rng = np.random.default_rng(60 + a_bits + 10 * stride + pad)
+    a = _levels(rng, (2, 5, 6, 7), a_bits)
+    w16 = oracle.to_f16(rng.normal(0, 0.3, (3, 5, 3, 3)).astype(np.float32))
+    w16.reshape(-1)[:3] = np.array([2.0 ** -24, -60000.0, -0.0], np.float16)
+    got = oracle.conv16w_acc(a, w16, a_bits, stride, pad)
+    want = _brute_w16(a, w16, a_bits, stride, pad)
+    assert all(Fraction(float(g)) == v for g, v in zip(got.reshape(-1), want.reshape(-1)))
+
+
+@pytest.mark.parametrize("a_bits", [1, 2, 3])
+def test_integer_weights_reduce_to_the_level_product(a_bits):
+    """Integer-valued 16-bit weights in the code range: the integer product
+    of the quantized path, padding included."""
+    rng = np.random.default_rng(70 + a_bits)
+    a = _levels(rng, (2, 37, 9, 8), a_bits)
+    w = rng.integers(-4, 5, (11, 37, 3, 3)).astype(np.int8)
+    got = oracle.conv16w_acc(a, w.astype(np.float16), a_bits, 1, 1)
+    np.testing.assert_array_equal(got, oracle.conv_levels(a, w, 1, 1, oracle.pad_level(a_bits)).astype(np.float64))
