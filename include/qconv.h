@@ -69,6 +69,14 @@
  * acc * 2^-(2[w_bits==3]).  Only the fp32 accumulation rounds, so results
  * match the exact product within K * 2^-24 * sum|x * code| (in code units),
  * and exactly when every partial sum is an integer below 2^24.
+ *
+ * 16-bit weights (Table I rows with 1..3-bit inputs and 16-bit weights):
+ * w_bits = 16 packs fp32 OIHW weights into IEEE fp16 (round to nearest even)
+ * laid out as the fp16 operand copy above, [kh][kw][2 cw][cout_pad][16 x 2 B],
+ * and that is the whole packed buffer; out_scale still receives mean|W_c|.
+ * The product of the inputs' level codes (padding taps at Q(0)) with the
+ * fp16 weights is summed as for 16-bit inputs; its real value is
+ * acc * 2^-(2[a_bits==3]).
  */
 #ifndef QCONV_H
 #define QCONV_H
@@ -130,13 +138,15 @@ int qconv_pack_act(const float* x, int n, int c, int h, int w, int bits,
                    const float* thresholds, uint32_t* out_packed, void* stream);
 
 /* Bytes of the packed weight buffer: the bitplanes [kh][kw][ceil(cin/32)][cout_pad][P]
- * plus the int8, fp4 and fp16 operand copies described above. */
+ * plus the int8, fp4 and fp16 operand copies described above (bits = 16: the
+ * fp16 weights alone). */
 size_t qconv_packed_weight_bytes(int cout, int cin, int kh, int kw, int bits);
 
 /* Quantize fp32 OIHW weights w[cout][cin][kh][kw] (Eq. 20) and pack them.
  * out_scale[cout] (device) receives s_c = mean |W_c| (double sum over
  * (cin, kh, kw) in storage order, rounded once to float).  base_thresholds
- * (host, NULL = defaults) are multiplied by s_c per channel. */
+ * (host, NULL = defaults) are multiplied by s_c per channel.  bits = 16:
+ * round to fp16 instead (16-bit weights, see above; thresholds ignored). */
 int qconv_pack_weight(const float* w, int cout, int cin, int kh, int kw, int bits,
                       const float* base_thresholds, uint32_t* out_packed, float* out_scale,
                       void* stream);
@@ -155,14 +165,14 @@ typedef enum {
   QCONV_ALGO_BITPLANE = 1, /* VALU XNOR/AND + popcount over bitplanes         */
   QCONV_ALGO_MFMA_I8 = 2,  /* int8 matrix cores on the expanded level codes   */
   QCONV_ALGO_MFMA_FP4 = 3, /* fp4 (E2M1) matrix cores on the same codes        */
-  QCONV_ALGO_MFMA_F16 = 4  /* fp16 matrix cores: the only one for a_bits = 16   */
+  QCONV_ALGO_MFMA_F16 = 4  /* fp16 matrix cores: the only one with a 16-bit side */
 } qconv_algo;
 
 typedef struct {
   int n, cin, h, w;     /* input activations (packed with a_bits)         */
   int cout, kh, kw;     /* weights (packed with w_bits)                   */
   int stride, pad;      /* same stride / padding on both axes             */
-  int a_bits, w_bits;   /* a_bits 1..3 or 16 (fp16 inputs), w_bits 1..3  */
+  int a_bits, w_bits;   /* 1..3 each, or one of them 16 (fp16 side)       */
   int algo;             /* qconv_algo                                     */
 } qconv_desc;
 
@@ -203,9 +213,10 @@ int qconv_out_size(int in, int k, int stride, int pad);
  * staging buffer (at least one input row of 64 output pixels' receptive
  * field); asked for explicitly otherwise they return QCONV_EUNSUPPORTED,
  * and AUTO falls back to the bitplane kernels.  Every algorithm returns the
- * same bits.  a_bits = 16: act_packed is the fp16 tensor above, the
- * algorithm is QCONV_ALGO_MFMA_F16 (AUTO picks it; any other returns
- * QCONV_EUNSUPPORTED, as does QCONV_ALGO_MFMA_F16 for a_bits <= 3), the
+ * same bits.  a_bits = 16 or w_bits = 16 (not both): act_packed is the
+ * fp16 tensor above, resp. w_packed the fp16 weights; the algorithm is
+ * QCONV_ALGO_MFMA_F16 (AUTO picks it; any other returns QCONV_EUNSUPPORTED,
+ * as does QCONV_ALGO_MFMA_F16 for layers with no 16-bit side), the
  * epilogue runs on the fp32 accumulator (QCONV_EPI_INT32 returns
  * QCONV_EUNSUPPORTED) and the overflow check does not apply.  There is no
  * bitplane fallback for 16-bit inputs: input tiles that do not fit the
