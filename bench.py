@@ -14,6 +14,7 @@ the launch stream) and the CPU oracle timed on a bounded sample.
 Other workloads: --workload 1w1a | 1w2a (default) | 3w3a-L{0..3} |
 a16w{1,2,3} (fp16 inputs, same layer shape; the step converts fp32 -> fp16) |
 a{1,2,3}w16 (quantized inputs with fp16 weights, same layer shape) |
+convnet_w16 (ConvNet with 1-bit activations and fp16 weights) |
 aqe | convnet | resnet18 (the last two report images/s).
 """
 from __future__ import annotations
@@ -197,6 +198,9 @@ def cpu_baseline_net(params, wl, budget_s=12.0):
 
     if wl == "convnet":
         forward = oracle.convnet_forward
+    elif wl == "convnet_w16":
+        def forward(p):
+            return oracle.convnet16w_forward(p, 1)
     else:
         def forward(p):
             return oracle.resnet18_forward(p, 2, 2)
@@ -362,12 +366,15 @@ def main():
                                    "kind": "oracle",
                                    "sample": f"forward + backward + update over {m} activations (numpy, one thread), "
                                              f"{tc:.2f} s"}
-    elif wl in ("convnet", "resnet18"):
+    elif wl in ("convnet", "convnet_w16", "resnet18"):
         from paper_2003_04296_amd.nets import build_convnet, build_resnet18
 
         if wl == "convnet":
             params = synth.convnet_params(seed=1003, batch=256)
             net = build_convnet(params, dev)
+        elif wl == "convnet_w16":
+            params = synth.convnet_params(seed=1003, batch=256)
+            net = build_convnet(params, dev, a_bits=1, w_bits=16)
         else:
             params = synth.resnet18_params(seed=1004, batch=64)
             net = build_resnet18(params, dev)
@@ -382,8 +389,9 @@ def main():
         torch.cuda.synchronize()
         dt = (time.perf_counter() - t0) / args.steps
         out.update({"value": round(x.shape[0] / dt, 1), "unit": "images/s", "ms_per_step": round(dt * 1e3, 4),
-                    "dtype": "int32", "roofline": None,
-                    "config": {"workload": wl + ("_1w1a_batch256_32x32" if wl == "convnet" else "_2w2a_batch64_224x224"),
+                    "dtype": "f16" if wl == "convnet_w16" else "int32", "roofline": None,
+                    "config": {"workload": wl + {"convnet": "_1w1a_batch256_32x32", "convnet_w16": "_1a16w_batch256_32x32",
+                                                 "resnet18": "_2w2a_batch64_224x224"}[wl],
                                "batch": int(x.shape[0])}})
         if not args.no_cpu:
             out["cpu_baseline"] = cpu_baseline_net(params, wl)

@@ -300,7 +300,8 @@ int qnet_add_maxpool_f32(qnet* net, int src, int k, int stride, int pad);
 /* Quantize + pack an fp32 tensor with the default activation thresholds. */
 int qnet_add_quantize(qnet* net, int src, int bits);
 
-/* Quantized conv on a packed tensor with a BN epilogue:
+/* Quantized conv on a packed tensor with a BN epilogue (w_bits 1..3, or 16
+ * for fp16 weights packed by qconv_pack_weight with bits = 16):
  * pool2 != 0 -> 2x2 max pool of the accumulators first;
  * out_bits 1..3 -> packed Q(HardTanh(BN)) output; out_bits 0 -> fp32 BN
  * output, plus the fp32 tensor residual_src when residual_src > 0. */

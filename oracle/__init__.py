@@ -434,6 +434,40 @@ def convnet_forward(p: dict, return_levels: bool = False):
     return (logits, levels) if return_levels else logits
 
 
+def convnet16w_forward(p: dict, a_bits: int = 1, return_levels: bool = False):
+    """ConvNet (Model A family) with 16-bit weights and a_bits-bit
+    activations inside (Table I rows M x 16): fp32 first conv -> BN ->
+    Q(HardTanh); each hidden layer: the product of the input levels with the
+    fp16 weights (exact, rounded once to fp32) -> [2x2 max pool] -> BN ->
+    Q(HardTanh) (the last FC quantizes with 1 bit); fp32 last FC."""
+    def fold(bn):
+        return bn_fold({kk: _np(v) if kk != "eps" else v for kk, v in bn.items()})
+
+    x = _np(p["x"])
+    levels = []
+    c1 = p["convs"][0]
+    k, b = fold(c1["bn"])
+    a = quantize(hardtanh(bn_f32(conv_f32(x, _np(c1["w"]), 1, 1), k, b)), a_bits)
+    levels.append(a)
+    for i, layer in enumerate(p["convs"][1:], start=1):
+        k, b = fold(layer["bn"])
+        _, a = qconv16w_layer(a, to_f16(_np(layer["w"])), a_bits, 1, 1, "bn", k=k, b=b, pool=p["pools"][i],
+                              out_bits=a_bits)
+        levels.append(a)
+    n = a.shape[0]
+    for j, fc in enumerate(p["fcs"]):
+        w = _np(fc["w"])
+        a4 = a.reshape(n, -1, 1, 1) if a.ndim == 2 else a
+        w4 = w.reshape(w.shape[0], a4.shape[1], a4.shape[2], a4.shape[3])
+        k, b = fold(fc["bn"])
+        ob = 1 if j == len(p["fcs"]) - 1 else a_bits
+        _, a = qconv16w_layer(a4, to_f16(w4), a_bits, 1, 0, "bn", k=k, b=b, out_bits=ob)
+        a = a.reshape(n, -1)
+        levels.append(a)
+    logits = fc_f32(a.astype(np.float32), _np(p["fc_out"]["w"]), _np(p["fc_out"]["b"]))
+    return (logits, levels) if return_levels else logits
+
+
 def resnet18_forward(p: dict, a_bits: int = 2, w_bits: int = 2, return_acts: bool = False):
     """ResNet-18 with quantized 3x3/1x1 convs, fp32 stem and FC.
 

@@ -455,7 +455,7 @@ int qnet_add_qconv(qnet* net, int src, const uint32_t* w_packed, int cout, int k
                    int pad, int w_bits, int pool2, const float* bn_k, const float* bn_b,
                    int residual_src, int out_bits) {
   if (!valid_src(net, src) || !w_packed || !bn_k || !bn_b || cout < 1 || k < 1 || stride < 1 ||
-      pad < 0 || !bits_ok(w_bits) || out_bits < 0 || out_bits > 3)
+      pad < 0 || !(bits_ok(w_bits) || w_bits == 16) || out_bits < 0 || out_bits > 3)
     return QCONV_EINVAL;
   const QTensor s = net->t[src];
   if (s.bits == 0) return QCONV_EINVAL;
@@ -466,7 +466,8 @@ int qnet_add_qconv(qnet* net, int src, const uint32_t* w_packed, int cout, int k
     ho /= 2;
     wo /= 2;
   }
-  if ((int64_t)s.c * k * k * max_code(s.bits) * max_code(w_bits) >= (int64_t)1 << 31)
+  // 16-bit weights accumulate in fp32: no int32 bound
+  if (w_bits != 16 && (int64_t)s.c * k * k * max_code(s.bits) * max_code(w_bits) >= (int64_t)1 << 31)
     return QCONV_EOVERFLOW;
   if (residual_src > 0) {
     if (!valid_src(net, residual_src) || out_bits != 0) return QCONV_EINVAL;

@@ -432,3 +432,28 @@ def test_w16_api_rules(dev):
         with pytest.raises(q.QconvError) as ei:
             f()
         assert ei.value.status == q.QCONV_EUNSUPPORTED
+
+
+@pytest.mark.parametrize("a_bits", [1, 2, 3])
+def test_convnet_with_16_bit_weights(dev, a_bits):
+    """ConvNet (Model A widths), batch 2, 16-bit weights in every quantized
+    layer (Table I rows M x 16).  The hidden layers' weights are integer
+    valued, so every partial sum is an exact integer and every layer's levels
+    and the logits must equal the oracle's bit for bit."""
+    from paper_2003_04296_amd.nets import build_convnet
+
+    p = synth.convnet_params(seed=1013, batch=2)
+    g = synth.generator(1014)
+    for layer in p["convs"][1:] + p["fcs"]:
+        layer["w"] = torch.floor(synth.uniform(g, tuple(layer["w"].shape), -2.0, 3.0))
+    net = build_convnet(p, dev, a_bits=a_bits, w_bits=16)
+    logits = net.forward(p["x"].to(dev))
+    torch.cuda.synchronize()
+    want, levels = oracle.convnet16w_forward(p, a_bits, return_levels=True)
+    names = ["conv1", "conv2", "conv3", "conv4", "conv5", "conv6", "fc1", "fc2"]
+    for name, lv in zip(names, levels):
+        words, bits = net.tensor(net.ids[name], 2)
+        shape = lv.shape if lv.ndim == 4 else (lv.shape[0], lv.shape[1], 1, 1)
+        got = unpack_act(words.cpu().numpy(), *shape, bits).reshape(lv.shape)
+        np.testing.assert_array_equal(got, lv, err_msg=name)
+    np.testing.assert_array_equal(logits.cpu().numpy(), want)
