@@ -1491,11 +1491,12 @@ size_t block_lds(const MfmaArgs& m) { return 2 * PARAM_BYTES + (size_t)m.buf_byt
 
 int device_cus();
 
-// Block shape: 64-row split-K blocks when the 256-row shapes would leave
-// compute units without a block (measured on the ConvNet and ResNet-18
-// layers: with one or more 256-row items per CU the unsplit shape is faster,
-// with fewer the split one) or their input tile does not fit the staging
-// buffer; otherwise 128 or 64 output channels per block.
+// Block shape: 256 rows x 128 (or 64) output channels; when those leave
+// compute units without a block, 256 x 64 if that gives every CU one, else
+// 64-row split-K blocks (measured on the ConvNet and ResNet-18 layers: with
+// one or more 256-row items per CU the unsplit shapes are faster, with fewer
+// the split one); split-K too when the 256-row input tile does not fit the
+// staging buffer.
 int pick_cfg(const ConvArgs& a) {
   const int big = a.cout <= 64 ? 1 : 0;
   MfmaArgs m;
@@ -1507,6 +1508,11 @@ int pick_cfg(const ConvArgs& a) {
   const int64_t blocks = (int64_t)m.tiles_px * m.tiles_co;
   const int steps = a.kh * a.kw * m.ksteps;
   if (blocks < device_cus() && steps >= 8) {
+    // 64-channel blocks double the block count; when that gives every CU a
+    // block they beat the split-K shape (ResNet-18 3x3 layers: 512 ch at
+    // 7x7, batch 256, 59 -> 43 us; 256 ch at 14x14, batch 64, 22 -> 18 us)
+    MfmaArgs h;
+    if (big == 0 && plan(a, 1, &h) && (int64_t)h.tiles_px * h.tiles_co >= device_cus()) return 1;
     MfmaArgs s;
     if (plan(a, 2, &s)) return 2;
   }

@@ -227,6 +227,43 @@ def test_bn_residual_and_repack(dev, bits, algo, hw):
 
 
 # ---------------------------------------------------------------------------
+# 256-row x 64-channel blocks on layers whose 128-channel blocks would leave
+# compute units idle while the 64-channel ones give every CU one
+# ---------------------------------------------------------------------------
+
+HALF_CASES = [
+    # n, cin, h, w, cout
+    (32, 70, 14, 14, 500),  # one 196-pixel image per item, ragged cin and cout
+    (130, 64, 7, 7, 640),   # five whole 7x7 images per item, ragged last item
+]
+
+
+@pytest.mark.parametrize("bits", [(2, 2), (3, 3), (1, 1)])
+@pytest.mark.parametrize("case", HALF_CASES)
+def test_half_width_blocks(dev, bits, case):
+    ab, wb = bits
+    n, cin, h, w, cout = case
+    name = q.kernel_name(n, cin, h, w, cout, 3, 1, 1, ab, wb)
+    assert name.startswith("conv_mfma_kernel<") and name.split(", ")[2] == "1", name
+    x, wt = _inputs(31, n, cin, h, w, cout, 3)
+    k, b = _bn(31, cout)
+    act = q.pack_act(x.to(dev), ab)
+    wq, _ = q.pack_weight(wt.to(dev), wb)
+    acc, _ = q.conv(act, wq, n, cin, h, w, cout, 3, 1, 1, ab, wb)
+    outp = torch.empty(q.packed_act_words(n, cout, h, w, ab), dtype=torch.int32, device=dev)
+    z, _ = q.conv(act, wq, n, cin, h, w, cout, 3, 1, 1, ab, wb, mode=q.EPI_BN_F32, bn_k=k.to(dev),
+                  bn_b=b.to(dev), out_bits=ab, out_packed=outp)
+    torch.cuda.synchronize()
+    want, _ = _oracle_acc(x, wt, ab, wb, 1, 1)
+    np.testing.assert_array_equal(acc.cpu().numpy(), want)
+    shift = oracle.level_shift(ab) + oracle.level_shift(wb)
+    zz = oracle.epi_bn(want, k.numpy(), b.numpy(), shift)
+    np.testing.assert_array_equal(z.cpu().numpy(), zz)
+    np.testing.assert_array_equal(unpack_act(outp.cpu().numpy(), n, cout, h, w, ab),
+                                  oracle.quantize(oracle.hardtanh(zz), ab))
+
+
+# ---------------------------------------------------------------------------
 # the store-overlapped kernel: two wave groups per block alternate between
 # the MFMAs of one item and the stores of the previous one; chosen for
 # unpacked, unpooled outputs with at least two items per compute unit
