@@ -456,10 +456,18 @@ __device__ __forceinline__ void swap_res_load(const MfmaArgs& m, int img0, int u
 // is a scalar.  Lanes whose unit does not exist get an offset past the end
 // of the buffer, so their stores and residual loads are dropped.  The
 // block's per-channel parameters come from LDS.
-template <int KIND, int RES = 2, class AccT>
+// OB > 0: the packed planes of Q(HardTanh(z)) (Eqs. 4, 21, 22) as well (KIND
+// K_PACK: only those).  A lane holds 16 of the 32 channels of its unit, so
+// it sets its 16 bits of each plane word with the quantizer's compares, and
+// one exchange with lane l ^ 32 completes the word, which lanes 0-31 store.
+template <int KIND, int RES = 2, int OB = 0, class AccT>
 __device__ __forceinline__ void tile_epilogue_swap(const MfmaArgs& m, const AccT& acc, int img0, int u0,
                                                    int T, int co32, int co_blk, const float* prm,
                                                    int lane, const float (*pre)[16] = nullptr) {
+  constexpr int POUT = OB ? planes_of(OB) : 1;
+  uint32_t pw[POUT];
+#pragma unroll
+  for (int p = 0; p < POUT; ++p) pw[p] = 0u;
   const ConvArgs& a = m.c;
   const int g = lane >> 5, r32 = lane & 31;
   const float inv = 1.0f / (float)(1 << a.shift);
@@ -495,19 +503,75 @@ __device__ __forceinline__ void tile_epilogue_swap(const MfmaArgs& m, const AccT
     for (int i = 0; i < 4; ++i) {
       const int so = (8 * q + i) * pstride;
       uint32_t bits;
+      float z = 0.0f;
       if constexpr (KIND == K_INT32) {
         bits = (uint32_t)acc_i(acc, 4 * q + i);
       } else {
-        float z = acc_f(acc, 4 * q + i) * inv;
+        z = acc_f(acc, 4 * q + i) * inv;
         if constexpr (KIND == K_SCALE) z = kv[i] * z;
+        if constexpr (KIND == K_BNF32 || KIND == K_PACK) z = fmaf(kv[i], z, bv[i]);
         if constexpr (KIND == K_BNF32) {
-          z = fmaf(kv[i], z, bv[i]);
           if (res) z = z + rv[4 * q + i];
         }
         bits = __float_as_uint(z);
       }
-      if (full || cbase + 8 * q + i < a.cout) __builtin_amdgcn_raw_buffer_store_b32(bits, orsrc, voff, so, 0);
+      const bool cok = full || cbase + 8 * q + i < a.cout;
+      if constexpr (KIND != K_PACK) {
+        if (cok) __builtin_amdgcn_raw_buffer_store_b32(bits, orsrc, voff, so, 0);
+      }
+      if constexpr (OB > 0) {
+        const float zz = m.ht_needed ? hardtanh(z) : z;
+        const int b = 8 * q + 4 * g + i;  // bit of channel co32 + b
+        const uint32_t s = (cok & (zz > 0.0f)) ? 1u : 0u;
+        if constexpr (OB == 1) {
+          pw[0] |= s << b;
+        } else if constexpr (OB == 2) {
+          const uint32_t nz = (cok & !(fabsf(zz) <= a.othr.t0)) ? 1u : 0u;
+          pw[0] |= (s & nz) << b;
+          pw[1] |= nz << b;
+        } else {
+          const float az = fabsf(zz);
+          const uint32_t a1 = (cok & !(az <= a.othr.t0)) ? 1u : 0u;
+          const uint32_t a2 = (cok & !(az <= a.othr.t1)) ? 1u : 0u;
+          const uint32_t a3 = (cok & !(az <= a.othr.t2)) ? 1u : 0u;
+          pw[0] |= (s & a1) << b;
+          pw[1] |= a3 << b;
+          pw[2] |= (a2 & ~a3) << b;
+          pw[3] |= (a1 & ~a2) << b;
+        }
+      }
     }
+  }
+  if constexpr (OB > 0) {
+#pragma unroll
+    for (int p = 0; p < POUT; ++p) pw[p] |= (uint32_t)__shfl_xor((int)pw[p], 32);
+    if (g == 0 && uok) {
+      uint32_t* dst = a.out_packed + (((int64_t)img * m.upi + uu) * a.out_cw + (co32 >> 5)) * POUT;
+      store_words<POUT>(dst, pw);
+    }
+  }
+}
+
+// The swapped tile epilogue for the layer's output mode.
+template <class AccT>
+__device__ __forceinline__ void tile_epilogue_swap_mode(const MfmaArgs& m, const AccT& acc, int img0, int u0,
+                                                        int T, int co32, int co_blk, const float* prm,
+                                                        int lane) {
+  const ConvArgs& a = m.c;
+  const int ob = a.out_packed ? a.out_bits : 0;
+  if (a.mode == QCONV_EPI_INT32) {
+    tile_epilogue_swap<K_INT32>(m, acc, img0, u0, T, co32, co_blk, prm, lane);
+  } else if (a.mode == QCONV_EPI_SCALE_F32) {
+    tile_epilogue_swap<K_SCALE>(m, acc, img0, u0, T, co32, co_blk, prm, lane);
+  } else if (a.mode == QCONV_EPI_BN_F32) {
+    if (ob == 0) tile_epilogue_swap<K_BNF32, 2, 0>(m, acc, img0, u0, T, co32, co_blk, prm, lane);
+    else if (ob == 1) tile_epilogue_swap<K_BNF32, 2, 1>(m, acc, img0, u0, T, co32, co_blk, prm, lane);
+    else if (ob == 2) tile_epilogue_swap<K_BNF32, 2, 2>(m, acc, img0, u0, T, co32, co_blk, prm, lane);
+    else tile_epilogue_swap<K_BNF32, 2, 3>(m, acc, img0, u0, T, co32, co_blk, prm, lane);
+  } else {
+    if (ob == 1) tile_epilogue_swap<K_PACK, 0, 1>(m, acc, img0, u0, T, co32, co_blk, prm, lane);
+    else if (ob == 2) tile_epilogue_swap<K_PACK, 0, 2>(m, acc, img0, u0, T, co32, co_blk, prm, lane);
+    else tile_epilogue_swap<K_PACK, 0, 3>(m, acc, img0, u0, T, co32, co_blk, prm, lane);
   }
 }
 
@@ -740,7 +804,7 @@ __device__ __forceinline__ void load_params(const ConvArgs& a, int co_blk, int t
     const int cs = min(co_blk + c, a.cout - 1);
     float v = 0.0f;
     if (a.mode == QCONV_EPI_SCALE_F32) v = half ? 0.0f : a.scale[cs];
-    else if (a.mode == QCONV_EPI_BN_F32) v = half ? a.bn_b[cs] : a.bn_k[cs];
+    else if (a.mode == QCONV_EPI_BN_F32 || a.mode == QCONV_EPI_BN_PACK) v = half ? a.bn_b[cs] : a.bn_k[cs];
     prm[half * 128 + c] = v;
   }
 }
@@ -943,12 +1007,7 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
         const int co32 = co_w + 32 * tj;
         if (co32 < a.cout) {
           if constexpr (SWAP) {
-            if (a.mode == QCONV_EPI_INT32)
-              tile_epilogue_swap<K_INT32>(m, sum, cur.img0, cur.u0, ti, co32, cur.co_blk, prm, lane);
-            else if (a.mode == QCONV_EPI_SCALE_F32)
-              tile_epilogue_swap<K_SCALE>(m, sum, cur.img0, cur.u0, ti, co32, cur.co_blk, prm, lane);
-            else
-              tile_epilogue_swap<K_BNF32>(m, sum, cur.img0, cur.u0, ti, co32, cur.co_blk, prm, lane);
+            tile_epilogue_swap_mode(m, sum, cur.img0, cur.u0, ti, co32, cur.co_blk, prm, lane);
           } else {
             acc_t one[1][1] = {{sum}};
             if (m.pool)
@@ -974,12 +1033,7 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
 #undef QC_PICK
               default: break;
             }
-            if (a.mode == QCONV_EPI_INT32)
-              tile_epilogue_swap<K_INT32>(m, tcur, cur.img0, cur.u0, wm * MT + i, co32, cur.co_blk, prm, lane);
-            else if (a.mode == QCONV_EPI_SCALE_F32)
-              tile_epilogue_swap<K_SCALE>(m, tcur, cur.img0, cur.u0, wm * MT + i, co32, cur.co_blk, prm, lane);
-            else
-              tile_epilogue_swap<K_BNF32>(m, tcur, cur.img0, cur.u0, wm * MT + i, co32, cur.co_blk, prm, lane);
+            tile_epilogue_swap_mode(m, tcur, cur.img0, cur.u0, wm * MT + i, co32, cur.co_blk, prm, lane);
           }
         } else {
           if (m.pool)
@@ -1523,7 +1577,7 @@ int pick_cfg(const ConvArgs& a) {
 // fits a buffer resource.
 bool use_swap(const MfmaArgs& m) {
   const ConvArgs& a = m.c;
-  return !a.pool && a.out_packed == nullptr && a.mode != QCONV_EPI_BN_PACK && m.out_bytes > 0;
+  return !a.pool && m.out_bytes > 0;
 }
 
 constexpr int LDS_PER_CU = 160 * 1024;
@@ -1558,6 +1612,7 @@ size_t pp_lds(const MfmaArgs& m, int cfg) {
 // buffers, when every block gets at least one item per group.
 bool use_pp(const MfmaArgs& m, int cfg, int cus) {
   if (cfg == 2 || m.c.mfma_op == OP_F16 || !use_swap(m) || m.nchunks != 1 || m.act_bytes == 0) return false;
+  if (m.c.out_packed != nullptr || m.c.mode == QCONV_EPI_BN_PACK) return false;  // unpacked outputs only
   if (pp_lds(m, cfg) > (size_t)LDS_PER_CU) return false;
   return (int64_t)m.tiles_px * m.tiles_co >= 2 * (int64_t)cus;
 }
