@@ -827,7 +827,17 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
   static_assert(SK == 1 || SK == MT * NT, "a split-K block has one tile per wave");
   extern __shared__ __attribute__((aligned(16))) uint8_t lds_raw[];
   const ConvArgs& a = m.c;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // wave-uniform indices in scalar registers; per-lane indices are derived
+  // afresh from fresh_tid() wherever a loop iteration needs them, so that
+  // nothing computed from them stays live across the item loop (held there,
+  // such values were spilled to scratch, and every reload waited for all
+  // stores in flight: loads and stores share one in-order counter)
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  auto fresh_tid = [&]() __attribute__((always_inline)) {
+    int t = tid;
+    asm volatile("" : "+v"(t));
+    return t;
+  };
   const int wk = wave % SK;  // K-split index
   const int wmn = wave / SK;
   const int wm = wmn / WN, wn = wmn - (wmn / WN) * WN;
@@ -877,7 +887,7 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
     int nimg0 = cur.img0, niy0 = cur.iy0;
     if (has_next) {
       if (nchunk == 0) item_origin(m, nw, &nimg0, &niy0);
-      load_halo<PA, NI>(m, nimg0, niy0, nchunk, tid, raw);
+      load_halo<PA, NI>(m, nimg0, niy0, nchunk, fresh_tid(), raw);
     }
 
     // ---- MFMA over this wave's share of the (tap, k-step) steps of the stage ----
@@ -887,9 +897,10 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
     {
       const uint8_t* lds = halo_base + sbuf * buf_bytes;
       const int co_w = cur.co_blk + 32 * NT * wn;
+      const int bt = fresh_tid();
       int bvoff[NT];
 #pragma unroll
-      for (int j = 0; j < NT; ++j) bvoff[j] = (co_w + 32 * j + r32) * 32 + g * 16;
+      for (int j = 0; j < NT; ++j) bvoff[j] = (co_w + 32 * j + (bt & 31)) * 32 + ((bt >> 5) & 1) * 16;
       const int ks0 = chunk * steps_per_chunk;
       const int spc = min(m.ksteps, ks0 + steps_per_chunk) - ks0;  // k-steps per tap in this chunk
       const int nsteps_all = taps * spc;
@@ -960,10 +971,11 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
     // ---- the next stage's halo into the other buffer (the epilogue below
     // reads no halo buffer; a split-K block never has a next stage) ----
     if (has_next)
-      store_halo<OPK, PA, NI>(m, nimg0, niy0, nchunk, tid, raw, halo_base + (sbuf ^ 1) * buf_bytes);
+      store_halo<OPK, PA, NI>(m, nimg0, niy0, nchunk, fresh_tid(), raw, halo_base + (sbuf ^ 1) * buf_bytes);
 
     // ---- epilogue of a finished item ----
     if (chunk == m.nchunks - 1) {
+      const int elane = fresh_tid() & 63;
       const float* prm = prm_base + ipar * (PARAM_BYTES / 4);
       const int co_w = cur.co_blk + 32 * NT * wn;
       if constexpr (SK > 1) {
@@ -982,7 +994,7 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
               t.y = acc_f(acc[i][j], 4 * v4 + 1);
               t.z = acc_f(acc[i][j], 4 * v4 + 2);
               t.w = acc_f(acc[i][j], 4 * v4 + 3);
-              red[((wave * (MT * NT) + i * NT + j) * 4 + v4) * 64 + lane] = t;
+              red[((wave * (MT * NT) + i * NT + j) * 4 + v4) * 64 + elane] = t;
             }
         __syncthreads();
         const int tile = wave;  // this wave's tile after the reduction
@@ -992,7 +1004,7 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
           float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
 #pragma unroll
           for (int ww = 0; ww < SK; ++ww) {
-            const float4 t = red[((ww * (MT * NT) + tile) * 4 + v4) * 64 + lane];
+            const float4 t = red[((ww * (MT * NT) + tile) * 4 + v4) * 64 + elane];
             s0 += t.x;
             s1 += t.y;
             s2 += t.z;
@@ -1007,13 +1019,13 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
         const int co32 = co_w + 32 * tj;
         if (co32 < a.cout) {
           if constexpr (SWAP) {
-            tile_epilogue_swap_mode(m, sum, cur.img0, cur.u0, ti, co32, cur.co_blk, prm, lane);
+            tile_epilogue_swap_mode(m, sum, cur.img0, cur.u0, ti, co32, cur.co_blk, prm, elane);
           } else {
             acc_t one[1][1] = {{sum}};
             if (m.pool)
-              epilogue_mode<1>(m, one, cur.img0, cur.u0, ti, co32, lane);
+              epilogue_mode<1>(m, one, cur.img0, cur.u0, ti, co32, elane);
             else
-              epilogue_mode<0>(m, one, cur.img0, cur.u0, ti, co32, lane);
+              epilogue_mode<0>(m, one, cur.img0, cur.u0, ti, co32, elane);
           }
         }
       } else if (co_w < a.cout) {
@@ -1033,13 +1045,13 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
 #undef QC_PICK
               default: break;
             }
-            tile_epilogue_swap_mode(m, tcur, cur.img0, cur.u0, wm * MT + i, co32, cur.co_blk, prm, lane);
+            tile_epilogue_swap_mode(m, tcur, cur.img0, cur.u0, wm * MT + i, co32, cur.co_blk, prm, elane);
           }
         } else {
           if (m.pool)
-            epilogue_mode<1>(m, acc, cur.img0, cur.u0, wm * MT, co_w, lane);
+            epilogue_mode<1>(m, acc, cur.img0, cur.u0, wm * MT, co_w, elane);
           else
-            epilogue_mode<0>(m, acc, cur.img0, cur.u0, wm * MT, co_w, lane);
+            epilogue_mode<0>(m, acc, cur.img0, cur.u0, wm * MT, co_w, elane);
         }
       }
 #pragma unroll
@@ -1054,8 +1066,9 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
     if (nchunk == 0) {
       ipar ^= 1;
       w = nw;
-      decode_item<MT, NT, WN>(m, w, wm, r32, g, &cur);
-      if constexpr (SWAP) load_params<BCO>(a, cur.co_blk, tid, prm_base + ipar * (PARAM_BYTES / 4));
+      const int dt = fresh_tid();
+      decode_item<MT, NT, WN>(m, w, wm, dt & 31, (dt >> 5) & 1, &cur);
+      if constexpr (SWAP) load_params<BCO>(a, cur.co_blk, fresh_tid(), prm_base + ipar * (PARAM_BYTES / 4));
     }
     chunk = nchunk;
     sbuf ^= 1;
