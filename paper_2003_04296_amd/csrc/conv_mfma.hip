@@ -427,6 +427,37 @@ __device__ __forceinline__ void tile_epilogue(const MfmaArgs& m, const AccT& acc
   }
 }
 
+// Plane bits of Q(HardTanh(z)) for the 16 values a lane holds in the
+// swapped orientation (Eqs. 4, 21, 22; the quantizer's compares): value
+// v = 4q + i goes to bit 8q + i; the caller shifts the words by 4g, masks
+// missing channels and merges the other half of the word.  HT: apply
+// HardTanh first (only when a threshold reaches 1 does it change a result).
+template <int OB, bool HT>
+__device__ __forceinline__ void swap_plane_bits(const float (&zs)[16], const Thr& t, uint32_t* pw) {
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int pos = 8 * (v / 4) + (v % 4);
+    const float zz = HT ? hardtanh(zs[v]) : zs[v];
+    const uint32_t s = zz > 0.0f ? 1u : 0u;
+    if constexpr (OB == 1) {
+      pw[0] |= s << pos;
+    } else if constexpr (OB == 2) {
+      const uint32_t nz = !(fabsf(zz) <= t.t0) ? 1u : 0u;
+      pw[0] |= (s & nz) << pos;
+      pw[1] |= nz << pos;
+    } else {
+      const float az = fabsf(zz);
+      const uint32_t a1 = !(az <= t.t0) ? 1u : 0u;
+      const uint32_t a2 = !(az <= t.t1) ? 1u : 0u;
+      const uint32_t a3 = !(az <= t.t2) ? 1u : 0u;
+      pw[0] |= (s & a1) << pos;
+      pw[1] |= a3 << pos;
+      pw[2] |= (a2 & ~a3) << pos;
+      pw[3] |= (a1 & ~a2) << pos;
+    }
+  }
+}
+
 // Residual values of one tile of the swapped orientation (register
 // v = 4q + i of lane l: channel co32 + 8q + 4(l/32) + i, unit 32T + l%32),
 // loaded in one batch: on gfx9 loads and stores share one in-order counter,
@@ -468,6 +499,7 @@ __device__ __forceinline__ void tile_epilogue_swap(const MfmaArgs& m, const AccT
   uint32_t pw[POUT];
 #pragma unroll
   for (int p = 0; p < POUT; ++p) pw[p] = 0u;
+  float zs[16];  // z of the 16 values, for the packed planes
   const ConvArgs& a = m.c;
   const int g = lane >> 5, r32 = lane & 31;
   const float inv = 1.0f / (float)(1 << a.shift);
@@ -515,36 +547,35 @@ __device__ __forceinline__ void tile_epilogue_swap(const MfmaArgs& m, const AccT
         }
         bits = __float_as_uint(z);
       }
-      const bool cok = full || cbase + 8 * q + i < a.cout;
       if constexpr (KIND != K_PACK) {
-        if (cok) __builtin_amdgcn_raw_buffer_store_b32(bits, orsrc, voff, so, 0);
+        if (full || cbase + 8 * q + i < a.cout) __builtin_amdgcn_raw_buffer_store_b32(bits, orsrc, voff, so, 0);
       }
-      if constexpr (OB > 0) {
-        const float zz = m.ht_needed ? hardtanh(z) : z;
-        const int b = 8 * q + 4 * g + i;  // bit of channel co32 + b
-        const uint32_t s = (cok & (zz > 0.0f)) ? 1u : 0u;
-        if constexpr (OB == 1) {
-          pw[0] |= s << b;
-        } else if constexpr (OB == 2) {
-          const uint32_t nz = (cok & !(fabsf(zz) <= a.othr.t0)) ? 1u : 0u;
-          pw[0] |= (s & nz) << b;
-          pw[1] |= nz << b;
-        } else {
-          const float az = fabsf(zz);
-          const uint32_t a1 = (cok & !(az <= a.othr.t0)) ? 1u : 0u;
-          const uint32_t a2 = (cok & !(az <= a.othr.t1)) ? 1u : 0u;
-          const uint32_t a3 = (cok & !(az <= a.othr.t2)) ? 1u : 0u;
-          pw[0] |= (s & a1) << b;
-          pw[1] |= a3 << b;
-          pw[2] |= (a2 & ~a3) << b;
-          pw[3] |= (a1 & ~a2) << b;
-        }
-      }
+      zs[4 * q + i] = z;
     }
   }
   if constexpr (OB > 0) {
+    if (m.ht_needed)
+      swap_plane_bits<OB, true>(zs, a.othr, pw);
+    else
+      swap_plane_bits<OB, false>(zs, a.othr, pw);
+    if (!full) {
+      // channels past the last one are 0 in every plane: bit 8q + i holds
+      // channel cbase + 8q + i
+      const int lim = a.cout - cbase;
+      uint32_t vm = 0u;
 #pragma unroll
-    for (int p = 0; p < POUT; ++p) pw[p] |= (uint32_t)__shfl_xor((int)pw[p], 32);
+      for (int q = 0; q < 4; ++q) {
+        const int nb = min(max(lim - 8 * q, 0), 4);
+        vm |= ((1u << nb) - 1u) << (8 * q);
+      }
+#pragma unroll
+      for (int p = 0; p < POUT; ++p) pw[p] &= vm;
+    }
+#pragma unroll
+    for (int p = 0; p < POUT; ++p) {
+      pw[p] <<= 4 * g;  // this lane's channels are cbase + ...: nibbles of half g
+      pw[p] |= (uint32_t)__shfl_xor((int)pw[p], 32);
+    }
     if (g == 0 && uok) {
       uint32_t* dst = a.out_packed + (((int64_t)img * m.upi + uu) * a.out_cw + (co32 >> 5)) * POUT;
       store_words<POUT>(dst, pw);
