@@ -53,8 +53,9 @@
  *                buffer by three matrix-core operand copies of the same
  *                levels, expanded from those bitplanes (channels past cin
  *                and padding output channels are 0): int8 codes [kh][kw][cw][cout_pad][32 B], E2M1 (fp4)
- *                codes [kh][kw][ceil(cw/2)][cout_pad][32 B] (64 channels,
- *                two per byte, low nibble first) and IEEE fp16 codes
+ *                codes [kh][kw][ceil(cw/2)][cout_pad][32 B] (64 channels:
+ *                16 B per 32-channel word, whose u32 q holds channels q,
+ *                q + 4, ..., q + 28 in nibbles 0..7) and IEEE fp16 codes
  *                [kh][kw][2 cw][cout_pad][16 x 2 B] (16 channels per
  *                record); the codes 0, +-1, +-2, +-4 are exact in all three.
  *   An all-zero activation word reads as level -1 for 1 bit and 0 for 2/3

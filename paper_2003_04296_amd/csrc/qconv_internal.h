@@ -93,30 +93,26 @@ __device__ __forceinline__ void expand_i8_word(const uint32_t* pl, uint32_t vali
   }
 }
 
-// Byte -> eight nibble slots: channel i of the byte goes to nibble 2i (i < 4)
-// or nibble 2(i-4)+1 (i >= 4).  Any fixed channel order works for the
-// product as long as both operands use it; this one costs two spreads.
-__device__ __forceinline__ uint32_t spread8(uint32_t b) {
-  return spread4(b & 0xFu) | (spread4((b >> 4) & 0xFu) << 4);
-}
-
 // E2M1 (fp4) codes of 32 channels as 4 words: +1 = 0x2, +2 = 0x4, +4 = 0x6,
-// sign bit 0x8, zero = 0x0.
+// sign bit 0x8, zero = 0x0.  Word q holds channels q, q + 4, ..., q + 28 in
+// nibbles 0..7, so each word takes one shift and one mask per plane: bit
+// q + 4k of a plane lands in bit 4k.  Any fixed channel order works for the
+// product as long as both operands use it (weights and activations are
+// expanded by this one function).
 template <int P>
 __device__ __forceinline__ void expand_fp4_word(const uint32_t* pl, uint32_t valid, uint32_t out[4]) {
+  constexpr uint32_t K = 0x11111111u;
   if constexpr (P <= 2) {
     const uint32_t M = (P == 1) ? valid : pl[1];
     const uint32_t N = M & ~pl[0];
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      out[q] = (spread8((M >> (8 * q)) & 0xFFu) << 1) | (spread8((N >> (8 * q)) & 0xFFu) << 3);
+    for (int q = 0; q < 4; ++q) out[q] = (((M >> q) & K) << 1) | (((N >> q) & K) << 3);
   } else {
     const uint32_t E1 = pl[1], E2 = pl[2], E3 = pl[3];
     const uint32_t B1 = E1 | E3, B2 = E1 | E2, N = (E1 | E2 | E3) & ~pl[0];
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      out[q] = (spread8((B1 >> (8 * q)) & 0xFFu) << 1) | (spread8((B2 >> (8 * q)) & 0xFFu) << 2) |
-               (spread8((N >> (8 * q)) & 0xFFu) << 3);
+      out[q] = (((B1 >> q) & K) << 1) | (((B2 >> q) & K) << 2) | (((N >> q) & K) << 3);
   }
 }
 

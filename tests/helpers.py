@@ -70,14 +70,10 @@ def weight_copies(words, cout, cin, kh, kw, bits):
     f4 = raw[off:off + kh * kw * cwp * cop * 32].reshape(kh, kw, cwp, cop, 2, 4, 4)  # pair, word, u32 q, byte
     # levels from int8: channel cw*32 + c at byte c
     lv8 = np.moveaxis(i8, 2, 3).reshape(kh, kw, cop, cw * 32)[:, :, :cout, :cin]
-    # fp4: u32 q of a word holds channels 8q..8q+7; nibble 2i <- channel 8q+i, nibble 2i+1 <- 8q+4+i
+    # fp4: u32 q of a word holds channels q, q + 4, ..., q + 28 in nibbles 0..7
     u32 = f4.copy().view(np.uint32).reshape(kh, kw, cwp, cop, 2, 4)
     nib = np.stack([(u32 >> (4 * k)) & 0xF for k in range(8)], axis=-1)  # ..., q, nibble k
-    order = np.empty(8, np.int64)
-    for i in range(4):
-        order[i] = 2 * i
-        order[4 + i] = 2 * i + 1
-    nib = nib[..., order]  # channel-ordered within the byte group
+    nib = np.swapaxes(nib, -1, -2)  # ..., k, q: channel 4k + q in row-major order
     mag = np.array([0, 0, 1, 0, 2, 0, 4, 0] * 2, np.int64)[nib]
     sgn = np.where(nib & 8, -1, 1)
     val = (mag * sgn).reshape(kh, kw, cwp, cop, 2 * 32)  # pair, 64 channels
