@@ -1248,26 +1248,27 @@ __global__ __launch_bounds__(1024, 1) void conv_mfma_pp_kernel(const MfmaArgs m)
       __builtin_amdgcn_make_buffer_rsrc((void*)a.act, (short)0, m.act_bytes, 0x00020000);
   auto item_w = [&](int k) __attribute__((always_inline)) { return (int)blockIdx.x + k * (int)gridDim.x; };
 
-  // ---- prologue: each group loads the halo words of its first item; group
-  // 1 then copies the weights and parameters into LDS (up to eight 16-byte
-  // loads in flight per thread, all issued before the first is used) while
-  // group 0 expands item 0 ----
+  // ---- prologue: each group loads the halo words of its first item, then
+  // all 16 waves copy the weights into LDS (up to eight 16-byte loads in
+  // flight per thread, all issued before the first is used: one round for
+  // up to 128 KB); group 1 then loads the parameters while group 0 expands
+  // item 0 ----
   uint32_t raw[NI][PA];
   const int gtid0 = tid & (PP_GROUP - 1);
   int img0, iy0;
   item_origin(m, item_w(grp < n_my ? grp : 0), &img0, &iy0);
   load_halo_rsrc<PA, NI, PP_GROUP>(m, arsrc, img0, iy0, gtid0, raw);
-  if (grp == 1) {
+  {
     const __amdgpu_buffer_rsrc_t brsrc =
         __builtin_amdgcn_make_buffer_rsrc((void*)m.wx, (short)0, m.wx_bytes, 0x00020000);
     const int chunks = taps * ksteps * BCO * 2;  // 16-byte pieces
-    for (int c0 = 0; c0 < chunks; c0 += 8 * PP_GROUP) {
+    for (int c0 = 0; c0 < chunks; c0 += 8 * 2 * PP_GROUP) {
       // a thread past the last piece copies the last piece again (same
       // value, same place), so that every load is consumed
       v4i v[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        const int c = min(c0 + u * PP_GROUP + gtid0, chunks - 1);
+        const int c = min(c0 + u * 2 * PP_GROUP + tid, chunks - 1);
         const int tk = c / (2 * BCO);
         const int rem = c - tk * (2 * BCO);
         v[u] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(
@@ -1275,16 +1276,17 @@ __global__ __launch_bounds__(1024, 1) void conv_mfma_pp_kernel(const MfmaArgs m)
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        const int c = min(c0 + u * PP_GROUP + gtid0, chunks - 1);
+        const int c = min(c0 + u * 2 * PP_GROUP + tid, chunks - 1);
         const int tk = c / (2 * BCO);
         const int rem = c - tk * (2 * BCO);
         *reinterpret_cast<v4i*>(bw + ((tk * 2 + (rem & 1)) * BCO + (rem >> 1)) * 16) = v[u];
       }
     }
-    load_params<BCO>(a, co_blk, gtid0, prm);
-  } else {
-    expand_halo<OPK, PA, NI, PP_GROUP>(m, arsrc, img0, iy0, gtid0, raw, halo);
   }
+  if (grp == 1)
+    load_params<BCO>(a, co_blk, gtid0, prm);
+  else
+    expand_halo<OPK, PA, NI, PP_GROUP>(m, arsrc, img0, iy0, gtid0, raw, halo);
   // Explicit waits for every outstanding global access where that costs
   // nothing (here, and at the start of each store phase, where the only ones
   // are the halo loads of a phase ago): no load issued before them is then
