@@ -120,11 +120,23 @@ def _stream(stream):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
-def _host_f32(vals):
+# threshold values a quantizer of `bits` reads (Eq. 21: one delta; Eq. 22: three)
+_THR_COUNT = {1: 0, 2: 1, 3: 3}
+
+
+def _host_thr(vals, bits: int, what: str):
+    """Host float array of the thresholds for `bits` (None = the defaults).
+    The C side reads exactly 1 value for 2 bits and 3 for 3 bits, so the
+    length is checked here; 1-bit and 16-bit quantizers take none."""
     if vals is None:
         return None
-    arr = (ctypes.c_float * len(vals))(*[float(v) for v in vals])
-    return arr
+    vals = [float(v) for v in (vals.tolist() if hasattr(vals, "tolist") else vals)]
+    need = _THR_COUNT.get(bits, 0)
+    if need == 0:
+        return None
+    if len(vals) != need:
+        raise ValueError(f"{what}: {bits}-bit thresholds take {need} value(s), got {len(vals)}")
+    return (ctypes.c_float * need)(*vals)
 
 
 def planes(bits: int) -> int:
@@ -157,7 +169,7 @@ def pack_act(x, bits: int, thresholds=None, out=None, stream=None):
     n, c, h, w = x.shape
     if out is None:
         out = torch.empty(packed_act_words(n, c, h, w, bits), dtype=torch.int32, device=x.device)
-    t = _host_f32(thresholds)
+    t = _host_thr(thresholds, bits, "pack_act")
     _check(lib().qconv_pack_act(_ptr(x), n, c, h, w, bits, t, _ptr(out), _stream(stream)), "qconv_pack_act")
     return out
 
@@ -169,7 +181,7 @@ def pack_weight(w, bits: int, base_thresholds=None, stream=None):
     cout, cin, kh, kw = w.shape
     out = torch.empty(packed_weight_words(cout, cin, kh, kw, bits), dtype=torch.int32, device=w.device)
     scale = torch.empty(cout, dtype=torch.float32, device=w.device)
-    t = _host_f32(base_thresholds)
+    t = _host_thr(base_thresholds, bits, "pack_weight")
     _check(lib().qconv_pack_weight(_ptr(w), cout, cin, kh, kw, bits, t, _ptr(out), _ptr(scale), _stream(stream)),
            "qconv_pack_weight")
     return out, scale
@@ -181,7 +193,7 @@ def aqe_forward(x, bits: int, alpha: float, thresholds=None, scale=None, group_s
     import torch
 
     y = torch.empty_like(x) if out is None else out
-    t = _host_f32(thresholds)
+    t = _host_thr(thresholds, bits, "aqe_forward")
     _check(lib().aqe_forward(_ptr(x), x.numel(), bits, float(alpha), t, _ptr(scale), int(group_size), _ptr(y),
                              _stream(stream)), "aqe_forward")
     return y
@@ -231,7 +243,7 @@ def conv(act_packed, w_packed, n, cin, h, w, cout, k, stride, pad, a_bits, w_bit
     if out_packed is None and mode == EPI_BN_PACK:
         out_packed = torch.empty(packed_act_words(n, cout, ho, wo, out_bits), dtype=torch.int32, device=dev)
     d = qconv_desc(n, cin, h, w, cout, k, k, stride, pad, a_bits, w_bits, algo)
-    thr = _host_f32(out_thresholds) if out_thresholds else None  # kept alive across the call
+    thr = _host_thr(out_thresholds, out_bits, "conv") if out_thresholds is not None else None  # alive across the call
     e = qconv_epilogue(mode, flags, _ptr(scale), _ptr(bn_k), _ptr(bn_b), _ptr(residual), out_bits,
                        ctypes.cast(thr, ctypes.c_void_p) if thr is not None else None)
     _check(lib().qconv_forward(ctypes.byref(d), _ptr(act_packed), _ptr(w_packed), ctypes.byref(e), _ptr(out),

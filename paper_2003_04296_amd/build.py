@@ -32,13 +32,42 @@ def sources() -> list[str]:
 
 
 def build(verbose: bool = False) -> str:
+    """Compile every source to an object in parallel (one hipcc per source),
+    then link them into libqconv.so."""
+    import concurrent.futures
+    import tempfile
+    import time
+
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+    compile_flags = [f for f in HIPCC_FLAGS if f != "-shared"]
+    tmpdir = tempfile.mkdtemp(prefix="qconv_build_")
+    srcs = sources()
+    objs = [os.path.join(tmpdir, os.path.basename(s) + ".o") for s in srcs]
+
+    def one(pair):
+        src, obj = pair
+        t0 = time.time()
+        cmd = [hipcc, *compile_flags, "-c", src, "-o", obj]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        return src, r, time.time() - t0, cmd
+
+    jobs = max(1, min(len(srcs), int(os.environ.get("MAX_JOBS", os.cpu_count() or 4))))
+    with concurrent.futures.ThreadPoolExecutor(jobs) as ex:
+        for src, r, dt, cmd in ex.map(one, zip(srcs, objs)):
+            if verbose:
+                print(f"{os.path.basename(src)}: {dt:.1f} s", flush=True)
+            if r.returncode != 0:
+                sys.stderr.write(r.stdout + r.stderr)
+                raise subprocess.CalledProcessError(r.returncode, cmd)
     tmp = LIB + ".tmp"
-    cmd = [hipcc, *HIPCC_FLAGS, *sources(), "-o", tmp]
+    cmd = [hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
     os.replace(tmp, LIB)
+    for o in objs:
+        os.remove(o)
+    os.rmdir(tmpdir)
     return LIB
 
 

@@ -235,18 +235,23 @@ int prepare_conv(const qconv_desc* d, const uint32_t* act_packed, const uint32_t
     if (d->n > 0 && !mfma_supports(a)) return QCONV_EUNSUPPORTED;
     return QCONV_ALGO_MFMA_F16;
   }
+  // the fp4 matrix cores accumulate in fp32: every partial sum is an integer
+  // of magnitude at most K * max|a| * max|w|, exact only below 2^24
+  const bool fp4_exact = K * max_code(d->a_bits) * max_code(d->w_bits) < ((int64_t)1 << 24);
+  if (d->algo == QCONV_ALGO_MFMA_FP4 && !fp4_exact) return QCONV_EUNSUPPORTED;
   if (d->algo == QCONV_ALGO_MFMA_I8 || d->algo == QCONV_ALGO_MFMA_FP4) {
     a.mfma_op = d->algo == QCONV_ALGO_MFMA_FP4 ? OP_FP4 : OP_I8;
     if (d->n > 0 && !mfma_supports(a)) return QCONV_EUNSUPPORTED;
     return d->algo;
   }
-  // AUTO: the fp4 matrix cores, except for tiny contractions (K <= 256, the
-  // 1x1 shortcut convolutions of ResNet-18), where staging an input tile in
-  // LDS costs more than the whole bitplane product (measured 18-19 us on the
-  // bitplane kernel against 21-29 us on the matrix cores for those layers)
+  // AUTO: the fp4 matrix cores (int8 ones, whose int32 accumulator is exact
+  // at any size, past the fp4 bound), except for tiny contractions (K <= 256,
+  // the 1x1 shortcut convolutions of ResNet-18), where staging an input tile
+  // in LDS costs more than the whole bitplane product (measured 18-19 us on
+  // the bitplane kernel against 21-29 us on the matrix cores for those layers)
   if (d->algo == QCONV_ALGO_AUTO && d->n > 0 && K > 256) {
-    a.mfma_op = OP_FP4;
-    if (mfma_supports(a)) return QCONV_ALGO_MFMA_FP4;
+    a.mfma_op = fp4_exact ? OP_FP4 : OP_I8;
+    if (mfma_supports(a)) return fp4_exact ? QCONV_ALGO_MFMA_FP4 : QCONV_ALGO_MFMA_I8;
   }
   return QCONV_ALGO_BITPLANE;
 }

@@ -1,0 +1,9 @@
+// conv_mfma_fp4_p1.hip -- the matrix-core convolution kernels for operand
+// format OP_FP4 with 1 activation word(s) per 32 channels (conv_mfma.h).
+#include "conv_mfma.h"
+
+namespace qc {
+namespace mfma {
+QC_MFMA_DEFINE(fp4_p1, OP_FP4, 1)
+}  // namespace mfma
+}  // namespace qc

@@ -1,0 +1,9 @@
+// conv_mfma_i8_p2.hip -- the matrix-core convolution kernels for operand
+// format OP_I8 with 2 activation word(s) per 32 channels (conv_mfma.h).
+#include "conv_mfma.h"
+
+namespace qc {
+namespace mfma {
+QC_MFMA_DEFINE(i8_p2, OP_I8, 2)
+}  // namespace mfma
+}  // namespace qc

@@ -239,3 +239,44 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(q, "LIB_PATH", str(tmp_path / "absent.so"))
     with pytest.raises(RuntimeError, match="no CPU fallback"):
         q.lib()
+
+
+def test_fp4_refused_past_exact_fp32_accumulation():
+    """The fp4 matrix cores accumulate in fp32, exact only while every partial
+    sum (at most K * max|a| * max|w|) stays below 2^24: an explicit fp4 request
+    past that is refused, and AUTO takes the int8 matrix cores (exact int32)
+    or the bitplane kernel instead."""
+    bint = q.qconv_epilogue(q.EPI_INT32, 0, None, None, None, None, 0, None)
+    L = q.lib()
+    for ab, wb, mx in ((3, 3, 16), (1, 1, 1), (3, 1, 4)):
+        k_lim = (1 << 24) // mx  # smallest K whose bound reaches 2^24
+        for cin, ok in ((k_lim - 1, True), (k_lim, False), (k_lim + 1000, False)):
+            d = _desc(n=1, cin=cin, h=2, w=2, kh=1, kw=1, pad=0, a_bits=ab, w_bits=wb, cout=32,
+                      algo=q.ALGO_MFMA_FP4)
+            rc = L.qconv_resolve_algo(ctypes.byref(d), ctypes.byref(bint))
+            if ok:
+                assert rc == q.ALGO_MFMA_FP4, (ab, wb, cin)
+            else:
+                assert rc == q.QCONV_EUNSUPPORTED, (ab, wb, cin)
+                d.algo = q.ALGO_AUTO
+                auto = L.qconv_resolve_algo(ctypes.byref(d), ctypes.byref(bint))
+                assert auto in (q.ALGO_MFMA_I8, q.ALGO_BITPLANE), (ab, wb, cin, auto)
+                d.algo = q.ALGO_MFMA_I8
+                assert L.qconv_resolve_algo(ctypes.byref(d), ctypes.byref(bint)) in (q.ALGO_MFMA_I8,
+                                                                                       q.QCONV_EUNSUPPORTED)
+    # the 3x3 form of the 3W3A bound: K = 9 cin
+    assert q.resolve_algo(1, 116508, 4, 4, 32, 3, 1, 1, 3, 3, algo=q.ALGO_AUTO) == q.ALGO_MFMA_FP4
+    assert q.resolve_algo(1, 116509, 4, 4, 32, 3, 1, 1, 3, 3, algo=q.ALGO_AUTO) != q.ALGO_MFMA_FP4
+
+
+@pytest.mark.parametrize("bits,vals", [(2, [0.5, 0.6]), (3, [0.1, 0.2]), (3, [0.1, 0.2, 0.3, 0.4]), (2, [])])
+def test_binding_checks_threshold_counts(bits, vals):
+    """The C side reads exactly one threshold for 2 bits and three for 3 bits
+    from the host array; the binding refuses any other count before the call."""
+    with pytest.raises(ValueError, match="thresholds take"):
+        q._host_thr(vals, bits, "test")
+    assert q._host_thr(None, bits, "test") is None
+    assert q._host_thr(np.array([0.5] * {2: 1, 3: 3}[bits], np.float32), bits, "test") is not None
+    # zero-valued thresholds are a real setting, not "use the defaults"
+    arr = q._host_thr(np.zeros({2: 1, 3: 3}[bits], np.float32), bits, "test")
+    assert arr is not None and list(arr) == [0.0] * {2: 1, 3: 3}[bits]

@@ -226,11 +226,21 @@ def _close(got, want, bound, extra_ulps_of=None):
 
 
 def _codes_valid(got, want, z, bound, bits):
-    """Codes equal, except where z lies within `bound` of a threshold."""
-    t = np.array([0.0] + list(oracle.ACT_THRESHOLDS[bits]), np.float64)
-    near = (np.abs(np.abs(z.astype(np.float64))[..., None] - t) <= bound[..., None] + 4 * np.spacing(np.float32(1))).any(-1)
+    """Codes equal, except where z lies within `bound` of a threshold; there
+    the GPU code must be one the quantizer gives to some value within the
+    bound of z: Q(HardTanh(.)) is monotone, so it lies between the codes of
+    z - bound and z + bound (each widened by one fp32 ulp outwards)."""
+    z64 = z.astype(np.float64)
+    b64 = np.broadcast_to(bound, z.shape).astype(np.float64)
+    lo_z = np.nextafter((z64 - b64).astype(np.float32), np.float32(-np.inf))
+    hi_z = np.nextafter((z64 + b64).astype(np.float32), np.float32(np.inf))
+    lo = oracle.quantize(oracle.hardtanh(lo_z), bits).astype(np.int32)
+    hi = oracle.quantize(oracle.hardtanh(hi_z), bits).astype(np.int32)
+    g = got.astype(np.int32)
     diff = got != want
-    assert not (diff & ~near).any(), int((diff & ~near).sum())
+    assert ((lo <= g) & (g <= hi)).all(), int((diff & ~((lo <= g) & (g <= hi))).sum())
+    # a differing code only where the bound straddles a threshold
+    assert not (diff & (lo == hi)).any(), int((diff & (lo == hi)).sum())
     assert diff.mean() < 1e-3
 
 

@@ -1,0 +1,167 @@
+"""GPU parity of the quantizers' free parameters against the oracle (run
+with -m gpu): the delta of Eq. 21 and the thresholds of Eq. 22, which the
+paper leaves open, at values other than the defaults.
+
+Thresholds that reach 1 make the HardTanh of the Sec. III-E constructs
+matter (Q(HardTanh(z)) differs from Q(z) once a level boundary sits at or
+beyond 1), so those cases run the HardTanh branch of every epilogue.  Every
+output is compared bit for bit with the oracle's own quantizer applied to the
+oracle's own BN result."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2003_04296_amd as q
+from paper_2003_04296_amd import synth
+from helpers import tail_bits_zero, unpack_act, unpack_weight
+
+pytestmark = pytest.mark.gpu
+
+ALGOS = {"bitplane": q.ALGO_BITPLANE, "mfma_i8": q.ALGO_MFMA_I8, "mfma_fp4": q.ALGO_MFMA_FP4}
+
+# activation thresholds (ordered, >= 0); the sets marked "ht" have a boundary at or past 1
+OUT_THRESHOLDS = {
+    2: [(0.2,), (1.0,), (1.7,)],
+    3: [(0.05, 0.3, 0.8), (0.25, 0.5, 1.0), (0.4, 1.1, 2.0), (0.0, 0.0, 0.0), (0.3, 0.3, 0.9)],
+}
+WEIGHT_BASE_THRESHOLDS = {2: [(0.3,), (1.2,)], 3: [(0.2, 0.5, 0.9), (0.3, 0.8, 1.5), (0.0, 0.5, 0.5)]}
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    oracle.lib()
+    q.lib()
+    return torch.device("cuda:0")
+
+
+def _inputs(seed, n, cin, h, w, cout, k):
+    g = synth.generator(seed)
+    x = synth.normal(g, (n, cin, h, w), 1.0)
+    wt = synth.normal(g, (cout, cin, k, k), 2.0 / (cin * k * k))
+    flat = x.view(-1)
+    vals = torch.tensor([0.0, -0.0, float("nan"), 1.0, -1.0, 0.2, 0.25, 0.5, 1.1, 2.0, 0.3, -0.9])
+    flat[:vals.numel()] = vals
+    return x, wt
+
+
+def _wide_bn(seed, cout, kmax):
+    """BN parameters that spread z over about [-3, 3], so every level of every
+    threshold set is reached, ties included."""
+    g = synth.generator(seed)
+    k = synth.uniform(g, (cout,), 0.2 * kmax, kmax)
+    b = synth.normal(g, (cout,), 0.5)
+    return k, b
+
+
+@pytest.mark.parametrize("bits", [2, 3])
+def test_pack_act_thresholds(dev, bits):
+    n, c, h, w = 3, 70, 9, 11
+    x, _ = _inputs(41, n, c, h, w, 1, 1)
+    x = x * 1.5
+    for thr in OUT_THRESHOLDS[bits]:
+        words = q.pack_act(x.to(dev), bits, thresholds=thr)
+        torch.cuda.synchronize()
+        got = unpack_act(words.cpu().numpy(), n, c, h, w, bits)
+        np.testing.assert_array_equal(got, oracle.quantize(x.numpy(), bits, thr), err_msg=str(thr))
+        assert tail_bits_zero(words.cpu().numpy(), c, bits)
+
+
+@pytest.mark.parametrize("bits", [2, 3])
+def test_pack_weight_base_thresholds(dev, bits):
+    cout, cin, k = 70, 40, 3
+    _, wt = _inputs(42, 1, cin, 1, 1, cout, k)
+    for bt in WEIGHT_BASE_THRESHOLDS[bits]:
+        words, scale = q.pack_weight(wt.to(dev), bits, base_thresholds=bt)
+        torch.cuda.synchronize()
+        lv, s = oracle.quantize_weights(wt.numpy(), bits, bt)
+        np.testing.assert_array_equal(scale.cpu().numpy(), s)
+        np.testing.assert_array_equal(unpack_weight(words.cpu().numpy(), cout, cin, k, k, bits), lv, err_msg=str(bt))
+
+
+CASES = [
+    # n, cin, h, w, cout, k, stride, pad
+    (2, 40, 10, 9, 70, 3, 1, 1),     # ragged channels, odd width
+    (3, 64, 16, 16, 96, 3, 1, 1),    # 256-row items, two channel tiles
+    (64, 96, 4, 4, 100, 4, 1, 0),    # fully connected as a conv (split-K blocks)
+]
+
+
+def _oracle_z(x, wt, ab, wb, s, p, kk, bb, pool):
+    la = oracle.quantize(x.numpy(), ab)
+    lw, _ = oracle.quantize_weights(wt.numpy(), wb)
+    acc = oracle.qconv_acc(la, lw, ab, s, p)
+    if pool:
+        acc = oracle.maxpool2_int(acc)
+    return oracle.epi_bn(acc, kk.numpy(), bb.numpy(), oracle.level_shift(ab) + oracle.level_shift(wb))
+
+
+@pytest.mark.parametrize("algo", list(ALGOS))
+@pytest.mark.parametrize("out_bits", [2, 3])
+@pytest.mark.parametrize("pool", [False, True])
+@pytest.mark.parametrize("ci", range(len(CASES)))
+def test_requantize_thresholds(dev, ci, pool, out_bits, algo):
+    """{QConv-[pool]-BN-HardTanh} with non-default requantization thresholds:
+    BN_PACK, and BN_F32 with a packed copy, against Q(HardTanh(z)) of the
+    oracle with the same thresholds."""
+    n, cin, h, w, cout, k, s, p = CASES[ci]
+    ho, wo = q.out_size(h, k, s, p), q.out_size(w, k, s, p)
+    if pool and (ho < 2 or wo < 2):
+        pytest.skip("no 2x2 window")
+    flags = q.EPI_POOL2 if pool else 0
+    for ab, wb in [(1, 1), (2, 2), (3, 3)]:
+        x, wt = _inputs(43 + ci + ab, n, cin, h, w, cout, k)
+        kmax = 3.0 / np.sqrt(cin * k * k) * (4 if ab == 3 else 1)
+        kk, bb = _wide_bn(44 + ci + ab, cout, kmax)
+        z = _oracle_z(x, wt, ab, wb, s, p, kk, bb, pool)
+        act = q.pack_act(x.to(dev), ab)
+        wq, _ = q.pack_weight(wt.to(dev), wb)
+        oh, ow = z.shape[2], z.shape[3]
+        for thr in OUT_THRESHOLDS[out_bits]:
+            want = oracle.quantize(oracle.hardtanh(z), out_bits, thr)
+            try:
+                _, outp = q.conv(act, wq, n, cin, h, w, cout, k, s, p, ab, wb, mode=q.EPI_BN_PACK, flags=flags,
+                                 bn_k=kk.to(dev), bn_b=bb.to(dev), out_bits=out_bits, algo=ALGOS[algo],
+                                 out_thresholds=thr)
+            except q.QconvError as e:
+                if e.status == q.QCONV_EUNSUPPORTED:
+                    pytest.skip("configuration not supported by this algorithm")
+                raise
+            outp2 = torch.empty_like(outp)
+            zf, _ = q.conv(act, wq, n, cin, h, w, cout, k, s, p, ab, wb, mode=q.EPI_BN_F32, flags=flags,
+                           bn_k=kk.to(dev), bn_b=bb.to(dev), out_bits=out_bits, out_packed=outp2, algo=ALGOS[algo],
+                           out_thresholds=thr)
+            torch.cuda.synchronize()
+            msg = f"bits {(ab, wb)} thresholds {thr}"
+            np.testing.assert_array_equal(unpack_act(outp.cpu().numpy(), n, cout, oh, ow, out_bits), want, err_msg=msg)
+            np.testing.assert_array_equal(zf.cpu().numpy(), z, err_msg=msg)
+            np.testing.assert_array_equal(unpack_act(outp2.cpu().numpy(), n, cout, oh, ow, out_bits), want,
+                                          err_msg=msg)
+            assert tail_bits_zero(outp.cpu().numpy(), cout, out_bits)
+            # the HardTanh branch changes the result for these thresholds somewhere
+            if (out_bits == 2 and thr[0] >= 1.0) or (out_bits == 3 and thr[2] >= 1.0):
+                assert np.any(want != oracle.quantize(z, out_bits, thr)), msg
+
+
+def test_requantize_thresholds_with_residual(dev):
+    """BN + residual in fp32, then the packed copy of Q(HardTanh(z + r)) with
+    thresholds at 1 (the residual block's repack)."""
+    n, cin, h, w, cout = 3, 64, 8, 8, 64
+    for ab, thr in [(2, (1.0,)), (3, (0.25, 0.5, 1.0))]:
+        x, wt = _inputs(45 + ab, n, cin, h, w, cout, 3)
+        kk, bb = _wide_bn(46 + ab, cout, 3.0 / 24 * (4 if ab == 3 else 1))
+        res = synth.normal(synth.generator(47), (n, cout, h, w), 1.0)
+        z = oracle.add(_oracle_z(x, wt, ab, ab, 1, 1, kk, bb, False), res.numpy())
+        act = q.pack_act(x.to(dev), ab)
+        wq, _ = q.pack_weight(wt.to(dev), ab)
+        for algo in ALGOS.values():
+            outp = torch.empty(q.packed_act_words(n, cout, h, w, ab), dtype=torch.int32, device=dev)
+            out, _ = q.conv(act, wq, n, cin, h, w, cout, 3, 1, 1, ab, ab, mode=q.EPI_BN_F32, flags=q.EPI_RESIDUAL,
+                            bn_k=kk.to(dev), bn_b=bb.to(dev), residual=res.to(dev), out_bits=ab, out_packed=outp,
+                            algo=algo, out_thresholds=thr)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(out.cpu().numpy(), z)
+            np.testing.assert_array_equal(unpack_act(outp.cpu().numpy(), n, cout, h, w, ab),
+                                          oracle.quantize(oracle.hardtanh(z), ab, thr), err_msg=str((ab, algo)))

@@ -135,3 +135,81 @@ def test_weight_ternary_threshold_is_07_mean_abs(oracle_mod):
 def test_pad_levels(oracle_mod):
     # The padding tap holds Q(0): -1 for the sign quantizer, 0 otherwise.
     assert [oracle_mod.pad_level(b) for b in (1, 2, 3)] == [-1, 0, 0]
+
+
+def test_hardtanh_clamps_to_unit_interval(oracle_mod):
+    """HardTanh (Sec. III-E) is max(-1, min(1, x)): evaluated here with Python's
+    own float min/max on a sweep through +-1, one ulp either side of +-1, the
+    extremes, infinities and signed zeros; NaN passes through."""
+    one = np.float32(1)
+    pts = [0.0, -0.0, 0.5, -0.5, 1.0, -1.0, 2.0, -2.0, 1e-45, -1e-45, 3e38, -3e38, np.inf, -np.inf,
+           np.nextafter(one, np.float32(2)), np.nextafter(one, np.float32(0)),
+           np.nextafter(-one, np.float32(-2)), np.nextafter(-one, np.float32(0))]
+    x = np.concatenate([np.array(pts, np.float32), np.linspace(-4, 4, 4001, dtype=np.float32)])
+    got = oracle_mod.hardtanh(x)
+    want = np.array([max(-1.0, min(1.0, float(v))) for v in x], np.float32)
+    np.testing.assert_array_equal(got, want)
+    # signed zeros are kept (no clamp applies to them)
+    assert np.signbit(oracle_mod.hardtanh(np.array([-0.0], np.float32))[0])
+    assert not np.signbit(oracle_mod.hardtanh(np.array([0.0], np.float32))[0])
+    # values inside [-1, 1] are returned unchanged, values outside land exactly on the bound
+    inside = x[np.abs(x) <= 1]
+    np.testing.assert_array_equal(oracle_mod.hardtanh(inside), inside)
+    assert set(np.unique(got[np.abs(x) > 1]).tolist()) == {-1.0, 1.0}
+    nan = oracle_mod.hardtanh(np.array([np.nan], np.float32))
+    assert np.isnan(nan[0])
+
+
+def _pow2_channel(scale_exp: int, rng):
+    """One output channel of 3-bit test weights whose mean |w| is exactly
+    2^scale_exp: a dyadic grid over [-1.5, 1.5] (in units of the scale, so it
+    holds the midpoints 1/8, 3/8, 3/4 of adjacent levels exactly), the
+    neighbours one ulp either side of each midpoint in pairs whose |sum| is
+    exact, and one balancing weight that makes sum |w| = K * 2^scale_exp."""
+    s = 2.0 ** scale_exp
+    grid = [i / 64 for i in range(-96, 97)]
+    pts = []
+    for m in (0.125, 0.375, 0.75):
+        mf = np.float32(m)
+        up = float(np.nextafter(mf, np.float32(2))) - m
+        dn = m - float(np.nextafter(mf, np.float32(0)))
+        # m + up and k copies of m - dn with up == k * dn sum to an exact dyadic value
+        k = int(round(up / dn))
+        pts += [m + up] + [m - dn] * k
+        pts += [-(m + up)] + [-(m - dn)] * k
+    units = grid + pts
+    rng.shuffle(units)
+    total = sum(abs(Fraction(u)) for u in units)
+    kk = len(units) + 1
+    bal = Fraction(kk) - total
+    assert bal >= 0
+    units.append(float(bal))
+    w = np.array([u * s for u in units], np.float32)
+    assert sum(abs(Fraction(float(v))) for v in w) == Fraction(kk) * Fraction(s)
+    return w
+
+
+def test_pow2_weight_thresholds_round_to_nearest_scaled_level(oracle_mod):
+    """3-bit weights (Eq. 22 with thresholds t * s_c): brute force in exact
+    rationals, each weight goes to the nearest of {0, +-s/4, +-s/2, +-s}
+    (s = mean |W_c|), ties to the smaller magnitude, saturating at s.  With s a
+    power of two every threshold t * s is exact in fp32, so the oracle must
+    agree on every weight, the exact midpoints and their fp32 neighbours
+    included.  A wrong base threshold (any value other than 1/8, 3/8, 3/4)
+    moves a grid point to another level."""
+    rng = np.random.default_rng(7)
+    chans = [_pow2_channel(e, rng) for e in (-5, -1, 0, 3)]
+    kk = chans[0].size
+    w = np.stack(chans).reshape(len(chans), kk, 1, 1)
+    lv, s = oracle_mod.quantize_weights(w, 3)
+    for c, e in enumerate((-5, -1, 0, 3)):
+        assert float(s[c]) == 2.0 ** e
+        sc = Fraction(2) ** e
+        levels = [Fraction(0), sc / 4, sc / 2, sc]
+        for i in range(kk):
+            v = float(w[c, i, 0, 0])
+            a = abs(Fraction(v))
+            best = min(levels, key=lambda L: (abs(a - L), L))
+            code = int(best / sc * 4)
+            want = code if v > 0 else -code
+            assert int(lv[c, i, 0, 0]) == want, (c, v)
