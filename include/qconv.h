@@ -161,11 +161,16 @@ int qconv_fold_bn(const float* gamma, const float* beta, const float* mean, cons
 /* Quantized convolution with fused epilogue (Algorithm 1 + Sec. III-E)      */
 /* ------------------------------------------------------------------------ */
 typedef enum {
-  QCONV_ALGO_AUTO = 0,     /* library choice: fp4 matrix cores where supported,
-                              the bitplane kernel for K = cin*kh*kw <= 256     */
+  QCONV_ALGO_AUTO = 0,     /* library choice: fp4 matrix cores where supported
+                              (int8 ones where fp4 would not be exact, see
+                              QCONV_ALGO_MFMA_FP4), the bitplane kernel for
+                              K = cin*kh*kw <= 256                             */
   QCONV_ALGO_BITPLANE = 1, /* VALU XNOR/AND + popcount over bitplanes         */
   QCONV_ALGO_MFMA_I8 = 2,  /* int8 matrix cores on the expanded level codes   */
-  QCONV_ALGO_MFMA_FP4 = 3, /* fp4 (E2M1) matrix cores on the same codes        */
+  QCONV_ALGO_MFMA_FP4 = 3, /* fp4 (E2M1) matrix cores on the same codes; they
+                              accumulate in fp32, exact only while
+                              K * max|a| * max|w| < 2^24: past that this
+                              algorithm returns QCONV_EUNSUPPORTED             */
   QCONV_ALGO_MFMA_F16 = 4  /* fp16 matrix cores: the only one with a 16-bit side */
 } qconv_algo;
 
@@ -326,6 +331,18 @@ size_t qnet_workspace_bytes(const qnet* net, int batch);
  * write the last tensor (fp32 [batch][features]) to logits. */
 int qnet_forward(const qnet* net, const float* x, int batch, float* logits, void* workspace,
                  size_t workspace_bytes, void* stream);
+
+/* Layers [first, first + count) of qnet_forward only (layer i produces
+ * tensor i + 1), on a workspace laid out for `batch` images exactly as
+ * qnet_forward lays it out: the tensors those layers read must already hold
+ * what earlier layers (of this or a previous call) wrote there.  Running
+ * every range in order is the same as qnet_forward; used to time or
+ * overlap parts of a network.  count == 0 launches nothing. */
+int qnet_forward_range(const qnet* net, const float* x, int batch, float* logits, void* workspace,
+                       size_t workspace_bytes, int first, int count, void* stream);
+
+/* Number of layers added so far (negative status for a NULL network). */
+int qnet_num_layers(const qnet* net);
 
 /* Shape of tensor `id` for `batch` images (host out-params; bits 0 = fp32),
  * and its byte offset inside the workspace after qnet_forward (the last

@@ -24,7 +24,8 @@ EXPORTED = (
     "qconv_pack_act", "qconv_packed_weight_bytes", "qconv_pack_weight", "qconv_fold_bn",
     "qconv_out_size", "qconv_forward", "qnet_create", "qnet_destroy", "qnet_add_conv_f32",
     "qnet_add_maxpool_f32", "qnet_add_quantize", "qnet_add_qconv", "qnet_add_avgpool",
-    "qnet_add_fc_f32", "qnet_workspace_bytes", "qnet_forward", "qnet_tensor_info", "qconv_resolve_algo",
+    "qnet_add_fc_f32", "qnet_workspace_bytes", "qnet_forward", "qnet_forward_range", "qnet_num_layers",
+    "qnet_tensor_info", "qconv_resolve_algo",
     "qconv_kernel_name", "aqe_forward", "aqe_backward", "aqe_sgd_clip",
 )
 
@@ -97,6 +98,8 @@ def lib() -> ctypes.CDLL:
     L.qnet_workspace_bytes.restype = sz
     L.qnet_workspace_bytes.argtypes = [vp, i32]
     L.qnet_forward.argtypes = [vp, vp, i32, vp, vp, sz, vp]
+    L.qnet_forward_range.argtypes = [vp, vp, i32, vp, vp, sz, i32, i32, vp]
+    L.qnet_num_layers.argtypes = [vp]
     L.qnet_tensor_info.argtypes = [vp, i32, i32] + [ctypes.POINTER(i32)] * 4 + [ctypes.POINTER(sz)]
     _lib = L
     return L
@@ -174,13 +177,17 @@ def pack_act(x, bits: int, thresholds=None, out=None, stream=None):
     return out
 
 
-def pack_weight(w, bits: int, base_thresholds=None, stream=None):
-    """fp32 OIHW device tensor -> (packed weights, s_c)."""
+def pack_weight(w, bits: int, base_thresholds=None, stream=None, out=None):
+    """fp32 OIHW device tensor -> (packed weights, s_c); out = (words, scale)
+    reuses existing buffers."""
     import torch
 
     cout, cin, kh, kw = w.shape
-    out = torch.empty(packed_weight_words(cout, cin, kh, kw, bits), dtype=torch.int32, device=w.device)
-    scale = torch.empty(cout, dtype=torch.float32, device=w.device)
+    if out is None:
+        out = torch.empty(packed_weight_words(cout, cin, kh, kw, bits), dtype=torch.int32, device=w.device)
+        scale = torch.empty(cout, dtype=torch.float32, device=w.device)
+    else:
+        out, scale = out
     t = _host_thr(base_thresholds, bits, "pack_weight")
     _check(lib().qconv_pack_weight(_ptr(w), cout, cin, kh, kw, bits, t, _ptr(out), _ptr(scale), _stream(stream)),
            "qconv_pack_weight")
@@ -282,39 +289,45 @@ class Net:
         if not self._h:
             raise QconvError(QCONV_EINVAL, "qnet_create")
         self._keep = []  # device tensors the layers point at
+        self.layers = []  # per layer: what was added (kind, source, parameters), for reports
 
     def __del__(self):
         if getattr(self, "_h", None) and _lib is not None:
             _lib.qnet_destroy(self._h)
             self._h = None
 
-    def _add(self, rc, what, *keep):
+    def _add(self, rc, what, *keep, **info):
         self._keep.extend(k for k in keep if k is not None)
-        return _check(rc, what)
+        tid = _check(rc, what)
+        self.layers.append(dict(kind=what.replace("qnet_add_", ""), dst=tid, **info))
+        return tid
 
     def conv_f32(self, src, w, bn_k, bn_b, stride=1, pad=0, relu=False, out_bits=0):
         cout, _, k, _ = w.shape
         return self._add(lib().qnet_add_conv_f32(self._h, src, _ptr(w), cout, k, stride, pad, _ptr(bn_k), _ptr(bn_b),
-                                                 int(relu), out_bits), "qnet_add_conv_f32", w, bn_k, bn_b)
+                                                 int(relu), out_bits), "qnet_add_conv_f32", w, bn_k, bn_b,
+                         src=src, cout=cout, k=k, stride=stride, pad=pad, out_bits=out_bits)
 
     def maxpool_f32(self, src, k, stride, pad):
-        return self._add(lib().qnet_add_maxpool_f32(self._h, src, k, stride, pad), "qnet_add_maxpool_f32")
+        return self._add(lib().qnet_add_maxpool_f32(self._h, src, k, stride, pad), "qnet_add_maxpool_f32",
+                         src=src, k=k, stride=stride, pad=pad)
 
     def quantize(self, src, bits):
-        return self._add(lib().qnet_add_quantize(self._h, src, bits), "qnet_add_quantize")
+        return self._add(lib().qnet_add_quantize(self._h, src, bits), "qnet_add_quantize", src=src, out_bits=bits)
 
     def qconv(self, src, w_packed, cout, k, stride, pad, w_bits, bn_k, bn_b, pool2=False, residual_src=-1,
               out_bits=0):
         return self._add(lib().qnet_add_qconv(self._h, src, _ptr(w_packed), cout, k, stride, pad, w_bits, int(pool2),
                                               _ptr(bn_k), _ptr(bn_b), residual_src, out_bits),
-                         "qnet_add_qconv", w_packed, bn_k, bn_b)
+                         "qnet_add_qconv", w_packed, bn_k, bn_b, src=src, cout=cout, k=k, stride=stride, pad=pad,
+                         w_bits=w_bits, pool2=bool(pool2), residual_src=residual_src, out_bits=out_bits)
 
     def avgpool(self, src):
-        return self._add(lib().qnet_add_avgpool(self._h, src), "qnet_add_avgpool")
+        return self._add(lib().qnet_add_avgpool(self._h, src), "qnet_add_avgpool", src=src)
 
     def fc_f32(self, src, w, bias=None):
         return self._add(lib().qnet_add_fc_f32(self._h, src, _ptr(w), _ptr(bias), w.shape[0]), "qnet_add_fc_f32",
-                         w, bias)
+                         w, bias, src=src, cout=w.shape[0])
 
     def workspace_bytes(self, batch):
         return lib().qnet_workspace_bytes(self._h, batch)
@@ -331,3 +344,13 @@ class Net:
         _check(lib().qnet_forward(self._h, _ptr(x), x.shape[0], _ptr(logits), _ptr(workspace), nbytes,
                                   _stream(stream)), "qnet_forward")
         return logits
+
+    def forward_range(self, x, logits, workspace, first, count, stream=None):
+        """Layers [first, first + count) of forward() on the same workspace."""
+        nbytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+        _check(lib().qnet_forward_range(self._h, _ptr(x), x.shape[0], _ptr(logits), _ptr(workspace), nbytes,
+                                        int(first), int(count), _stream(stream)), "qnet_forward_range")
+        return logits
+
+    def num_layers(self):
+        return _check(lib().qnet_num_layers(self._h), "qnet_num_layers")

@@ -540,10 +540,11 @@ int qnet_tensor_info(const qnet* net, int id, int batch, int* c, int* h, int* w,
   return QCONV_OK;
 }
 
-int qnet_forward(const qnet* net, const float* x, int batch, float* logits, void* workspace,
-                 size_t workspace_bytes, void* stream) {
+int qnet_forward_range(const qnet* net, const float* x, int batch, float* logits, void* workspace,
+                       size_t workspace_bytes, int first, int count, void* stream) {
   if (!net || batch < 0 || net->L.empty()) return QCONV_EINVAL;
-  if (batch == 0) return QCONV_OK;
+  if (first < 0 || count < 0 || first + count > (int)net->L.size()) return QCONV_EINVAL;
+  if (batch == 0 || count == 0) return QCONV_OK;
   if (!x || !logits) return QCONV_EINVAL;
   const QTensor& last = net->t.back();
   if (last.bits != 0) return QCONV_EUNSUPPORTED;
@@ -561,7 +562,7 @@ int qnet_forward(const qnet* net, const float* x, int batch, float* logits, void
   };
   Thr dflt[4];
   for (int b = 1; b <= 3; ++b) act_thresholds(b, nullptr, &dflt[b]);
-  for (size_t i = 0; i < net->L.size(); ++i) {
+  for (size_t i = (size_t)first; i < (size_t)(first + count); ++i) {
     const QLayer& l = net->L[i];
     const int dst = (int)i + 1;
     const QTensor& si = net->t[l.src];
@@ -619,5 +620,13 @@ int qnet_forward(const qnet* net, const float* x, int batch, float* logits, void
   }
   return QCONV_OK;
 }
+
+int qnet_forward(const qnet* net, const float* x, int batch, float* logits, void* workspace,
+                 size_t workspace_bytes, void* stream) {
+  return qnet_forward_range(net, x, batch, logits, workspace, workspace_bytes, 0, net ? (int)net->L.size() : 0,
+                            stream);
+}
+
+int qnet_num_layers(const qnet* net) { return net ? (int)net->L.size() : QCONV_EINVAL; }
 
 }  // extern "C"
