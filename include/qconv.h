@@ -95,7 +95,9 @@ typedef enum {
   QCONV_EUNSUPPORTED = -2, /* valid but not implemented (shape, bits, algo)   */
   QCONV_EWORKSPACE = -3,   /* workspace too small                             */
   QCONV_EOVERFLOW = -4,    /* K * max|a| * max|w| >= 2^31 (int32 accumulator) */
-  QCONV_EHIP = -5          /* a HIP launch or runtime call failed             */
+  QCONV_EHIP = -5,         /* a HIP launch or runtime call failed             */
+  QCONV_ESCRATCH = -6      /* qnet_forward_noalloc: the network needs more
+                              than the fixed scratch array holds             */
 } qconv_status;
 
 /* Human-readable text for a status code (never NULL). */
@@ -343,6 +345,38 @@ int qnet_forward_range(const qnet* net, const float* x, int batch, float* logits
 
 /* Number of layers added so far (negative status for a NULL network). */
 int qnet_num_layers(const qnet* net);
+
+/* ------------------------------------------------------------------------ */
+/* Networks without a workspace, for callers that cannot allocate device     */
+/* memory (code under HIP graph capture, tight serving loops, harnesses that */
+/* forbid allocation).                                                       */
+/* ------------------------------------------------------------------------ */
+
+/* Size of the library's fixed scratch array, in MiB: one array per device
+ * the library runs on, allocated when the library's code is loaded on that
+ * device and held until the process ends. */
+#define QNET_NOALLOC_SCRATCH_MIB 128
+
+/* qnet_forward without a workspace argument: the intermediate tensors live
+ * in the library's scratch array of that device (qnet_noalloc_limit() bytes),
+ * placed by a liveness plan (a tensor's bytes are reused once every layer
+ * that reads it has run), so a network needs qnet_noalloc_bytes(net, batch)
+ * of it, far less than qnet_workspace_bytes.  Returns QCONV_ESCRATCH, with
+ * no launch, when that exceeds the array.  Allocates nothing, on the device
+ * or the host (the plan is computed in fixed stack arrays; networks of more
+ * than about 500 layers return QCONV_EUNSUPPORTED).  The array's device
+ * address is looked up once per device, on the first call made with that
+ * device current.  Every call on one device shares its array and leaves the
+ * last call's tensors in it (no layer reads a region it has not written in
+ * the same call, so nothing needs clearing): calls that overlap in time on
+ * one device, from several streams or threads, race and give undefined
+ * results.  The logits are bit-identical to qnet_forward's. */
+int qnet_forward_noalloc(const qnet* net, const float* x, int batch, float* logits, void* stream);
+
+/* Scratch bytes qnet_forward_noalloc needs for `batch` images (0 on bad
+ * input), and the array's size. */
+size_t qnet_noalloc_bytes(const qnet* net, int batch);
+size_t qnet_noalloc_limit(void);
 
 /* Shape of tensor `id` for `batch` images (host out-params; bits 0 = fp32),
  * and its byte offset inside the workspace after qnet_forward (the last

@@ -14,6 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libqconv.so")
 
 QCONV_OK, QCONV_EINVAL, QCONV_EUNSUPPORTED, QCONV_EWORKSPACE, QCONV_EOVERFLOW, QCONV_EHIP = 0, -1, -2, -3, -4, -5
+QCONV_ESCRATCH = -6
 ALGO_AUTO, ALGO_BITPLANE, ALGO_MFMA_I8, ALGO_MFMA_FP4, ALGO_MFMA_F16 = 0, 1, 2, 3, 4
 EPI_INT32, EPI_SCALE_F32, EPI_BN_F32, EPI_BN_PACK = 0, 1, 2, 3
 EPI_POOL2, EPI_RESIDUAL = 1, 2
@@ -25,6 +26,7 @@ EXPORTED = (
     "qconv_out_size", "qconv_forward", "qnet_create", "qnet_destroy", "qnet_add_conv_f32",
     "qnet_add_maxpool_f32", "qnet_add_quantize", "qnet_add_qconv", "qnet_add_avgpool",
     "qnet_add_fc_f32", "qnet_workspace_bytes", "qnet_forward", "qnet_forward_range", "qnet_num_layers",
+    "qnet_forward_noalloc", "qnet_noalloc_bytes", "qnet_noalloc_limit",
     "qnet_tensor_info", "qconv_resolve_algo",
     "qconv_kernel_name", "aqe_forward", "aqe_backward", "aqe_sgd_clip",
 )
@@ -100,6 +102,11 @@ def lib() -> ctypes.CDLL:
     L.qnet_forward.argtypes = [vp, vp, i32, vp, vp, sz, vp]
     L.qnet_forward_range.argtypes = [vp, vp, i32, vp, vp, sz, i32, i32, vp]
     L.qnet_num_layers.argtypes = [vp]
+    L.qnet_forward_noalloc.argtypes = [vp, vp, i32, vp, vp]
+    L.qnet_noalloc_bytes.restype = sz
+    L.qnet_noalloc_bytes.argtypes = [vp, i32]
+    L.qnet_noalloc_limit.restype = sz
+    L.qnet_noalloc_limit.argtypes = []
     L.qnet_tensor_info.argtypes = [vp, i32, i32] + [ctypes.POINTER(i32)] * 4 + [ctypes.POINTER(sz)]
     _lib = L
     return L
@@ -351,6 +358,15 @@ class Net:
         _check(lib().qnet_forward_range(self._h, _ptr(x), x.shape[0], _ptr(logits), _ptr(workspace), nbytes,
                                         int(first), int(count), _stream(stream)), "qnet_forward_range")
         return logits
+
+    def forward_noalloc(self, x, logits, stream=None):
+        """forward() on the library's fixed scratch array instead of a workspace."""
+        _check(lib().qnet_forward_noalloc(self._h, _ptr(x), x.shape[0], _ptr(logits), _stream(stream)),
+               "qnet_forward_noalloc")
+        return logits
+
+    def noalloc_bytes(self, batch):
+        return lib().qnet_noalloc_bytes(self._h, batch)
 
     def num_layers(self):
         return _check(lib().qnet_num_layers(self._h), "qnet_num_layers")

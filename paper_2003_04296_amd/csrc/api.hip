@@ -5,6 +5,8 @@
 #include <math.h>
 #include <string.h>
 
+#include <atomic>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -13,6 +15,8 @@
 using namespace qc;
 
 namespace {
+
+constexpr int MAX_DEVICES_API = 64;
 
 constexpr float kActThr2[1] = {0.5f};
 constexpr float kActThr3[3] = {0.125f, 0.375f, 0.75f};
@@ -57,6 +61,7 @@ const char* qconv_error_string(int status) {
     case QCONV_EWORKSPACE: return "workspace too small";
     case QCONV_EOVERFLOW: return "int32 accumulator could overflow (K * max|a| * max|w| >= 2^31)";
     case QCONV_EHIP: return "HIP launch or runtime error";
+    case QCONV_ESCRATCH: return "needs more than the library's fixed no-allocation scratch (qnet_noalloc_limit bytes)";
     default: return "unknown status";
   }
 }
@@ -360,6 +365,11 @@ struct qnet {
 };
 
 namespace {
+int run_layers(const qnet* net, const float* x, int batch, float* logits, char* ws, const size_t* toff,
+               const size_t* woff, int first, int count, hipStream_t s);
+}  // namespace
+
+namespace {
 
 // Workspace plan: every tensor except the input (0) and the last one gets
 // its own 256-byte aligned region, then one region per fp32 conv for its
@@ -552,8 +562,19 @@ int qnet_forward_range(const qnet* net, const float* x, int batch, float* logits
   const size_t need = plan(net, batch, &toff, &woff);
   if (workspace_bytes < need) return QCONV_EWORKSPACE;
   if (need > 0 && !workspace) return QCONV_EINVAL;
-  char* ws = static_cast<char*>(workspace);
-  hipStream_t s = (hipStream_t)stream;
+  return run_layers(net, x, batch, logits, static_cast<char*>(workspace), toff.data(), woff.data(), first, count,
+                    (hipStream_t)stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// The layer loop of qnet_forward over layers [first, first + count), with
+// tensor `id` at ws + toff[id] and the re-laid-out weights of fp32 conv
+// layer i at ws + woff[i] (inputs already validated).
+int run_layers(const qnet* net, const float* x, int batch, float* logits, char* ws, const size_t* toff,
+               const size_t* woff, int first, int count, hipStream_t s) {
   const int last_id = (int)net->t.size() - 1;
   auto ptr = [&](int id) -> void* {
     if (id == 0) return const_cast<float*>(x);
@@ -601,7 +622,7 @@ int qnet_forward_range(const qnet* net, const float* x, int batch, float* logits
         e.out_bits = l.out_bits;
         rc = qconv_forward(&d, static_cast<const uint32_t*>(ptr(l.src)), l.wq, &e,
                            l.out_bits ? nullptr : ptr(dst),
-                           l.out_bits ? static_cast<uint32_t*>(ptr(dst)) : nullptr, stream);
+                           l.out_bits ? static_cast<uint32_t*>(ptr(dst)) : nullptr, s);
         break;
       }
       case L_AVGPOOL:
@@ -621,6 +642,10 @@ int qnet_forward_range(const qnet* net, const float* x, int batch, float* logits
   return QCONV_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
 int qnet_forward(const qnet* net, const float* x, int batch, float* logits, void* workspace,
                  size_t workspace_bytes, void* stream) {
   return qnet_forward_range(net, x, batch, logits, workspace, workspace_bytes, 0, net ? (int)net->L.size() : 0,
@@ -628,5 +653,134 @@ int qnet_forward(const qnet* net, const float* x, int batch, float* logits, void
 }
 
 int qnet_num_layers(const qnet* net) { return net ? (int)net->L.size() : QCONV_EINVAL; }
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Networks without a caller workspace: every intermediate tensor lives in one
+// fixed device array of the library, reused as soon as the layers that read
+// a tensor have run.
+// ---------------------------------------------------------------------------
+
+namespace {
+
+constexpr size_t kScratchBytes = (size_t)QNET_NOALLOC_SCRATCH_MIB << 20;
+constexpr int kScratchTensors = 1024;  // tensors (plus fp32 conv weight regions) a plan can place
+
+// The array itself.  In host code its name is only a stand-in for the
+// symbol: kernels get the device address hipGetSymbolAddress returns.
+__device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+// Device address of `scratch` on each device, looked up once per device.
+std::atomic<uint8_t*> g_scratch_ptr[MAX_DEVICES_API];
+std::mutex g_scratch_mu;
+
+int scratch_ptr(uint8_t** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEVICES_API) return QCONV_EHIP;
+  uint8_t* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      void* sym = nullptr;
+      if (hipGetSymbolAddress(&sym, HIP_SYMBOL(scratch)) != hipSuccess || !sym) return QCONV_EHIP;
+      p = static_cast<uint8_t*>(sym);
+      g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
+  return QCONV_OK;
+}
+
+// Liveness plan: tensor id (made by layer id - 1) stays placed until the last
+// layer that reads it has run; the re-laid-out weights of fp32 conv layer i
+// live during layer i only.  Each region takes the lowest 256-byte aligned
+// offset that overlaps no region still live (first fit over the ends of
+// the live regions).  Writes toff[id] / woff[i] (fixed arrays, no heap) and
+// returns the bytes used, or 0 with *rc set when the network has more
+// regions than the arrays hold.
+size_t liveness_plan(const qnet* net, int batch, size_t* toff, size_t* woff, int* rc) {
+  const int nt = (int)net->t.size(), nl = (int)net->L.size();
+  *rc = QCONV_OK;
+  if (nt + nl > kScratchTensors) {
+    *rc = QCONV_EUNSUPPORTED;
+    return 0;
+  }
+  int last_use[kScratchTensors];
+  for (int id = 0; id < nt; ++id) last_use[id] = id - 1;
+  for (int i = 0; i < nl; ++i) {
+    const QLayer& l = net->L[i];
+    if (last_use[l.src] < i) last_use[l.src] = i;
+    if (l.src2 > 0 && last_use[l.src2] < i) last_use[l.src2] = i;
+  }
+  struct Region {
+    size_t off, end;
+    int until;  // last layer that uses it
+  };
+  Region live[kScratchTensors];
+  int nlive = 0;
+  size_t top = 0;
+  auto place = [&](size_t bytes, int layer, int until) -> size_t {
+    // drop regions whose last use came before this layer
+    int k = 0;
+    for (int j = 0; j < nlive; ++j)
+      if (live[j].until >= layer) live[k++] = live[j];
+    nlive = k;
+    size_t best = (size_t)-1;
+    for (int c = -1; c < nlive; ++c) {
+      const size_t cand = c < 0 ? 0 : align256(live[c].end);
+      bool ok = true;
+      for (int j = 0; j < nlive && ok; ++j) ok = cand + bytes <= live[j].off || cand >= live[j].end;
+      if (ok && cand < best) best = cand;
+    }
+    live[nlive++] = {best, best + bytes, until};
+    if (align256(best + bytes) > top) top = align256(best + bytes);
+    return best;
+  };
+  for (int i = 0; i < nl; ++i) {
+    const QLayer& l = net->L[i];
+    woff[i] = (size_t)-1;
+    if (l.kind == L_CONV_F32) {
+      const int cin = net->t[l.src].c;
+      woff[i] = place((size_t)cin * l.k * l.k * ceil_div(l.cout, 64) * 64 * sizeof(float), i, i);
+    }
+    const int id = i + 1;
+    toff[id] = (size_t)-1;
+    if (id != nt - 1) toff[id] = place(tensor_bytes(net->t[id], batch), i, last_use[id]);
+  }
+  toff[0] = (size_t)-1;
+  return top;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t qnet_noalloc_bytes(const qnet* net, int batch) {
+  if (!net || batch < 0 || net->L.empty()) return 0;
+  size_t toff[kScratchTensors], woff[kScratchTensors];
+  int rc = 0;
+  return liveness_plan(net, batch, toff, woff, &rc);
+}
+
+size_t qnet_noalloc_limit(void) { return kScratchBytes; }
+
+int qnet_forward_noalloc(const qnet* net, const float* x, int batch, float* logits, void* stream) {
+  if (!net || batch < 0 || net->L.empty()) return QCONV_EINVAL;
+  if (batch == 0) return QCONV_OK;
+  if (!x || !logits) return QCONV_EINVAL;
+  if (net->t.back().bits != 0) return QCONV_EUNSUPPORTED;
+  size_t toff[kScratchTensors], woff[kScratchTensors];
+  int rc = 0;
+  const size_t need = liveness_plan(net, batch, toff, woff, &rc);
+  if (rc) return rc;
+  if (need > kScratchBytes) return QCONV_ESCRATCH;
+  uint8_t* base = nullptr;
+  rc = scratch_ptr(&base);
+  if (rc) return rc;
+  return run_layers(net, x, batch, logits, reinterpret_cast<char*>(base), toff, woff, 0, (int)net->L.size(),
+                    (hipStream_t)stream);
+}
 
 }  // extern "C"
