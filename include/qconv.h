@@ -305,7 +305,11 @@ int qnet_add_conv_f32(qnet* net, int src, const float* w, int cout, int k, int s
 /* fp32 k x k / stride max pooling with padding (padding never wins). */
 int qnet_add_maxpool_f32(qnet* net, int src, int k, int stride, int pad);
 
-/* Quantize + pack an fp32 tensor with the default activation thresholds. */
+/* Quantize + pack an fp32 tensor with the default activation thresholds.
+ * When src is the fp32 output of a qnet_add_qconv layer (out_bits 0, with or
+ * without a residual) and no other quantize layer was folded into it yet,
+ * that conv's epilogue writes this tensor as well (Algorithm 1: a_l^q =
+ * h(a_l) right after the layer) and this layer launches nothing. */
 int qnet_add_quantize(qnet* net, int src, int bits);
 
 /* Quantized conv on a packed tensor with a BN epilogue (w_bits 1..3, or 16

@@ -320,7 +320,15 @@ class Net:
                          src=src, k=k, stride=stride, pad=pad)
 
     def quantize(self, src, bits):
-        return self._add(lib().qnet_add_quantize(self._h, src, bits), "qnet_add_quantize", src=src, out_bits=bits)
+        # the library folds Q(x) of a quantized conv's fp32 output into that
+        # conv's epilogue (qnet_add_quantize); recorded here for reports
+        prod = next((L for L in self.layers if L["dst"] == src), None)
+        fused = bool(prod and prod["kind"] == "qconv" and prod["out_bits"] == 0 and not prod.get("pack_dst"))
+        tid = self._add(lib().qnet_add_quantize(self._h, src, bits), "qnet_add_quantize", src=src, out_bits=bits,
+                        fused_into=prod["dst"] - 1 if fused else None)
+        if fused:
+            prod["pack_dst"] = tid
+        return tid
 
     def qconv(self, src, w_packed, cout, k, stride, pad, w_bits, bn_k, bn_b, pool2=False, residual_src=-1,
               out_bits=0):

@@ -348,6 +348,10 @@ struct QLayer {
   const float* bn_b = nullptr;
   const float* bias = nullptr;
   int cout = 0, k = 0, stride = 1, pad = 0, w_bits = 0, pool2 = 0, relu = 0, out_bits = 0;
+  // a quantized conv with an fp32 output also writes tensor pack_dst, the
+  // packed Q(HardTanh(z)) of its output, from the same epilogue; the
+  // quantize layer that made that tensor is then `fused` and launches nothing
+  int pack_dst = -1, fused = 0;
 };
 
 size_t tensor_bytes(const QTensor& t, int batch) {
@@ -463,6 +467,16 @@ int qnet_add_quantize(qnet* net, int src, int bits) {
   l.kind = L_QUANTIZE;
   l.src = src;
   l.out_bits = bits;
+  // Q(x) of a quantized conv's fp32 output comes out of that conv's own
+  // epilogue (Algorithm 1: a_l^q = h(a_l) right after the layer), as the
+  // packed Q(HardTanh(z)); with the default thresholds (all below 1)
+  // HardTanh changes no level, so the bits are those of Q(x)
+  QLayer& prod = net->L[src - 1 >= 0 ? src - 1 : 0];
+  const int id = (int)net->t.size();
+  if (src > 0 && prod.kind == L_QCONV && prod.out_bits == 0 && prod.pack_dst < 0) {
+    prod.pack_dst = id;
+    l.fused = 1;
+  }
   return add_tensor(net, l, {s.c, s.h, s.w, bits});
 }
 
@@ -606,6 +620,7 @@ int run_layers(const qnet* net, const float* x, int batch, float* logits, char* 
                                 l.k, l.stride, l.pad, static_cast<float*>(ptr(dst)), s);
         break;
       case L_QUANTIZE:
+        if (l.fused) break;  // written by the epilogue of the conv that made its source
         rc = launch_pack_act(static_cast<const float*>(ptr(l.src)), batch, si.c, si.h, si.w,
                              l.out_bits, dflt[l.out_bits], static_cast<uint32_t*>(ptr(dst)), s);
         break;
@@ -620,9 +635,13 @@ int run_layers(const qnet* net, const float* x, int batch, float* logits, char* 
         e.bn_b = l.bn_b;
         e.residual = l.src2 > 0 ? static_cast<const float*>(ptr(l.src2)) : nullptr;
         e.out_bits = l.out_bits;
+        uint32_t* packed = l.out_bits ? static_cast<uint32_t*>(ptr(dst)) : nullptr;
+        if (l.pack_dst > 0) {
+          packed = static_cast<uint32_t*>(ptr(l.pack_dst));
+          e.out_bits = net->t[l.pack_dst].bits;
+        }
         rc = qconv_forward(&d, static_cast<const uint32_t*>(ptr(l.src)), l.wq, &e,
-                           l.out_bits ? nullptr : ptr(dst),
-                           l.out_bits ? static_cast<uint32_t*>(ptr(dst)) : nullptr, s);
+                           l.out_bits ? nullptr : ptr(dst), packed, s);
         break;
       }
       case L_AVGPOOL:
@@ -746,8 +765,10 @@ size_t liveness_plan(const qnet* net, int batch, size_t* toff, size_t* woff, int
       woff[i] = place((size_t)cin * l.k * l.k * ceil_div(l.cout, 64) * 64 * sizeof(float), i, i);
     }
     const int id = i + 1;
+    if (l.kind == L_QUANTIZE && l.fused) continue;  // placed with the conv that writes it
     toff[id] = (size_t)-1;
     if (id != nt - 1) toff[id] = place(tensor_bytes(net->t[id], batch), i, last_use[id]);
+    if (l.pack_dst > 0) toff[l.pack_dst] = place(tensor_bytes(net->t[l.pack_dst], batch), i, last_use[l.pack_dst]);
   }
   toff[0] = (size_t)-1;
   return top;

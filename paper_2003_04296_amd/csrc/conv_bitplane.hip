@@ -11,6 +11,10 @@
 // the pairs with equal e_j + e_r are merged first (the masks are disjoint
 // because magnitudes are one-hot), which gives five shift classes.
 //
+// This kernel serves every bitplane layer the LDS-tiled XNOR kernel
+// (conv_xnor.hip) does not: 3-bit operands (SHIFT), packed or pooled
+// outputs, other kernel sizes and strides.
+//
 // Work mapping: one lane = one output pixel (or one 2x2 pooling window,
 // walked pixel by pixel), one wave = TN consecutive output channels, so the
 // weight words of a (tap, word) step are wave-uniform and come in through
@@ -254,6 +258,7 @@ int launch_pp(const ConvArgs& a, hipStream_t s) {
 }  // namespace
 
 int bitplane_kernel_name(const ConvArgs& a, char* buf, int len) {
+  if (xnor_supports(a)) return xnor_kernel_name(a, buf, len);
   const int pa = planes_of(a.a_bits), pw = planes_of(a.w_bits);
   int tn = 0;
 #define QC_CASE(A, W) \
@@ -276,6 +281,7 @@ int bitplane_kernel_name(const ConvArgs& a, char* buf, int len) {
 }
 
 int launch_conv_bitplane(const ConvArgs& a, hipStream_t s) {
+  if (xnor_supports(a)) return launch_conv_xnor(a, s);
   const int pa = planes_of(a.a_bits), pw = planes_of(a.w_bits);
 #define QC_CASE(A, W) \
   if (pa == A && pw == W) return launch_pp<A, W>(a, s);

@@ -1221,7 +1221,7 @@ constexpr int PP_GROUP = 512;  // threads per wave group
 // buffer per group.  Serves unpacked, unpooled outputs (pixels as the A
 // operand, so that a lane holds one channel); needs a single channel chunk
 // and packed activations below 2 GiB.
-template <int OPK, int PA, int CFG>
+template <int OPK, int PA, int CFG, int OB>
 __global__ __launch_bounds__(1024, 1) void conv_mfma_pp_kernel(const MfmaArgs m) {
   using O = OpT<OPK>;
   using acc_t = typename O::acc_t;
@@ -1399,6 +1399,11 @@ __global__ __launch_bounds__(1024, 1) void conv_mfma_pp_kernel(const MfmaArgs m)
     const bool st = k >= 1 && co_w < a.cout;
     int pimg0 = 0, pu0 = 0;
     if (st) item_units(m, item_w(k - 1), &pimg0, &pu0);
+    // BN tiles (OB > 0: with the packed Q(HardTanh(z)) of the next layer)
+    auto bn_tile = [&](auto RESC, const acc_t& A, int T, int co32, const float(*pre)[16])
+                       __attribute__((always_inline)) {
+      tile_epilogue_swap<K_BNF32, decltype(RESC)::value, OB>(m, A, pimg0, pu0, T, co32, co_blk, prm, plane, pre);
+    };
     if (a.mode == QCONV_EPI_BN_F32 && a.residual_on) {
       // residual layers: the residual values of tile t + 1 are loaded before
       // the stores of tile t, so no load waits for the stores of its own tile
@@ -1412,8 +1417,7 @@ __global__ __launch_bounds__(1024, 1) void conv_mfma_pp_kernel(const MfmaArgs m)
           constexpr int i1 = (TT + 1) / NT, j1 = (TT + 1) % NT;
           if (st && co_w + 32 * j1 < a.cout) swap_res_load(m, pimg0, pu0, wm * MT + i1, co_w + 32 * j1, plane, rnext);
         }
-        if (st && co32 < a.cout)
-          tile_epilogue_swap<K_BNF32, 1>(m, acc[i][j], pimg0, pu0, wm * MT + i, co32, co_blk, prm, plane, &rcur);
+        if (st && co32 < a.cout) bn_tile(std::integral_constant<int, 1>{}, acc[i][j], wm * MT + i, co32, &rcur);
         if constexpr (TT + 1 < MT * NT) {
 #pragma unroll
           for (int v = 0; v < 16; ++v) rcur[v] = rnext[v];
@@ -1432,7 +1436,7 @@ __global__ __launch_bounds__(1024, 1) void conv_mfma_pp_kernel(const MfmaArgs m)
           else if (a.mode == QCONV_EPI_SCALE_F32)
             tile_epilogue_swap<K_SCALE, 0>(m, acc[i][j], pimg0, pu0, T, co32, co_blk, prm, plane);
           else
-            tile_epilogue_swap<K_BNF32, 0>(m, acc[i][j], pimg0, pu0, T, co32, co_blk, prm, plane);
+            bn_tile(std::integral_constant<int, 0>{}, acc[i][j], T, co32, nullptr);
         }
         if constexpr (TT < NI) expand_one(std::integral_constant<int, TT>{});
       });
@@ -1510,7 +1514,12 @@ int launch_cfg(MfmaArgs m, hipStream_t s) {
       const size_t plds = pp_lds(m, CFG);
       // every block keeps one output-channel tile: a multiple of tiles_co blocks
       m.grid = max(m.tiles_co, (min(total, cus) / m.tiles_co) * m.tiles_co);
-      auto kern = conv_mfma_pp_kernel<OPK, PA, CFG>;
+      // OB: the bits of a packed copy of a BN output; one width per input
+      // width (the one a network of that width asks for), others are refused
+      // by use_pp
+      constexpr int OB_NET = PA == 1 ? 1 : (PA == 2 ? 2 : 3);
+      auto kern = conv_mfma_pp_kernel<OPK, PA, CFG, 0>;
+      if (m.c.out_packed) kern = conv_mfma_pp_kernel<OPK, PA, CFG, OB_NET>;
       // the dynamic-LDS limit of this instantiation, raised once per device
       static std::atomic<int> lds_set[MAX_DEVICES];
       int dev = 0;

@@ -195,7 +195,10 @@ size_t pp_lds(const MfmaArgs& m, int cfg) {
 // buffers, when every block gets at least one item per group.
 bool use_pp(const MfmaArgs& m, int cfg, int cus) {
   if (cfg == 2 || m.c.mfma_op == OP_F16 || !use_swap(m) || m.nchunks != 1 || m.act_bytes == 0) return false;
-  if (m.c.out_packed != nullptr || m.c.mode == QCONV_EPI_BN_PACK) return false;  // unpacked outputs only
+  // unpacked outputs; a packed copy of a BN output rides along when its
+  // width is the input's (the case of a network of one activation width)
+  if (m.c.mode == QCONV_EPI_BN_PACK) return false;
+  if (m.c.out_packed != nullptr && (m.c.mode != QCONV_EPI_BN_F32 || m.c.out_bits != m.c.a_bits)) return false;
   if (pp_lds(m, cfg) > (size_t)LDS_PER_CU) return false;
   return (int64_t)m.tiles_px * m.tiles_co >= 2 * (int64_t)cus;
 }
@@ -217,7 +220,8 @@ int mfma_kernel_name(const ConvArgs& a, char* buf, int len) {
   if (!plan(a, cfg, &m)) return QCONV_EUNSUPPORTED;
   char name[96];
   if (use_pp(m, cfg, device_cus()))
-    snprintf(name, sizeof(name), "conv_mfma_pp_kernel<%d, %d, %d>", a.mfma_op, act_words(a.a_bits), cfg);
+    snprintf(name, sizeof(name), "conv_mfma_pp_kernel<%d, %d, %d, %d>", a.mfma_op, act_words(a.a_bits), cfg,
+             a.out_packed ? a.out_bits : 0);
   else
     snprintf(name, sizeof(name), "conv_mfma_kernel<%d, %d, %d, %d>", a.mfma_op, act_words(a.a_bits), cfg,
              use_swap(m) ? 1 : 0);

@@ -54,6 +54,54 @@ __global__ __launch_bounds__(256) void pack_act_kernel(const float* __restrict__
   for (int p = 0; p < P; ++p) dst[p] = word[p];
 }
 
+// The same quantizer with the packed words staged in LDS: a block owns 64
+// pixels of one image and every word of them; wave w computes words w,
+// w + 4, ... with lanes along the pixels (each channel read one contiguous
+// 256-byte run), then the block writes the 64 pixels' words as one
+// contiguous run (the per-thread stores of pack_act_kernel land 4 * P bytes
+// apart and write each HBM sector twice).
+constexpr int PACK_PIX = 64;
+template <int BITS>
+__global__ __launch_bounds__(256) void pack_act_lds_kernel(const float* __restrict__ x, int c, int hw, int cwn,
+                                                           int chunks, Thr t, uint32_t* __restrict__ out) {
+  constexpr int P = planes_of(BITS);
+  extern __shared__ uint32_t tile[];  // [PACK_PIX][cwn][P]
+  const int b = blockIdx.x / chunks;
+  const int pix0 = (blockIdx.x - b * chunks) * PACK_PIX;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int pix = pix0 + lane;
+  const bool pok = pix < hw;
+  for (int cw = wave; cw < cwn; cw += 4) {
+    const int c0 = cw * 32;
+    const int nch = min(32, c - c0);
+    const float* src = x + ((int64_t)b * c + c0) * hw + (pok ? pix : 0);
+    uint32_t word[P];
+#pragma unroll
+    for (int p = 0; p < P; ++p) word[p] = 0u;
+    if (nch == 32) {
+#pragma unroll 8
+      for (int j = 0; j < 32; ++j) {
+        const uint32_t pl = quant_planes<BITS>(src[(int64_t)j * hw], t);
+#pragma unroll
+        for (int p = 0; p < P; ++p) word[p] |= ((pl >> p) & 1u) << j;
+      }
+    } else {
+      for (int j = 0; j < nch; ++j) {
+        const uint32_t pl = quant_planes<BITS>(src[(int64_t)j * hw], t);
+#pragma unroll
+        for (int p = 0; p < P; ++p) word[p] |= ((pl >> p) & 1u) << j;
+      }
+    }
+#pragma unroll
+    for (int p = 0; p < P; ++p) tile[(lane * cwn + cw) * P + p] = word[p];
+  }
+  __syncthreads();
+  const int npix = min(PACK_PIX, hw - pix0);
+  const int nwords = npix * cwn * P;
+  uint32_t* dst = out + ((int64_t)b * hw + pix0) * cwn * P;
+  for (int i = threadIdx.x; i < nwords; i += 256) dst[i] = tile[i];
+}
+
 __global__ __launch_bounds__(256) void pack_act_f16_kernel(const float* __restrict__ x, int c, int hw, int cwn,
                                                            int64_t total, uint32_t* __restrict__ out) {
   const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -259,6 +307,18 @@ int launch_pack_act(const float* x, int n, int c, int h, int w, int bits, Thr t,
   const int cwn = ceil_div(c, 32);
   const int64_t total = (int64_t)n * cwn * hw;
   if (total == 0) return QCONV_OK;
+  const size_t lds = (size_t)PACK_PIX * cwn * planes_of(bits) * sizeof(uint32_t);
+  if (lds <= 32 * 1024) {
+    const int chunks = ceil_div(hw, PACK_PIX);
+    const dim3 g((unsigned)((int64_t)n * chunks));
+    switch (bits) {
+      case 1: pack_act_lds_kernel<1><<<g, 256, lds, s>>>(x, c, hw, cwn, chunks, t, out); break;
+      case 2: pack_act_lds_kernel<2><<<g, 256, lds, s>>>(x, c, hw, cwn, chunks, t, out); break;
+      default: pack_act_lds_kernel<3><<<g, 256, lds, s>>>(x, c, hw, cwn, chunks, t, out); break;
+    }
+    return hip_status();
+  }
+  // very wide tensors (more than 32 KB of words per 64 pixels): one thread per word
   const dim3 grid((unsigned)((total + 255) / 256));
   switch (bits) {
     case 1: pack_act_kernel<1><<<grid, 256, 0, s>>>(x, c, hw, cwn, total, t, out); break;

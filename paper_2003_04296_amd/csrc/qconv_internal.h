@@ -188,6 +188,11 @@ struct ConvArgs {
 };
 enum MfmaOp { OP_I8 = 0, OP_FP4 = 1, OP_F16 = 2 };
 int launch_conv_bitplane(const ConvArgs& a, hipStream_t s);
+// The LDS-tiled XNOR kernel (1-2 bit operands, 1x1 / 3x3, stride 1-2,
+// unpacked unpooled outputs); launch_conv_bitplane runs it when it applies.
+bool xnor_supports(const ConvArgs& a);
+int launch_conv_xnor(const ConvArgs& a, hipStream_t s);
+int xnor_kernel_name(const ConvArgs& a, char* buf, int len);
 int launch_conv_mfma(const ConvArgs& a, hipStream_t s);
 bool mfma_supports(const ConvArgs& a);
 // Name of the kernel instantiation each launcher would run (template

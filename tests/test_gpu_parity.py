@@ -227,6 +227,62 @@ def test_bn_residual_and_repack(dev, bits, algo, hw):
 
 
 # ---------------------------------------------------------------------------
+# the LDS-tiled XNOR kernel: 1- and 2-bit operands, 1x1 / 3x3, stride 1 / 2,
+# unpacked outputs; its K split across 1, 2 or 4 lanes follows the layer size
+# ---------------------------------------------------------------------------
+
+XNOR_CASES = [
+    # n, cin, h, w, cout, k, stride, pad
+    (64, 64, 56, 56, 128, 1, 2, 0),   # ResNet-18 shortcut shape: 1024 blocks
+    (16, 128, 32, 32, 128, 3, 1, 1),  # 512 blocks of 64 channels
+    (4, 128, 32, 32, 128, 3, 1, 1),   # the 1W1A workload's shape: 256 blocks of 32 channels
+    (3, 520, 9, 11, 70, 3, 1, 1),     # several staged chunks of words, ragged tiles and channels
+    (2, 33, 30, 30, 40, 3, 2, 1),     # stride 2 with odd halo columns, ragged last word
+    (5, 96, 7, 7, 300, 1, 1, 0),      # 1x1 stride 1, three channel tiles
+]
+
+
+def _expected_ks(case):
+    n, cin, h, w, cout, k, s, p = case
+    ho, wo = (h + 2 * p - k) // s + 1, (w + 2 * p - k) // s + 1
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    for ks in (1, 2, 4):
+        if n * -(-ho // 8) * -(-wo // 8) * -(-cout // (128 // ks)) >= 2 * cus:
+            return ks
+    return 4
+
+
+@pytest.mark.parametrize("bits", [(1, 1), (2, 1), (1, 2), (2, 2)])
+@pytest.mark.parametrize("case", XNOR_CASES)
+def test_xnor_kernel(dev, case, bits):
+    n, cin, h, w, cout, k, s, p = case
+    ab, wb = bits
+    name = q.kernel_name(n, cin, h, w, cout, k, s, p, ab, wb, algo=q.ALGO_BITPLANE)
+    assert name == f"conv_xnor_kernel<{ab}, {wb}, {_expected_ks(case)}>", name
+    x, wt = _inputs(900 + sum(case) + ab, n, cin, h, w, cout, k)
+    kk, bb = _bn(900 + cin, cout)
+    ho, wo = q.out_size(h, k, s, p), q.out_size(w, k, s, p)
+    res = synth.normal(synth.generator(901), (n, cout, ho, wo), 1.0)
+    act = q.pack_act(x.to(dev), ab)
+    wq, scale = q.pack_weight(wt.to(dev), wb)
+    conv = lambda **kw: q.conv(act, wq, n, cin, h, w, cout, k, s, p, ab, wb, algo=q.ALGO_BITPLANE, **kw)[0]
+    acc = conv()
+    sc = conv(mode=q.EPI_SCALE_F32, scale=scale)
+    z = conv(mode=q.EPI_BN_F32, bn_k=kk.to(dev), bn_b=bb.to(dev))
+    zr = conv(mode=q.EPI_BN_F32, flags=q.EPI_RESIDUAL, bn_k=kk.to(dev), bn_b=bb.to(dev), residual=res.to(dev))
+    torch.cuda.synchronize()
+    want, s_c = _oracle_acc(x, wt, ab, wb, s, p)
+    np.testing.assert_array_equal(acc.cpu().numpy(), want)
+    np.testing.assert_array_equal(sc.cpu().numpy(), oracle.epi_scale(want, s_c))
+    zw = oracle.epi_bn(want, kk.numpy(), bb.numpy())
+    np.testing.assert_array_equal(z.cpu().numpy(), zw)
+    np.testing.assert_array_equal(zr.cpu().numpy(), oracle.add(zw, res.numpy()))
+    # the matrix cores give the same bits
+    other, _ = _run_or_skip(lambda: q.conv(act, wq, n, cin, h, w, cout, k, s, p, ab, wb, algo=q.ALGO_MFMA_FP4))
+    assert torch.equal(other, acc)
+
+
+# ---------------------------------------------------------------------------
 # 256-row x 64-channel blocks on layers whose 128-channel blocks would leave
 # compute units idle while the 64-channel ones give every CU one
 # ---------------------------------------------------------------------------
@@ -341,6 +397,41 @@ def test_pp_kernel_epilogues(dev, ci, epi):
         if flags:
             want = oracle.add(want, res.numpy())
     np.testing.assert_array_equal(out.cpu().numpy(), want)
+
+
+@pytest.mark.parametrize("bits", [(2, 1), (1, 1), (3, 3), (2, 2)])
+@pytest.mark.parametrize("ci", [0, 1, 3])
+@pytest.mark.parametrize("resid", [False, True])
+def test_pp_kernel_packed_copy(dev, ci, bits, resid):
+    """BN (+ residual) fp32 output with the packed Q(HardTanh(z)) of the next
+    layer from the same store phase (a network's residual block output and
+    the next block's quantized input)."""
+    case = PP_CASES[ci]
+    n, cin, h, w, cout, k, s, p = case
+    ab, wb = bits
+    flags = q.EPI_RESIDUAL if resid else 0
+    name = q.kernel_name(n, cin, h, w, cout, k, s, p, ab, wb, mode=q.EPI_BN_F32, flags=flags, out_bits=ab,
+                         packed_out=True)
+    assert name.startswith("conv_mfma_pp_kernel<1,") and name.endswith(f", {ab}>"), name
+    x, wt = _inputs(340 + ci + ab, n, cin, h, w, cout, k)
+    kk, bb = _bn(340 + ci, cout)
+    ho, wo = q.out_size(h, k, s, p), q.out_size(w, k, s, p)
+    res = synth.normal(synth.generator(341 + ci), (n, cout, ho, wo), 1.0)
+    act = q.pack_act(x.to(dev), ab)
+    wq, _ = q.pack_weight(wt.to(dev), wb)
+    outp = torch.empty(q.packed_act_words(n, cout, ho, wo, ab), dtype=torch.int32, device=dev)
+    out, _ = q.conv(act, wq, n, cin, h, w, cout, k, s, p, ab, wb, mode=q.EPI_BN_F32, flags=flags,
+                    bn_k=kk.to(dev), bn_b=bb.to(dev), residual=res.to(dev) if resid else None, out_bits=ab,
+                    out_packed=outp)
+    torch.cuda.synchronize()
+    acc, _ = _oracle_acc(x, wt, ab, wb, s, p)
+    z = oracle.epi_bn(acc, kk.numpy(), bb.numpy(), oracle.level_shift(ab) + oracle.level_shift(wb))
+    if resid:
+        z = oracle.add(z, res.numpy())
+    np.testing.assert_array_equal(out.cpu().numpy(), z)
+    np.testing.assert_array_equal(unpack_act(outp.cpu().numpy(), n, cout, ho, wo, ab),
+                                  oracle.quantize(oracle.hardtanh(z), ab))
+    assert tail_bits_zero(outp.cpu().numpy(), cout, ab)
 
 
 def test_pp_kernel_repeated_launches_agree(dev):
