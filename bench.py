@@ -359,8 +359,9 @@ def conv_entry(case, mode, dev, stream, steps, warmup, algo, cpu, out_bits=0, cp
 
 
 def layer_work(net, li, batch, dev):
-    """(ops, algorithmic bytes, compute peak GOPS, bound name, kernel label) of
-    layer li of a qnet."""
+    """(ops, algorithmic bytes, compute peak GOPS, bound name, kernel name) of
+    layer li of a qnet; the bytes of tensors a layer's epilogue writes for
+    later (folded) layers count as its output."""
     L = net.layers[li]
     kind = L["kind"]
     ci, hi, wi, bi, _ = net.tensor_info(L["src"], batch)
@@ -368,10 +369,18 @@ def layer_work(net, li, batch, dev):
     n = batch
     bin_ = packed_bytes(n, ci, hi, wi, bi)
     bout = packed_bytes(n, co, ho, wo, bo)
+    kname = net.layer_kernel(li, batch)
+    extra = 0
+    for key in ("pool_dst", "pack_dst"):
+        if L.get(key):
+            pc, ph, pw, pb, _ = net.tensor_info(L[key], batch)
+            extra += packed_bytes(n, pc, ph, pw, pb)
+    if L.get("pool_dst"):
+        bout = 0  # the unpooled output is never written
     if kind == "conv_f32":
         k = L["k"]
         ops = 2.0 * n * co * ho * wo * ci * k * k
-        return ops, bin_ + co * ci * k * k * 4 + bout, FP32_PEAK_GOPS, "fp32", "conv_f32_kernel"
+        return ops, bin_ + co * ci * k * k * 4 + bout + extra, FP32_PEAK_GOPS, "fp32", kname
     if kind == "qconv":
         k, s, p = L["k"], L["stride"], L["pad"]
         hc, wc = q.out_size(hi, k, s, p), q.out_size(wi, k, s, p)
@@ -379,14 +388,9 @@ def layer_work(net, li, batch, dev):
         mode = q.EPI_BN_PACK if L["out_bits"] else q.EPI_BN_F32
         flags = (q.EPI_POOL2 if L["pool2"] else 0) | (q.EPI_RESIDUAL if L["residual_src"] > 0 else 0)
         ob = L["out_bits"]
-        extra = 0
         if L.get("pack_dst"):  # a folded quantize layer: the packed copy of the fp32 output
-            pc, ph, pw, pb, _ = net.tensor_info(L["pack_dst"], batch)
-            ob = pb
-            extra = packed_bytes(n, pc, ph, pw, pb)
+            ob = net.tensor_info(L["pack_dst"], batch)[3]
         used = q.ALGO_NAMES[q.resolve_algo(n, ci, hi, wi, co, k, s, p, bi, L["w_bits"], mode, flags, ob)]
-        kname = q.kernel_name(n, ci, hi, wi, co, k, s, p, bi, L["w_bits"], mode=mode, flags=flags,
-                              out_bits=ob, packed_out=bool(ob))
         nb = bin_ + weight_operand_bytes(co, ci, k, used, L["w_bits"]) + bout + extra
         if L["residual_src"] > 0:
             nb += bout
@@ -394,10 +398,8 @@ def layer_work(net, li, batch, dev):
         return ops, nb, peak, cb, kname
     if kind == "fc_f32":
         fin = ci * hi * wi
-        return 2.0 * n * fin * co, bin_ + fin * co * 4 + bout, FP32_PEAK_GOPS, "fp32", "fc_f32_kernel"
-    names = {"maxpool_f32": "maxpool_f32_kernel", "quantize": f"pack_act_lds_kernel<{bo}>",
-             "avgpool": "avgpool_f32_kernel"}
-    return 0.0, bin_ + bout, None, "hbm", names.get(kind, kind)
+        return 2.0 * n * fin * co, bin_ + fin * co * 4 + bout, FP32_PEAK_GOPS, "fp32", kname
+    return 0.0, bin_ + bout, None, "hbm", kname
 
 
 def net_entry(wl, dev, stream, steps, warmup, cpu, cpu_budget=8.0):

@@ -295,14 +295,31 @@ typedef struct qnet qnet;
 qnet* qnet_create(int in_c, int in_h, int in_w);
 void qnet_destroy(qnet* net);
 
-/* fp32 conv (zero padding, each output one fmaf chain over (ci, kh, kw)),
- * then z = fmaf(k, conv, b), then ReLU if relu != 0; out_bits == 0 keeps z as
- * fp32 NCHW, out_bits 1..3 quantizes HardTanh(z) and packs it.
- * w: fp32 [cout][cin][k][k]. */
+/* Arithmetic of the network's fp32 convolutions (call before adding
+ * layers; returns QCONV_EINVAL afterwards):
+ *   QNET_F32_MFMA (default): the fp32 matrix cores sum each output in their
+ *     own order (results within fp32 rounding of the chain below); a 3x3 / 2
+ *     max pooling (pad 1) of such a conv's output, and the quantize of
+ *     either, run in the conv's epilogue.  Layers the matrix-core kernel
+ *     does not fit (its LDS holds the input window, cin * k * k weights of
+ *     32 channels and a pooled tile) fall back to the chain.
+ *   QNET_F32_FMAF_CHAIN: each output one fmaf chain over (ci, kh, kw) from
+ *     +0, a fixed order that makes networks reproducible bit for bit. */
+enum { QNET_F32_FMAF_CHAIN = 0, QNET_F32_MFMA = 1 };
+int qnet_set_f32_algo(qnet* net, int algo);
+
+/* fp32 conv (zero padding; the sum over (ci, kh, kw) as qnet_set_f32_algo
+ * says), then z = fmaf(k, conv, b), then ReLU if relu != 0; out_bits == 0
+ * keeps z as fp32 NCHW, out_bits 1..3 quantizes HardTanh(z) and packs it.
+ * w: fp32 [cout][cin][k][k], read directly by the matrix-core kernel. */
 int qnet_add_conv_f32(qnet* net, int src, const float* w, int cout, int k, int stride, int pad,
                       const float* bn_k, const float* bn_b, int relu, int out_bits);
 
-/* fp32 k x k / stride max pooling with padding (padding never wins). */
+/* fp32 k x k / stride max pooling with padding (padding never wins; the
+ * window is scanned row by row and only a strictly greater value replaces
+ * the running maximum).  3 x 3 / 2 with pad 1 right after a matrix-core fp32
+ * conv with an fp32 output runs in that conv's epilogue (the conv's own
+ * unpooled tensor is then never written). */
 int qnet_add_maxpool_f32(qnet* net, int src, int k, int stride, int pad);
 
 /* Quantize + pack an fp32 tensor with the default activation thresholds.
@@ -349,6 +366,18 @@ int qnet_forward_range(const qnet* net, const float* x, int batch, float* logits
 
 /* Number of layers added so far (negative status for a NULL network). */
 int qnet_num_layers(const qnet* net);
+
+/* The layer whose launch writes the tensor of layer `layer`: an earlier
+ * layer when its epilogue takes over a folded quantize or max pooling (which
+ * then launches nothing), else `layer` itself.  Negative status for a NULL
+ * network or a layer index out of range. */
+int qnet_layer_fused_into(const qnet* net, int layer);
+
+/* Name of the main GPU kernel layer `layer` launches for `batch` images, as
+ * a profiler shows it (an empty string for a layer written by an earlier
+ * layer's epilogue); returns the name's length or a negative status.
+ * Launches nothing. */
+int qnet_layer_kernel(const qnet* net, int layer, int batch, char* buf, int len);
 
 /* ------------------------------------------------------------------------ */
 /* Networks without a workspace, for callers that cannot allocate device     */

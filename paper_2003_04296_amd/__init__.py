@@ -18,6 +18,7 @@ QCONV_ESCRATCH = -6
 ALGO_AUTO, ALGO_BITPLANE, ALGO_MFMA_I8, ALGO_MFMA_FP4, ALGO_MFMA_F16 = 0, 1, 2, 3, 4
 EPI_INT32, EPI_SCALE_F32, EPI_BN_F32, EPI_BN_PACK = 0, 1, 2, 3
 EPI_POOL2, EPI_RESIDUAL = 1, 2
+F32_FMAF_CHAIN, F32_MFMA = 0, 1
 OP_NAMES = {1: "XNOR", 2: "SHIFT", 3: "XNOR-ADDER", 4: "SHIFT-ADDER", 5: "MAC"}
 
 EXPORTED = (
@@ -26,7 +27,8 @@ EXPORTED = (
     "qconv_out_size", "qconv_forward", "qnet_create", "qnet_destroy", "qnet_add_conv_f32",
     "qnet_add_maxpool_f32", "qnet_add_quantize", "qnet_add_qconv", "qnet_add_avgpool",
     "qnet_add_fc_f32", "qnet_workspace_bytes", "qnet_forward", "qnet_forward_range", "qnet_num_layers",
-    "qnet_forward_noalloc", "qnet_noalloc_bytes", "qnet_noalloc_limit",
+    "qnet_forward_noalloc", "qnet_noalloc_bytes", "qnet_noalloc_limit", "qnet_set_f32_algo", "qnet_layer_fused_into",
+    "qnet_layer_kernel",
     "qnet_tensor_info", "qconv_resolve_algo",
     "qconv_kernel_name", "aqe_forward", "aqe_backward", "aqe_sgd_clip",
 )
@@ -107,6 +109,9 @@ def lib() -> ctypes.CDLL:
     L.qnet_noalloc_bytes.argtypes = [vp, i32]
     L.qnet_noalloc_limit.restype = sz
     L.qnet_noalloc_limit.argtypes = []
+    L.qnet_set_f32_algo.argtypes = [vp, i32]
+    L.qnet_layer_fused_into.argtypes = [vp, i32]
+    L.qnet_layer_kernel.argtypes = [vp, i32, i32, ctypes.c_char_p, i32]
     L.qnet_tensor_info.argtypes = [vp, i32, i32] + [ctypes.POINTER(i32)] * 4 + [ctypes.POINTER(sz)]
     _lib = L
     return L
@@ -291,10 +296,12 @@ def kernel_name(n, cin, h, w, cout, k, stride, pad, a_bits, w_bits, mode=EPI_INT
 class Net:
     """A qnet layer list (tensor ids as in include/qconv.h)."""
 
-    def __init__(self, in_c: int, in_h: int, in_w: int):
+    def __init__(self, in_c: int, in_h: int, in_w: int, f32_algo: int = F32_MFMA):
         self._h = lib().qnet_create(in_c, in_h, in_w)
         if not self._h:
             raise QconvError(QCONV_EINVAL, "qnet_create")
+        _check(lib().qnet_set_f32_algo(self._h, int(f32_algo)), "qnet_set_f32_algo")
+        self.f32_algo = f32_algo
         self._keep = []  # device tensors the layers point at
         self.layers = []  # per layer: what was added (kind, source, parameters), for reports
 
@@ -309,6 +316,29 @@ class Net:
         self.layers.append(dict(kind=what.replace("qnet_add_", ""), dst=tid, **info))
         return tid
 
+    def fused_into(self, layer):
+        """The earlier layer whose epilogue writes layer `layer`'s tensor, or None."""
+        if layer < 0:
+            return None
+        r = _check(lib().qnet_layer_fused_into(self._h, layer), "qnet_layer_fused_into")
+        return None if r == layer else r
+
+    def layer_kernel(self, layer, batch):
+        """The GPU kernel layer `layer` launches ("" when an earlier layer writes its tensor)."""
+        buf = ctypes.create_string_buffer(128)
+        _check(lib().qnet_layer_kernel(self._h, layer, batch, buf, 128), "qnet_layer_kernel")
+        return buf.value.decode()
+
+    def _mark_fused(self, tid):
+        """Record (for reports) which layer writes the tensor a layer just added."""
+        li = tid - 1
+        prod = self.fused_into(li)
+        self.layers[li]["fused_into"] = prod
+        if prod is not None:
+            key = "pool_dst" if self.layers[li]["kind"] == "maxpool_f32" else "pack_dst"
+            self.layers[prod][key] = tid
+        return tid
+
     def conv_f32(self, src, w, bn_k, bn_b, stride=1, pad=0, relu=False, out_bits=0):
         cout, _, k, _ = w.shape
         return self._add(lib().qnet_add_conv_f32(self._h, src, _ptr(w), cout, k, stride, pad, _ptr(bn_k), _ptr(bn_b),
@@ -316,19 +346,12 @@ class Net:
                          src=src, cout=cout, k=k, stride=stride, pad=pad, out_bits=out_bits)
 
     def maxpool_f32(self, src, k, stride, pad):
-        return self._add(lib().qnet_add_maxpool_f32(self._h, src, k, stride, pad), "qnet_add_maxpool_f32",
-                         src=src, k=k, stride=stride, pad=pad)
+        return self._mark_fused(self._add(lib().qnet_add_maxpool_f32(self._h, src, k, stride, pad),
+                                          "qnet_add_maxpool_f32", src=src, k=k, stride=stride, pad=pad))
 
     def quantize(self, src, bits):
-        # the library folds Q(x) of a quantized conv's fp32 output into that
-        # conv's epilogue (qnet_add_quantize); recorded here for reports
-        prod = next((L for L in self.layers if L["dst"] == src), None)
-        fused = bool(prod and prod["kind"] == "qconv" and prod["out_bits"] == 0 and not prod.get("pack_dst"))
-        tid = self._add(lib().qnet_add_quantize(self._h, src, bits), "qnet_add_quantize", src=src, out_bits=bits,
-                        fused_into=prod["dst"] - 1 if fused else None)
-        if fused:
-            prod["pack_dst"] = tid
-        return tid
+        return self._mark_fused(self._add(lib().qnet_add_quantize(self._h, src, bits), "qnet_add_quantize", src=src,
+                                          out_bits=bits))
 
     def qconv(self, src, w_packed, cout, k, stride, pad, w_bits, bn_k, bn_b, pool2=False, residual_src=-1,
               out_bits=0):

@@ -3,6 +3,7 @@
 // allocates device memory or synchronises; every launch goes to the
 // caller's stream.
 #include <math.h>
+#include <stdio.h>
 #include <string.h>
 
 #include <atomic>
@@ -352,6 +353,10 @@ struct QLayer {
   // packed Q(HardTanh(z)) of its output, from the same epilogue; the
   // quantize layer that made that tensor is then `fused` and launches nothing
   int pack_dst = -1, fused = 0;
+  // fp32 conv on the matrix cores (the network's fp32 algorithm when the
+  // layer fits it); pool_dst: the tensor of a 3x3 / 2 max pooling fused into
+  // its epilogue (the conv's own output is then never written)
+  int f32_mfma = 0, pool_dst = -1;
 };
 
 size_t tensor_bytes(const QTensor& t, int batch) {
@@ -366,11 +371,20 @@ size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 struct qnet {
   std::vector<QTensor> t;
   std::vector<QLayer> L;
+  int f32_algo = QNET_F32_MFMA;
 };
 
 namespace {
 int run_layers(const qnet* net, const float* x, int batch, float* logits, char* ws, const size_t* toff,
                const size_t* woff, int first, int count, hipStream_t s);
+
+// Whether fp32 conv layer l runs on the matrix cores: the kernel must fit it
+// as it will run (with its fused pooling or without); otherwise the chain.
+bool conv_uses_mfma(const qnet* net, const QLayer& l) {
+  if (l.kind != L_CONV_F32 || !l.f32_mfma) return false;
+  const QTensor& s = net->t[l.src];
+  return conv_f32_mfma_supports(1, s.c, s.h, s.w, l.cout, l.k, l.stride, l.pad, l.pool_dst > 0 ? 1 : 0);
+}
 }  // namespace
 
 namespace {
@@ -441,7 +455,17 @@ int qnet_add_conv_f32(qnet* net, int src, const float* w, int cout, int k, int s
   l.out_bits = out_bits;
   const int ho = qconv_out_size(s.h, k, stride, pad), wo = qconv_out_size(s.w, k, stride, pad);
   if (ho < 1 || wo < 1) return QCONV_EINVAL;
+  // matrix cores when the network asks for them and the kernel fits the layer
+  // unpooled or pooled (a fused pooling decides which, see conv_uses_mfma)
+  l.f32_mfma = net->f32_algo == QNET_F32_MFMA && (conv_f32_mfma_supports(1, s.c, s.h, s.w, cout, k, stride, pad, 0) ||
+                                                  conv_f32_mfma_supports(1, s.c, s.h, s.w, cout, k, stride, pad, 1));
   return add_tensor(net, l, {cout, ho, wo, out_bits});
+}
+
+int qnet_set_f32_algo(qnet* net, int algo) {
+  if (!net || (algo != QNET_F32_FMAF_CHAIN && algo != QNET_F32_MFMA) || !net->L.empty()) return QCONV_EINVAL;
+  net->f32_algo = algo;
+  return QCONV_OK;
 }
 
 int qnet_add_maxpool_f32(qnet* net, int src, int k, int stride, int pad) {
@@ -456,6 +480,17 @@ int qnet_add_maxpool_f32(qnet* net, int src, int k, int stride, int pad) {
   l.pad = pad;
   const int ho = qconv_out_size(s.h, k, stride, pad), wo = qconv_out_size(s.w, k, stride, pad);
   if (ho < 1 || wo < 1) return QCONV_EINVAL;
+  // 3x3 / 2 pooling (pad 1) of a matrix-core fp32 conv's own output runs in
+  // that conv's epilogue
+  if (src > 0 && k == 3 && stride == 2 && pad == 1) {
+    QLayer& prod = net->L[src - 1];
+    const QTensor& ps = net->t[prod.src];
+    if (prod.kind == L_CONV_F32 && prod.f32_mfma && prod.out_bits == 0 && prod.pool_dst < 0 && prod.pack_dst < 0 &&
+        conv_f32_mfma_supports(1, ps.c, ps.h, ps.w, prod.cout, prod.k, prod.stride, prod.pad, 1)) {
+      prod.pool_dst = (int)net->t.size();
+      l.fused = 1;
+    }
+  }
   return add_tensor(net, l, {s.c, ho, wo, 0});
 }
 
@@ -476,6 +511,20 @@ int qnet_add_quantize(qnet* net, int src, int bits) {
   if (src > 0 && prod.kind == L_QCONV && prod.out_bits == 0 && prod.pack_dst < 0) {
     prod.pack_dst = id;
     l.fused = 1;
+  } else if (src > 0 && prod.kind == L_MAXPOOL_F32 && prod.fused) {
+    // a pooling fused into a matrix-core fp32 conv: that conv packs its pooled output
+    QLayer& conv = net->L[prod.src - 1];
+    if (conv.pack_dst < 0) {
+      conv.pack_dst = id;
+      l.fused = 1;
+    }
+  } else if (src > 0 && prod.kind == L_CONV_F32 && prod.f32_mfma && prod.out_bits == 0 && prod.pool_dst < 0 &&
+             prod.pack_dst < 0) {
+    const QTensor& ps = net->t[prod.src];
+    if (conv_f32_mfma_supports(1, ps.c, ps.h, ps.w, prod.cout, prod.k, prod.stride, prod.pad, 0)) {
+      prod.pack_dst = id;
+      l.fused = 1;
+    }
   }
   return add_tensor(net, l, {s.c, s.h, s.w, bits});
 }
@@ -605,6 +654,17 @@ int run_layers(const qnet* net, const float* x, int batch, float* logits, char* 
     int rc = QCONV_OK;
     switch (l.kind) {
       case L_CONV_F32: {
+        if (conv_uses_mfma(net, l)) {
+          const bool pool = l.pool_dst > 0;
+          const int ob = l.out_bits ? l.out_bits : (l.pack_dst > 0 ? net->t[l.pack_dst].bits : 0);
+          float* outf = pool ? static_cast<float*>(ptr(l.pool_dst)) : (l.out_bits ? nullptr : static_cast<float*>(ptr(dst)));
+          uint32_t* outp = l.out_bits ? static_cast<uint32_t*>(ptr(dst))
+                                      : (l.pack_dst > 0 ? static_cast<uint32_t*>(ptr(l.pack_dst)) : nullptr);
+          rc = launch_conv_f32_mfma(static_cast<const float*>(ptr(l.src)), l.wf, batch, si.c, si.h, si.w, l.cout, l.k,
+                                    l.stride, l.pad, l.bn_k, l.bn_b, l.relu, pool ? 1 : 0, outf, outp, ob,
+                                    dflt[ob ? ob : 1], s);
+          break;
+        }
         float* wt = reinterpret_cast<float*>(ws + woff[i]);
         rc = launch_transpose_conv_weight(l.wf, l.cout, si.c, l.k, wt, s);
         if (rc) return rc;
@@ -616,6 +676,7 @@ int run_layers(const qnet* net, const float* x, int batch, float* logits, char* 
         break;
       }
       case L_MAXPOOL_F32:
+        if (l.fused) break;  // in the epilogue of the fp32 conv that made its source
         rc = launch_maxpool_f32(static_cast<const float*>(ptr(l.src)), batch, si.c, si.h, si.w,
                                 l.k, l.stride, l.pad, static_cast<float*>(ptr(dst)), s);
         break;
@@ -672,6 +733,54 @@ int qnet_forward(const qnet* net, const float* x, int batch, float* logits, void
 }
 
 int qnet_num_layers(const qnet* net) { return net ? (int)net->L.size() : QCONV_EINVAL; }
+
+int qnet_layer_kernel(const qnet* net, int layer, int batch, char* buf, int len) {
+  if (!net || layer < 0 || layer >= (int)net->L.size() || batch < 1) return QCONV_EINVAL;
+  const QLayer& l = net->L[layer];
+  const QTensor& si = net->t[l.src];
+  char name[128];
+  name[0] = 0;
+  if (l.fused) {
+    // written by an earlier layer's epilogue: no launch of its own
+  } else if (l.kind == L_CONV_F32) {
+    if (conv_uses_mfma(net, l)) {
+      const int ob = l.out_bits ? l.out_bits : (l.pack_dst > 0 ? net->t[l.pack_dst].bits : 0);
+      snprintf(name, sizeof(name), "conv_f32_mfma_kernel<%d, %d, %d, %d>", l.k, l.stride, l.pool_dst > 0 ? 1 : 0, ob);
+    } else {
+      snprintf(name, sizeof(name), "conv_f32_kernel<%d, %d>", l.out_bits, (l.out_bits == 0 && l.cout > 32) ? 64 : 32);
+    }
+  } else if (l.kind == L_QCONV) {
+    qconv_desc d = {batch, si.c, si.h, si.w, l.cout, l.k, l.k, l.stride, l.pad, si.bits, l.w_bits, QCONV_ALGO_AUTO};
+    qconv_epilogue e;
+    memset(&e, 0, sizeof(e));
+    e.mode = l.out_bits ? QCONV_EPI_BN_PACK : QCONV_EPI_BN_F32;
+    e.flags = (l.pool2 ? QCONV_EPI_POOL2 : 0) | (l.src2 > 0 ? QCONV_EPI_RESIDUAL : 0);
+    e.out_bits = l.out_bits ? l.out_bits : (l.pack_dst > 0 ? net->t[l.pack_dst].bits : 0);
+    const int rc = qconv_kernel_name(&d, &e, (l.out_bits || l.pack_dst > 0) ? 1 : 0, name, (int)sizeof(name));
+    if (rc < 0) return rc;
+  } else if (l.kind == L_MAXPOOL_F32) {
+    snprintf(name, sizeof(name), "%s", (l.k == 3 && l.stride == 2 && l.pad == 1 && si.w % 2 == 0)
+                                           ? "maxpool3s2_f32_kernel" : "maxpool_f32_kernel");
+  } else if (l.kind == L_QUANTIZE) {
+    snprintf(name, sizeof(name), "pack_act_lds_kernel<%d>", l.out_bits);
+  } else if (l.kind == L_AVGPOOL) {
+    snprintf(name, sizeof(name), "avgpool_f32_kernel");
+  } else {
+    snprintf(name, sizeof(name), "fc_f32_kernel<%d>", si.bits);
+  }
+  if (buf && len > 0) snprintf(buf, (size_t)len, "%s", name);
+  return (int)strlen(name);
+}
+
+int qnet_layer_fused_into(const qnet* net, int layer) {
+  if (!net || layer < 0 || layer >= (int)net->L.size()) return QCONV_EINVAL;
+  const int id = layer + 1;
+  for (int i = 0; i < layer; ++i) {
+    const QLayer& l = net->L[i];
+    if (l.pack_dst == id || l.pool_dst == id) return i;
+  }
+  return layer;
+}
 
 }  // extern "C"
 
@@ -760,14 +869,17 @@ size_t liveness_plan(const qnet* net, int batch, size_t* toff, size_t* woff, int
   for (int i = 0; i < nl; ++i) {
     const QLayer& l = net->L[i];
     woff[i] = (size_t)-1;
-    if (l.kind == L_CONV_F32) {
+    if (l.kind == L_CONV_F32 && !conv_uses_mfma(net, l)) {
       const int cin = net->t[l.src].c;
       woff[i] = place((size_t)cin * l.k * l.k * ceil_div(l.cout, 64) * 64 * sizeof(float), i, i);
     }
     const int id = i + 1;
-    if (l.kind == L_QUANTIZE && l.fused) continue;  // placed with the conv that writes it
+    if ((l.kind == L_QUANTIZE || l.kind == L_MAXPOOL_F32) && l.fused) continue;  // placed with the conv that writes it
     toff[id] = (size_t)-1;
-    if (id != nt - 1) toff[id] = place(tensor_bytes(net->t[id], batch), i, last_use[id]);
+    // a conv whose pooling is fused never writes its own output
+    if (id != nt - 1 && !(l.kind == L_CONV_F32 && l.pool_dst > 0))
+      toff[id] = place(tensor_bytes(net->t[id], batch), i, last_use[id]);
+    if (l.pool_dst > 0) toff[l.pool_dst] = place(tensor_bytes(net->t[l.pool_dst], batch), i, last_use[l.pool_dst]);
     if (l.pack_dst > 0) toff[l.pack_dst] = place(tensor_bytes(net->t[l.pack_dst], batch), i, last_use[l.pack_dst]);
   }
   toff[0] = (size_t)-1;

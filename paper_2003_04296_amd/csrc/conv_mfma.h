@@ -891,7 +891,7 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
   load_halo<PA, NI>(m, cur.img0, cur.iy0, 0, tid, raw);
   if constexpr (SWAP) load_params<BCO>(a, cur.co_blk, tid, prm_base);
   store_halo<OPK, PA, NI>(m, cur.img0, cur.iy0, 0, tid, raw, halo_base);
-  __syncthreads();
+  lds_barrier();
 
   acc_t acc[MT][NT];
 #pragma unroll
@@ -1018,7 +1018,7 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
         // a split-K block has no next stage), one tile per wave
         // (the raw accumulator bits: int32 partials are summed as integers,
         // exact at any magnitude; fp32 ones hold exact integers below 2^24)
-        __syncthreads();
+        lds_barrier();
         using elem_t = typename std::conditional<std::is_same<acc_t, v16i>::value, int, float>::type;
         typedef elem_t e4 __attribute__((ext_vector_type(4)));
         e4* red = reinterpret_cast<e4*>(halo_base);
@@ -1035,7 +1035,7 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
               t.w = acc[i][j][4 * v4 + 3];
               red[((wave * (MT * NT) + i * NT + j) * 4 + v4) * 64 + elane] = t;
             }
-        __syncthreads();
+        lds_barrier();
         const int tile = wave;  // this wave's tile after the reduction
         acc_t sum;
 #pragma unroll
@@ -1105,20 +1105,13 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
     }
     chunk = nchunk;
     sbuf ^= 1;
-    __syncthreads();
+    lds_barrier();
   }
 }
 
 // s_waitcnt vmcnt(0): every vector memory access of the wave has completed.
 __device__ __forceinline__ void vm_wait_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
-// Workgroup barrier that orders LDS accesses only: outstanding global
-// stores are not waited for, so they keep draining across it.
-__device__ __forceinline__ void lds_barrier() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
 
 // Packed words of this thread's share of a halo tile (items it = tid +
 // STRIDE u, as in load_halo), read through a buffer resource over the packed

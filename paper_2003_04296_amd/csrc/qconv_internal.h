@@ -21,6 +21,18 @@ struct Thr {
   float t0, t1, t2;
 };
 
+// Workgroup barrier that orders LDS accesses only.  __syncthreads() also
+// waits for every outstanding global load and store of the wave (its
+// release fence covers global memory), which stalls a barrier that a
+// prefetch of the next tile or the previous tile's output stores are still
+// in flight across; this one leaves them in flight.  For blocks that share
+// data through LDS alone.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // Inference quantizer h(.) of Sec. III-C returning the bitplane pattern of
 // the level: bit 0 = sign (level > 0), bit p = magnitude plane p.
 //  1 bit : sign (Eq. 4), +1 only for x > 0.
@@ -204,6 +216,12 @@ int launch_conv_f32(const float* x, const float* wt_t /* [cin][k][k][cout_pad64]
                     int h, int w, int cout, int k, int stride, int pad, const float* bn_k,
                     const float* bn_b, int relu, int out_bits, Thr othr, float* out_f32,
                     uint32_t* out_packed, hipStream_t s);
+// fp32 conv on the matrix cores with BN, ReLU, optional 3x3 / 2 max pooling
+// (pad 1) and an optional packed Q(HardTanh(.)) copy (conv_f32_mfma.hip).
+bool conv_f32_mfma_supports(int n, int cin, int h, int w, int cout, int k, int stride, int pad, int pool);
+int launch_conv_f32_mfma(const float* x, const float* w, int n, int cin, int h, int wd, int cout, int k, int stride,
+                         int pad, const float* bn_k, const float* bn_b, int relu, int pool, float* out,
+                         uint32_t* out_packed, int out_bits, Thr othr, hipStream_t s);
 int launch_transpose_conv_weight(const float* w, int cout, int cin, int k, float* wt_t,
                                  hipStream_t s);
 int launch_maxpool_f32(const float* x, int n, int c, int h, int w, int k, int stride, int pad,

@@ -9,7 +9,7 @@ from __future__ import annotations
 
 import torch
 
-from . import Net, fold_bn, pack_weight
+from . import F32_MFMA, Net, fold_bn, pack_weight
 
 
 def _dev_bn(bn, device):
@@ -52,13 +52,14 @@ class QNetwork:
         return ws[off:off + 4 * words].view(torch.int32), bits
 
 
-def build_convnet(p: dict, device, a_bits: int = 1, w_bits: int = 1) -> QNetwork:
+def build_convnet(p: dict, device, a_bits: int = 1, w_bits: int = 1, f32_algo: int = F32_MFMA) -> QNetwork:
     """fp32 conv1 -> BN -> sign; binary convs with 2x2 max pool before BN
     where the topology has one; binary FCs (the first as a conv covering the
     whole 4x4 map, so its (c, h, w) weight order is the conv's OIHW order);
-    fp32 FC + bias."""
+    fp32 FC + bias.  f32_algo: the fp32 first conv on the matrix cores
+    (default) or as fixed fmaf chains (bit-exact against the oracle)."""
     hw = p["hw"]
-    net = Net(3, hw, hw)
+    net = Net(3, hw, hw, f32_algo)
     ids = {}
     c1 = p["convs"][0]
     k, b = _dev_bn(c1["bn"], device)
@@ -87,12 +88,14 @@ def build_convnet(p: dict, device, a_bits: int = 1, w_bits: int = 1) -> QNetwork
     return QNetwork(net, (3, hw, hw), fo["w"].shape[0], device, ids)
 
 
-def build_resnet18(p: dict, device, a_bits: int = 2, w_bits: int = 2) -> QNetwork:
+def build_resnet18(p: dict, device, a_bits: int = 2, w_bits: int = 2, f32_algo: int = F32_MFMA) -> QNetwork:
     """fp32 stem conv 7x7/2 -> BN -> ReLU -> max pool 3x3/2; eight basic
     blocks with quantized convs (q = Q(x); y = Q(BN1(q*W1)); out = BN2(y*W2)
-    + shortcut, shortcut = x or BN_d(q*W_d)); average pool; fp32 FC."""
+    + shortcut, shortcut = x or BN_d(q*W_d)); average pool; fp32 FC.  With the
+    matrix-core fp32 algorithm (default) the stem's max pooling and the first
+    block's quantize run in the stem conv's epilogue."""
     _, _, hh, ww = p["x"].shape
-    net = Net(3, hh, ww)
+    net = Net(3, hh, ww, f32_algo)
     ids = {}
     st = p["stem"]
     k, b = _dev_bn(st["bn"], device)

@@ -280,3 +280,29 @@ def test_binding_checks_threshold_counts(bits, vals):
     # zero-valued thresholds are a real setting, not "use the defaults"
     arr = q._host_thr(np.zeros({2: 1, 3: 3}[bits], np.float32), bits, "test")
     assert arr is not None and list(arr) == [0.0] * {2: 1, 3: 3}[bits]
+
+
+@pytest.mark.parametrize("algo", [q.F32_MFMA, q.F32_FMAF_CHAIN])
+def test_stem_fusion_bookkeeping(algo):
+    """A 7x7/2 fp32 stem followed by 3x3/2 max pooling and a 2-bit quantize:
+    with the matrix-core algorithm both later layers are written by the stem's
+    epilogue and launch nothing; with the fmaf chains each launches its own
+    kernel.  Host-side only (nothing is launched)."""
+    L = q.lib()
+    net = q.Net(3, 224, 224, algo)
+    h = net._h
+    t1 = L.qnet_add_conv_f32(h, 0, FAKE, 64, 7, 2, 3, FAKE, FAKE, 1, 0)
+    t2 = L.qnet_add_maxpool_f32(h, t1, 3, 2, 1)
+    t3 = L.qnet_add_quantize(h, t2, 2)
+    assert (t1, t2, t3) == (1, 2, 3)
+    fused = [L.qnet_layer_fused_into(h, i) for i in range(3)]
+    names = [net.layer_kernel(i, 8) for i in range(3)]
+    if algo == q.F32_MFMA:
+        assert fused == [0, 0, 0]
+        assert names == ["conv_f32_mfma_kernel<7, 2, 1, 2>", "", ""]
+    else:
+        assert fused == [0, 1, 2]
+        assert names[0].startswith("conv_f32_kernel<") and names[1] and names[2]
+    assert L.qnet_layer_fused_into(h, 3) == q.QCONV_EINVAL
+    assert L.qnet_layer_fused_into(h, -1) == q.QCONV_EINVAL
+    assert L.qnet_layer_fused_into(None, 0) == q.QCONV_EINVAL

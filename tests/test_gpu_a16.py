@@ -456,7 +456,7 @@ def test_convnet_with_16_bit_weights(dev, a_bits):
     g = synth.generator(1014)
     for layer in p["convs"][1:] + p["fcs"]:
         layer["w"] = torch.floor(synth.uniform(g, tuple(layer["w"].shape), -2.0, 3.0))
-    net = build_convnet(p, dev, a_bits=a_bits, w_bits=16)
+    net = build_convnet(p, dev, a_bits=a_bits, w_bits=16, f32_algo=q.F32_FMAF_CHAIN)
     logits = net.forward(p["x"].to(dev))
     torch.cuda.synchronize()
     want, levels = oracle.convnet16w_forward(p, a_bits, return_levels=True)

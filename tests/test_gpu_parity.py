@@ -648,7 +648,7 @@ def test_convnet_layers_and_logits(dev):
     from paper_2003_04296_amd.nets import build_convnet
 
     p = synth.convnet_params(seed=1003, batch=4)
-    net = build_convnet(p, dev)
+    net = build_convnet(p, dev, f32_algo=q.F32_FMAF_CHAIN)
     logits = net.forward(p["x"].to(dev))
     torch.cuda.synchronize()
     want, levels = oracle.convnet_forward(p, return_levels=True)
@@ -667,7 +667,7 @@ def test_convnet_full_batch(dev):
     from paper_2003_04296_amd.nets import build_convnet
 
     p = synth.convnet_params(seed=1003, batch=256)
-    net = build_convnet(p, dev)
+    net = build_convnet(p, dev, f32_algo=q.F32_FMAF_CHAIN)
     logits = net.forward(p["x"].to(dev)).cpu().numpy()
     want = oracle.convnet_forward(p)
     np.testing.assert_array_equal(logits, want)
@@ -679,7 +679,7 @@ def test_resnet18_blocks_and_logits(dev):
     from paper_2003_04296_amd.nets import build_resnet18
 
     p = synth.resnet18_params(seed=1004, batch=2)
-    net = build_resnet18(p, dev)
+    net = build_resnet18(p, dev, f32_algo=q.F32_FMAF_CHAIN)
     logits = net.forward(p["x"].to(dev))
     torch.cuda.synchronize()
     want, acts = oracle.resnet18_forward(p, 2, 2, return_acts=True)
@@ -698,7 +698,7 @@ def test_resnet18_full_batch(dev):
     from paper_2003_04296_amd.nets import build_resnet18
 
     p = synth.resnet18_params(seed=1004, batch=64)
-    net = build_resnet18(p, dev)
+    net = build_resnet18(p, dev, f32_algo=q.F32_FMAF_CHAIN)
     logits = net.forward(p["x"].to(dev)).cpu().numpy()
     want = oracle.resnet18_forward(p, 2, 2)
     np.testing.assert_array_equal(logits, want)
@@ -728,7 +728,7 @@ def test_fc_f32_fp32_input(dev, n, c, h, w, out, bias):
     x = synth.normal(g, (n, c, h, w), 1.0)
     wt = synth.normal(g, (out, c * h * w), 2.0 / (c * h * w))
     b = synth.normal(g, (out,), 0.1) if bias else None
-    net = q.Net(c, h, w)
+    net = q.Net(c, h, w, q.F32_FMAF_CHAIN)
     net.fc_f32(0, wt.to(dev), b.to(dev) if bias else None)
     got = _run_net(dev, net, x, out)
     want = oracle.fc_f32(x.numpy().reshape(n, -1), wt.numpy(), b.numpy() if bias else None)
@@ -763,7 +763,7 @@ def test_conv_f32_pools_and_head(dev, n, cin, hw, cout, k, s, p, pk, ps, pp):
     wt = synth.normal(g, (cout, cin, k, k), 2.0 / (cin * k * k))
     kk, bb = _bn(700 + hw, cout)
     fw = synth.normal(g, (11, cout), 2.0 / cout)
-    net = q.Net(cin, hw, hw)
+    net = q.Net(cin, hw, hw, q.F32_FMAF_CHAIN)
     t1 = net.conv_f32(0, wt.to(dev), kk.to(dev), bb.to(dev), stride=s, pad=p, relu=True)
     t2 = net.maxpool_f32(t1, pk, ps, pp)
     t3 = net.avgpool(t2)
