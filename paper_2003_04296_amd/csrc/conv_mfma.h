@@ -66,14 +66,25 @@ constexpr int MAX_LDS_WIDE = 76 * 1024;
 constexpr int BRING = 2;  // weight-fragment register sets in flight (deeper rings measured slower)
 // Packed words of the next stage held per thread in registers (bounded by
 // the registers left next to the accumulators); items past 256 times this
-// are loaded when the stage is expanded.
+// are loaded when the stage is expanded, each pair then waiting a full
+// global-memory latency.  The 128-channel block shape holds up to 2048
+// items of 1- and 2-bit inputs (its 3x3 halo tiles of 128 channels); the
+// smaller shapes, whose tiles are narrower and which run three blocks per
+// CU within 168 registers, hold 1024.
 // fp16 halo words (64 bytes each) are not held across the MFMAs: they are
 // loaded at the end of the stage instead (two per thread in flight), so
 // that no weight-fragment load of the MFMA loop waits behind them (loads of
 // a wave complete in order) and the registers stay free.
-__host__ __device__ constexpr int halo_items_per_thread(int words) {
-  return words == 1 ? 4 : words == 16 ? 0 : 8 / words;
+__host__ __device__ constexpr int halo_items_per_thread(int words, int cfg) {
+  return words == 16 ? 0 : (cfg == 0 && words <= 2 ? 8 : (words == 1 ? 4 : 8 / words));
 }
+
+// Blocks of conv_mfma_kernel per CU that its register budget is compiled
+// for (512 registers per SIMD lane shared by the resident waves): three for
+// the fp4 shapes of up to 64 output channels per block (168 registers), two
+// otherwise (the 128-channel shape holds twice the accumulators; the int8
+// and fp16 shapes spill within 168).
+__host__ __device__ constexpr int blocks_per_cu(int opk, int cfg) { return opk == OP_FP4 && cfg != 0 ? 3 : 2; }
 
 // n / d by a multiply-high, exact whenever n * d < 2^32 (checked on the host
 // against the largest dividend of each use).
@@ -495,8 +506,10 @@ __device__ __forceinline__ void swap_res_load(const MfmaArgs& m, int img0, int u
 // OB > 0: the packed planes of Q(HardTanh(z)) (Eqs. 4, 21, 22) as well (KIND
 // K_PACK: only those).  A lane holds 16 of the 32 channels of its unit, so
 // it sets its 16 bits of each plane word with the quantizer's compares, and
-// one exchange with lane l ^ 32 completes the word, which lanes 0-31 store.
-template <int KIND, int RES = 2, int OB = 0, class AccT>
+// one exchange with lane l ^ 32 completes the word, which lanes 0-31 store
+// (PERM: through v_permlane32_swap, else a shuffle through LDS, which takes
+// no extra register).
+template <int KIND, int RES = 2, int OB = 0, bool PERM = false, class AccT>
 __device__ __forceinline__ void tile_epilogue_swap(const MfmaArgs& m, const AccT& acc, int img0, int u0,
                                                    int T, int co32, int co_blk, const float* prm,
                                                    int lane, const float (*pre)[16] = nullptr) {
@@ -579,7 +592,15 @@ __device__ __forceinline__ void tile_epilogue_swap(const MfmaArgs& m, const AccT
 #pragma unroll
     for (int p = 0; p < POUT; ++p) {
       pw[p] <<= 4 * g;  // this lane's channels are cbase + ...: nibbles of half g
-      pw[p] |= (uint32_t)__shfl_xor((int)pw[p], 32);
+      if constexpr (PERM) {
+        // lanes 0-31 take the word of lane l + 32 (one VALU op, no LDS round
+        // trip); OR-ing both results is the same whichever of the two
+        // carries the swapped half
+        const auto sw = __builtin_amdgcn_permlane32_swap(pw[p], pw[p], false, false);
+        pw[p] |= sw[0] | sw[1];
+      } else {
+        pw[p] |= (uint32_t)__shfl_xor((int)pw[p], 32);
+      }
     }
     if (g == 0 && uok) {
       uint32_t* dst = a.out_packed + (((int64_t)img * m.upi + uu) * a.out_cw + (co32 >> 5)) * POUT;
@@ -611,69 +632,129 @@ __device__ __forceinline__ void tile_epilogue_swap_mode(const MfmaArgs& m, const
   }
 }
 
-// The epilogue over the wave's MT x NT tiles: a loop at run time that copies
-// one tile at a time out of the (statically indexed) accumulator array.
-template <int KIND, int OB, int POOL, int MT, int NT, class AccT>
+// The epilogue over the wave's MT x NT tiles.  The per-channel parameters
+// come from the block's LDS copy (kk at prm[c], bb at prm[128 + c] for
+// channel co_blk + c).  UNROLL: the tiles as a compile-time sequence, so that
+// independent tiles' loads, arithmetic and stores interleave; otherwise a
+// loop at run time that copies one tile at a time out of the (statically
+// indexed) accumulator array, which keeps the code of the rarely used output
+// modes small.
+template <int KIND, int OB, int POOL, bool UNROLL, int MT, int NT, class AccT>
 __device__ __forceinline__ void epilogue(const MfmaArgs& m, const AccT (&acc)[MT][NT], int img0,
-                                         int u0, int tile_m0, int co_w, int lane) {
+                                         int u0, int tile_m0, int co_w, int co_blk, const float* prm, int lane) {
   const ConvArgs& a = m.c;
   const int r32 = lane & 31;
-  float kk[NT], bb[NT];
-#pragma unroll
-  for (int j = 0; j < NT; ++j) {
-    const int co = co_w + 32 * j + r32;
-    const int cs = co < a.cout ? co : a.cout - 1;
-    kk[j] = 0.0f;
-    bb[j] = 0.0f;
-    if constexpr (KIND == K_SCALE) kk[j] = a.scale[cs];
-    if constexpr (KIND == K_BNF32 || KIND == K_PACK) {
-      kk[j] = a.bn_k[cs];
-      bb[j] = a.bn_b[cs];
-    }
-  }
+  auto one = [&](const AccT& t, int i, int j) __attribute__((always_inline)) {
+    const int co32 = co_w + 32 * j;
+    const int c = co32 - co_blk + r32;
+    const float kj = KIND == K_INT32 ? 0.0f : prm[c];
+    const float bj = (KIND == K_BNF32 || KIND == K_PACK) ? prm[128 + c] : 0.0f;
+    tile_epilogue<KIND, OB, POOL>(m, t, img0, u0, tile_m0 + i, co32, kj, bj, lane);
+  };
+  if constexpr (UNROLL) {
+    Unroll<0, MT * NT>::run([&](auto TT) {
+      constexpr int tt = decltype(TT)::value;
+      if (co_w + 32 * (tt % NT) < a.cout) one(acc[tt / NT][tt % NT], tt / NT, tt % NT);  // uniform
+    });
+  } else {
 #pragma nounroll
-  for (int tt = 0; tt < MT * NT; ++tt) {
-    const int i = tt / NT, j = tt - (tt / NT) * NT;
-    if (co_w + 32 * j >= a.cout) continue;  // uniform: tile past the last channel
-    AccT cur;
-    switch (tt) {
+    for (int tt = 0; tt < MT * NT; ++tt) {
+      const int i = tt / NT, j = tt - (tt / NT) * NT;
+      if (co_w + 32 * j >= a.cout) continue;  // uniform: tile past the last channel
+      AccT cur;
+      switch (tt) {
 #define QC_PICK(K)                   \
   case K:                            \
     if constexpr (K < MT * NT) cur = acc[K / NT][K % NT]; \
     break;
-      QC_PICK(0) QC_PICK(1) QC_PICK(2) QC_PICK(3) QC_PICK(4) QC_PICK(5) QC_PICK(6) QC_PICK(7)
+        QC_PICK(0) QC_PICK(1) QC_PICK(2) QC_PICK(3) QC_PICK(4) QC_PICK(5) QC_PICK(6) QC_PICK(7)
 #undef QC_PICK
-      default: break;
-    }
-    float kj = kk[0], bj = bb[0];
-#pragma unroll
-    for (int jj = 1; jj < NT; ++jj)
-      if (j == jj) {
-        kj = kk[jj];
-        bj = bb[jj];
+        default: break;
       }
-    tile_epilogue<KIND, OB, POOL>(m, cur, img0, u0, tile_m0 + i, co_w + 32 * j, kj, bj, lane);
+      one(cur, i, j);
+    }
   }
 }
 
+// The packed and BN outputs of pooled layers (the case of this orientation
+// in networks) run the unrolled tile sequence; other outputs the loop.
 template <int KIND, int POOL, int MT, int NT, class AccT>
 __device__ __forceinline__ void epilogue_ob(const MfmaArgs& m, const AccT (&acc)[MT][NT], int img0,
-                                            int u0, int tile_m0, int co_w, int lane) {
+                                            int u0, int tile_m0, int co_w, int co_blk, const float* prm, int lane) {
   const int ob = m.c.out_packed ? m.c.out_bits : 0;
-  if (ob == 0) epilogue<KIND, 0, POOL>(m, acc, img0, u0, tile_m0, co_w, lane);
-  else if (ob == 1) epilogue<KIND, 1, POOL>(m, acc, img0, u0, tile_m0, co_w, lane);
-  else if (ob == 2) epilogue<KIND, 2, POOL>(m, acc, img0, u0, tile_m0, co_w, lane);
-  else epilogue<KIND, 3, POOL>(m, acc, img0, u0, tile_m0, co_w, lane);
+  constexpr bool U = POOL == 1;  // unpooled layers take the swapped orientation
+  if (ob == 0) epilogue<KIND, 0, POOL, U && KIND == K_BNF32>(m, acc, img0, u0, tile_m0, co_w, co_blk, prm, lane);
+  else if (ob == 1) epilogue<KIND, 1, POOL, U>(m, acc, img0, u0, tile_m0, co_w, co_blk, prm, lane);
+  else if (ob == 2) epilogue<KIND, 2, POOL, U>(m, acc, img0, u0, tile_m0, co_w, co_blk, prm, lane);
+  else epilogue<KIND, 3, POOL, U>(m, acc, img0, u0, tile_m0, co_w, co_blk, prm, lane);
 }
 
 template <int POOL, int MT, int NT, class AccT>
 __device__ __forceinline__ void epilogue_mode(const MfmaArgs& m, const AccT (&acc)[MT][NT], int img0,
-                                              int u0, int tile_m0, int co_w, int lane) {
+                                              int u0, int tile_m0, int co_w, int co_blk, const float* prm,
+                                              int lane) {
   switch (m.c.mode) {
-    case QCONV_EPI_INT32: epilogue<K_INT32, 0, POOL>(m, acc, img0, u0, tile_m0, co_w, lane); break;
-    case QCONV_EPI_SCALE_F32: epilogue<K_SCALE, 0, POOL>(m, acc, img0, u0, tile_m0, co_w, lane); break;
-    case QCONV_EPI_BN_F32: epilogue_ob<K_BNF32, POOL>(m, acc, img0, u0, tile_m0, co_w, lane); break;
-    default: epilogue_ob<K_PACK, POOL>(m, acc, img0, u0, tile_m0, co_w, lane); break;
+    case QCONV_EPI_INT32:
+      epilogue<K_INT32, 0, POOL, false>(m, acc, img0, u0, tile_m0, co_w, co_blk, prm, lane);
+      break;
+    case QCONV_EPI_SCALE_F32:
+      epilogue<K_SCALE, 0, POOL, false>(m, acc, img0, u0, tile_m0, co_w, co_blk, prm, lane);
+      break;
+    case QCONV_EPI_BN_F32: epilogue_ob<K_BNF32, POOL>(m, acc, img0, u0, tile_m0, co_w, co_blk, prm, lane); break;
+    default: epilogue_ob<K_PACK, POOL>(m, acc, img0, u0, tile_m0, co_w, co_blk, prm, lane); break;
+  }
+}
+
+// The swapped epilogue over the wave's MT x NT tiles: packed and BN outputs
+// as an unrolled tile sequence (mode fixed at compile time), int32 and scaled
+// outputs one tile at a time.
+template <int KIND, int RES, int OB, int MT, int NT, class AccT>
+__device__ __forceinline__ void epilogue_swap_tiles(const MfmaArgs& m, const AccT (&acc)[MT][NT], int img0,
+                                                    int u0, int tile_m0, int co_w, int co_blk, const float* prm,
+                                                    int lane) {
+  Unroll<0, MT * NT>::run([&](auto TT) {
+    constexpr int tt = decltype(TT)::value;
+    const int co32 = co_w + 32 * (tt % NT);
+    if (co32 < m.c.cout)  // uniform
+      tile_epilogue_swap<KIND, RES, OB, true>(m, acc[tt / NT][tt % NT], img0, u0, tile_m0 + tt / NT, co32, co_blk,
+                                              prm, lane);
+  });
+}
+
+template <int MT, int NT, class AccT>
+__device__ __forceinline__ void epilogue_swap_all(const MfmaArgs& m, const AccT (&acc)[MT][NT], int img0, int u0,
+                                                  int tile_m0, int co_w, int co_blk, const float* prm, int lane) {
+  const ConvArgs& a = m.c;
+  const int ob = a.out_packed ? a.out_bits : 0;
+  if (a.mode == QCONV_EPI_BN_PACK) {
+    if (ob == 1) epilogue_swap_tiles<K_PACK, 0, 1>(m, acc, img0, u0, tile_m0, co_w, co_blk, prm, lane);
+    else if (ob == 2) epilogue_swap_tiles<K_PACK, 0, 2>(m, acc, img0, u0, tile_m0, co_w, co_blk, prm, lane);
+    else epilogue_swap_tiles<K_PACK, 0, 3>(m, acc, img0, u0, tile_m0, co_w, co_blk, prm, lane);
+  } else if (a.mode == QCONV_EPI_BN_F32) {
+    if (ob == 0) epilogue_swap_tiles<K_BNF32, 2, 0>(m, acc, img0, u0, tile_m0, co_w, co_blk, prm, lane);
+    else if (ob == 1) epilogue_swap_tiles<K_BNF32, 2, 1>(m, acc, img0, u0, tile_m0, co_w, co_blk, prm, lane);
+    else if (ob == 2) epilogue_swap_tiles<K_BNF32, 2, 2>(m, acc, img0, u0, tile_m0, co_w, co_blk, prm, lane);
+    else epilogue_swap_tiles<K_BNF32, 2, 3>(m, acc, img0, u0, tile_m0, co_w, co_blk, prm, lane);
+  } else {
+    const int r32 = lane & 31;
+    (void)r32;
+#pragma nounroll
+    for (int tt = 0; tt < MT * NT; ++tt) {
+      const int i = tt / NT, j = tt - (tt / NT) * NT;
+      const int co32 = co_w + 32 * j;
+      if (co32 >= a.cout) continue;
+      AccT tcur;
+      switch (tt) {
+#define QC_PICK(K)                                         \
+  case K:                                                  \
+    if constexpr (K < MT * NT) tcur = acc[K / NT][K % NT]; \
+    break;
+        QC_PICK(0) QC_PICK(1) QC_PICK(2) QC_PICK(3) QC_PICK(4) QC_PICK(5) QC_PICK(6) QC_PICK(7)
+#undef QC_PICK
+        default: break;
+      }
+      tile_epilogue_swap_mode(m, tcur, img0, u0, tile_m0 + i, co32, co_blk, prm, lane);
+    }
   }
 }
 
@@ -852,13 +933,13 @@ __device__ __forceinline__ void load_params(const ConvArgs& a, int co_blk, int t
 // after them, so that global latency, the expansion and the epilogue's
 // stores overlap the matrix work.  Split-K shapes run one item per block.
 template <int OPK, int PA, int CFG, int SWAP>
-__global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
+__global__ __launch_bounds__(256, blocks_per_cu(OPK, CFG)) void conv_mfma_kernel(const MfmaArgs m) {
   using O = OpT<OPK>;
   using acc_t = typename O::acc_t;
   using C = Cfg<CFG>;
   constexpr int MT = C::MT, NT = C::NT, WN = C::WN, SK = C::SK;
   constexpr int BCO = 32 * NT * WN;
-  constexpr int NI = halo_items_per_thread(PA);  // halo items per thread and stage
+  constexpr int NI = halo_items_per_thread(PA, CFG);  // halo items per thread and stage
   static_assert(SK == 1 || SK == MT * NT, "a split-K block has one tile per wave");
   extern __shared__ __attribute__((aligned(16))) uint8_t lds_raw[];
   const ConvArgs& a = m.c;
@@ -889,7 +970,7 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
   decode_item<MT, NT, WN>(m, w, wm, r32, g, &cur);
   uint32_t raw[NI > 0 ? NI : 1][PA];
   load_halo<PA, NI>(m, cur.img0, cur.iy0, 0, tid, raw);
-  if constexpr (SWAP) load_params<BCO>(a, cur.co_blk, tid, prm_base);
+  load_params<BCO>(a, cur.co_blk, tid, prm_base);
   store_halo<OPK, PA, NI>(m, cur.img0, cur.iy0, 0, tid, raw, halo_base);
   lds_barrier();
 
@@ -1056,35 +1137,19 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
           } else {
             acc_t one[1][1] = {{sum}};
             if (m.pool)
-              epilogue_mode<1>(m, one, cur.img0, cur.u0, ti, co32, elane);
+              epilogue_mode<1>(m, one, cur.img0, cur.u0, ti, co32, cur.co_blk, prm, elane);
             else
-              epilogue_mode<0>(m, one, cur.img0, cur.u0, ti, co32, elane);
+              epilogue_mode<0>(m, one, cur.img0, cur.u0, ti, co32, cur.co_blk, prm, elane);
           }
         }
       } else if (co_w < a.cout) {
         if constexpr (SWAP) {
-#pragma nounroll
-          for (int tt = 0; tt < MT * NT; ++tt) {
-            const int i = tt / NT, j = tt - (tt / NT) * NT;
-            const int co32 = co_w + 32 * j;
-            if (co32 >= a.cout) continue;
-            acc_t tcur;
-            switch (tt) {
-#define QC_PICK(K)                                         \
-  case K:                                                  \
-    if constexpr (K < MT * NT) tcur = acc[K / NT][K % NT]; \
-    break;
-              QC_PICK(0) QC_PICK(1) QC_PICK(2) QC_PICK(3) QC_PICK(4) QC_PICK(5) QC_PICK(6) QC_PICK(7)
-#undef QC_PICK
-              default: break;
-            }
-            tile_epilogue_swap_mode(m, tcur, cur.img0, cur.u0, wm * MT + i, co32, cur.co_blk, prm, elane);
-          }
+          epilogue_swap_all(m, acc, cur.img0, cur.u0, wm * MT, co_w, cur.co_blk, prm, elane);
         } else {
           if (m.pool)
-            epilogue_mode<1>(m, acc, cur.img0, cur.u0, wm * MT, co_w, elane);
+            epilogue_mode<1>(m, acc, cur.img0, cur.u0, wm * MT, co_w, cur.co_blk, prm, elane);
           else
-            epilogue_mode<0>(m, acc, cur.img0, cur.u0, wm * MT, co_w, elane);
+            epilogue_mode<0>(m, acc, cur.img0, cur.u0, wm * MT, co_w, cur.co_blk, prm, elane);
         }
       }
 #pragma unroll
@@ -1101,7 +1166,7 @@ __global__ __launch_bounds__(256, 2) void conv_mfma_kernel(const MfmaArgs m) {
       w = nw;
       const int dt = fresh_tid();
       decode_item<MT, NT, WN>(m, w, wm, dt & 31, (dt >> 5) & 1, &cur);
-      if constexpr (SWAP) load_params<BCO>(a, cur.co_blk, fresh_tid(), prm_base + ipar * (PARAM_BYTES / 4));
+      load_params<BCO>(a, cur.co_blk, fresh_tid(), prm_base + ipar * (PARAM_BYTES / 4));
     }
     chunk = nchunk;
     sbuf ^= 1;
@@ -1531,7 +1596,8 @@ int launch_cfg(MfmaArgs m, hipStream_t s) {
   if (CFG == 2) {
     m.grid = total;  // split-K: one item per block
   } else {
-    const int per_cu = max(1, min(2, (int)(LDS_PER_CU / lds)));
+    // resident blocks per CU: the register bound of the kernel, then LDS
+    const int per_cu = max(1, min(blocks_per_cu(OPK, CFG), (int)(LDS_PER_CU / lds)));
     m.grid = min(total, per_cu * cus);
   }
   if (use_swap(m)) {
