@@ -112,7 +112,8 @@ def level_shift(bits: int) -> int:
 
 
 def weight_scale(w) -> np.ndarray:
-    """s_c = mean |W_c| per output channel (double sum, one rounding)."""
+    """s_c = mean |W_c| per output channel (double sum in a fixed order:
+    256 strided partial sums, added pairwise; one rounding to float)."""
     w = _f32(w)
     cout = w.shape[0]
     k = w.size // cout

@@ -80,13 +80,22 @@ int oracle_quantize(const float* x, int64_t n, int bits, const float* thr, int8_
 }
 
 /* Per-output-channel weight scale s_c = mean |W_c| over the k = Cin*Kh*Kw
- * weights of channel c, summed in double in storage order, then rounded
- * once to float. */
+ * weights of channel c, in double with a fixed summation order, then
+ * rounded once to float: 256 partial sums P_j (j = 0..255), P_j adding
+ * |w_i| for the storage indices i = j, j + 256, j + 512, ... in turn; the
+ * partial sums are then added pairwise (P_0 + P_1, P_2 + P_3, ..., then
+ * those sums pairwise, and so on up to one sum); s_c = (float)(sum / k). */
 void oracle_weight_scale(const float* w, int cout, int64_t k, float* s) {
   for (int c = 0; c < cout; ++c) {
-    double sum = 0.0;
-    for (int64_t i = 0; i < k; ++i) sum += fabs((double)w[(int64_t)c * k + i]);
-    s[c] = (float)(sum / (double)k);
+    const float* wc = w + (int64_t)c * k;
+    double part[256];
+    for (int j = 0; j < 256; ++j) {
+      part[j] = 0.0;
+      for (int64_t i = j; i < k; i += 256) part[j] += fabs((double)wc[i]);
+    }
+    for (int step = 1; step < 256; step *= 2)
+      for (int j = 0; j < 256; j += 2 * step) part[j] = part[j] + part[j + step];
+    s[c] = (float)(part[0] / (double)k);
   }
 }
 

@@ -132,14 +132,38 @@ __global__ __launch_bounds__(256) void pack_act_f16_kernel(const float* __restri
 }
 
 // s_c = (float)(sum_k |W_ck| / K), the sum in double in storage order.
-__global__ void weight_scale_kernel(const float* __restrict__ w, int cout, int k,
-                                    float* __restrict__ scale) {
-  const int co = blockIdx.x * blockDim.x + threadIdx.x;
-  if (co >= cout) return;
+// s_c = mean |W_c| (Eq. 20's scale of a channel's weights), one block per
+// output channel.  The sum is taken in double in a fixed order, so the
+// result does not depend on the launch: thread j adds |w_i| for i = j,
+// j + 256, ... in turn (coalesced reads, up to 32 loads in flight), then the
+// 256 partial sums are added pairwise: lanes exchange with lane l ^ 1, l ^ 2,
+// ... l ^ 32 (every lane of a pair forms the same sum, IEEE addition being
+// commutative), and the four wave sums are added (w0 + w1) + (w2 + w3).  One
+// rounding to float at the end.
+__global__ __launch_bounds__(256) void weight_scale_kernel(const float* __restrict__ w, int k,
+                                                          float* __restrict__ scale) {
+  __shared__ double wsum[4];
+  const int co = blockIdx.x;
   const float* p = w + (int64_t)co * k;
-  double sum = 0.0;
-  for (int i = 0; i < k; ++i) sum += fabs((double)p[i]);
-  scale[co] = (float)(sum / (double)k);
+  double acc = 0.0;
+  constexpr int B = 32;
+  for (int i0 = threadIdx.x; i0 < k; i0 += 256 * B) {
+    // unguarded loads (indices clamped into the channel) so that all of them
+    // issue before the first addition; only in-range values are added
+    float v[B];
+#pragma unroll
+    for (int u = 0; u < B; ++u) v[u] = p[min(i0 + 256 * u, k - 1)];
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      const double t = fabs((double)v[u]);
+      if (i0 + 256 * u < k) acc += t;
+    }
+  }
+#pragma unroll
+  for (int m = 1; m < 64; m *= 2) acc = acc + __shfl_xor(acc, m);
+  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) scale[co] = (float)(((wsum[0] + wsum[1]) + (wsum[2] + wsum[3])) / (double)k);
 }
 
 template <int BITS>
@@ -339,7 +363,7 @@ int launch_pack_act_f16(const float* x, int n, int c, int h, int w, uint32_t* ou
 
 int launch_pack_weight_f16(const float* w, int cout, int cin, int kh, int kw, uint32_t* out, float* scale,
                            hipStream_t s) {
-  weight_scale_kernel<<<ceil_div(cout, 64), 64, 0, s>>>(w, cout, cin * kh * kw, scale);
+  weight_scale_kernel<<<cout, 256, 0, s>>>(w, cin * kh * kw, scale);
   const int cwn = ceil_div(cin, 32);
   const int64_t total = (int64_t)kh * kw * 2 * cwn * cout_pad(cout);
   pack_weight_f16_kernel<<<dim3((unsigned)((total + 255) / 256)), 256, 0, s>>>(w, cout, cin, kh, kw, cwn,
@@ -350,7 +374,7 @@ int launch_pack_weight_f16(const float* w, int cout, int cin, int kh, int kw, ui
 int launch_pack_weight(const float* w, int cout, int cin, int kh, int kw, int bits,
                        const float* base_thr, uint32_t* out, float* scale, hipStream_t s) {
   const int k = cin * kh * kw;
-  weight_scale_kernel<<<ceil_div(cout, 64), 64, 0, s>>>(w, cout, k, scale);
+  weight_scale_kernel<<<cout, 256, 0, s>>>(w, k, scale);
   const int cwn = ceil_div(cin, 32);
   const int cop = cout_pad(cout);
   const int64_t total = (int64_t)kh * kw * cwn * cop;

@@ -106,6 +106,24 @@ def test_weight_scale_is_mean_abs(oracle_mod):
         assert abs(float(s[c]) - exact[c]) <= np.spacing(np.float32(exact[c]))
 
 
+def test_weight_scale_counts_every_weight(oracle_mod):
+    # Integer-valued weights: every partial sum and the total are exact in
+    # double, so s_c is the exact mean, rounded by the one division and the
+    # one conversion to float.  K = 37 * 3 * 3 = 333 is not a multiple of the
+    # 256 partial sums (a dropped or doubled tail element changes the mean);
+    # an all-zero channel and a channel of one large weight close the set.
+    rng = np.random.default_rng(3)
+    w = rng.integers(-1000, 1001, size=(6, 37, 3, 3)).astype(np.float32)
+    w[2] = 0.0
+    w[3] = 0.0
+    w[3, 36, 2, 2] = -(2.0 ** 40)
+    s = oracle_mod.weight_scale(w)
+    for c in range(6):
+        total = int(np.abs(w[c]).astype(np.float64).sum())  # exact: integers far below 2^53
+        mean = Fraction(total, w[c].size)
+        assert s[c] == np.float32(float(mean)), (c, s[c], float(mean))
+
+
 @pytest.mark.parametrize("bits", [2, 3])
 def test_weight_thresholds_scale_with_channel(oracle_mod, bits):
     # Thresholds are relative to s_c: scaling a channel by 2^k leaves its levels unchanged.
