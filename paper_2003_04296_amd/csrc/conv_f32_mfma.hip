@@ -24,7 +24,21 @@
 // running maximum).  Without pooling a tile is 8 conv rows x 32 columns,
 // one M-tile per row.  Tiles and windows wholly inside the image skip the
 // bounds checks.
+//
+// LDS banks (64 on gfx950).  An operand read is one ds_read_b32 of 64
+// lanes: lanes 0-31 read 32 consecutive tile pixels at one tap, lanes 32-63
+// the same pixels at the k-step's other tap.  With stride 2 the window is
+// stored split by row and column parity (odd columns 32 floats after the
+// even ones, rows 81 floats apart, odd rows at an offset of 32 mod 64), so
+// that the 32 pixels of a half fall in 32 consecutive banks and the taps are
+// paired so that the other half reads exactly 32 banks away: (ky, 2a) with
+// (ky, 2a + 1), then (2b, k - 1) with (2b + 1, k - 1), the last tap with a
+// zero-weight padding tap.  The conv tile of the pooling epilogue is stored
+// pixel-major (40 floats per pixel: the two halves of an accumulator
+// register land 32 banks apart) and read with lanes on channels and the two
+// halves on pooled columns two apart (again 32 banks apart).
 #include <stdio.h>
+#include <algorithm>
 #include <string.h>
 
 #include "qconv_internal.h"
@@ -37,9 +51,16 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 
 constexpr int PT_H = 7, PT_W = 8;    // pooled outputs per tile
 constexpr int PT_H0 = 8, PT_W0 = 32;  // conv tile without pooling
-constexpr int CT_STRIDE = 257;        // LDS floats per channel of the conv tile (odd: no bank conflicts)
+constexpr int CT_PITCH = 40;          // LDS floats per pixel of the pooling conv tile (pixel-major)
+constexpr int CT_PIX = 256;           // pixel slots of the pooling conv tile
+constexpr int PO_PITCH = PT_H * PT_W + 1;  // LDS floats per channel of the staged pooled tile
 constexpr int F32M_NJ = 16;           // input window elements per thread (windows up to 4096 floats)
 constexpr size_t F32M_LDS_MAX = 80 * 1024;  // two blocks per CU
+constexpr int S2_HW = 32;             // stride 2: offset of the odd-column phase within a row
+constexpr int S2_WP = 81;             // stride 2: row pitch (17 mod 64)
+
+// smallest v >= x with v = 32 (mod 64)
+__host__ __device__ constexpr int up_32mod64(int x) { return x <= 32 ? 32 : ((x - 32 + 63) / 64) * 64 + 32; }
 
 template <int KSZ, int S, int POOL>
 struct Geo {
@@ -47,9 +68,49 @@ struct Geo {
   static constexpr int CT_W = POOL ? 2 * PT_W + 1 : PT_W0;
   static constexpr int IH = (CT_H - 1) * S + KSZ;           // staged input window
   static constexpr int IW = (CT_W - 1) * S + KSZ;
-  static constexpr int WIN = IH * IW;
+  static constexpr int WIN = IH * IW;                       // window elements per input channel
   static constexpr int KK = KSZ * KSZ, KS2 = (KK + 1) / 2;  // taps, k-steps of two taps
+  // LDS floats per input channel of the staged window, and the offset of
+  // the odd-row phase (stride 2)
+  static constexpr int HRP = S == 2 ? up_32mod64(((IH + 1) / 2) * S2_WP) : 0;
+  static constexpr int CIP = S == 2 ? HRP + (IH / 2) * S2_WP : WIN;
+  static_assert(S == 1 || ((IW + 1) / 2 <= S2_HW && S2_HW + IW / 2 <= S2_WP), "stride-2 row layout");
 };
+
+// Taps of k-step st: t0 (lanes 0-31) and t1 (lanes 32-63; -1 = padding).
+// Stride 1: taps 2 st and 2 st + 1 in OIHW order.  Stride 2: the pairing
+// that puts the two taps 32 banks apart in the phase-split window.
+template <int KSZ, int S>
+__host__ __device__ constexpr int step_tap(int st, int half) {
+  constexpr int KK = KSZ * KSZ;
+  if (S == 1) {
+    const int t = 2 * st + half;
+    return t < KK ? t : -1;
+  }
+  constexpr int HP = (KSZ - 1) / 2;  // column pairs per row
+  constexpr int NCOL = KSZ * HP;
+  if (st < NCOL) return (st / HP) * KSZ + 2 * (st % HP) + half;
+  if (st < NCOL + HP) return (2 * (st - NCOL) + half) * KSZ + KSZ - 1;
+  return half ? -1 : KK - 1;
+}
+
+// Whether the lanes 32-63 of k-step st read through the second base (the
+// odd-row phase with stride 2, the next window row with stride 1).
+template <int KSZ, int S>
+__host__ __device__ constexpr bool step_row(int st) {
+  if (S == 1) return (2 * st) % KSZ == KSZ - 1;
+  constexpr int HP = (KSZ - 1) / 2;
+  return st >= KSZ * HP && st < KSZ * HP + HP;
+}
+
+// Offset of tap t inside one channel's staged window.
+template <int KSZ, int S, int POOL>
+__host__ __device__ constexpr int tap_off(int t) {
+  using G = Geo<KSZ, S, POOL>;
+  const int ky = t / KSZ, kx = t % KSZ;
+  if (S == 1) return ky * G::IW + kx;
+  return (ky & 1) * G::HRP + (ky >> 1) * S2_WP + (kx & 1) * S2_HW + (kx >> 1);
+}
 
 struct F32M {
   const float* x;
@@ -66,55 +127,58 @@ struct F32M {
   uint32_t* out_packed;
   int out_cw;
   Thr othr;
-  int l_w, l_ct, l_pk;  // LDS float offsets: weights, conv tile, packed staging (window at 0)
+  int l_w, l_pk;  // LDS float offsets: weights, packed staging (window / conv tile region at 0)
 };
-
-// Tap t (t < KK) as an offset inside the window.
-template <int KSZ, int IW>
-__host__ __device__ constexpr int tap_off(int t) {
-  return (t / KSZ) * IW + (t % KSZ);
-}
 
 template <int KSZ, int S, int POOL, int OB>
 __global__ __launch_bounds__(256, 2) void conv_f32_mfma_kernel(const F32M m) {
   using G = Geo<KSZ, S, POOL>;
-  constexpr int KK = G::KK, KS2 = G::KS2, IW = G::IW, WIN = G::WIN, CT_W = G::CT_W;
+  constexpr int KS2 = G::KS2, IW = G::IW, WIN = G::WIN, CIP = G::CIP, CT_W = G::CT_W;
   extern __shared__ __attribute__((aligned(16))) float fl[];
   float* xin = fl;
   float* wB = fl + m.l_w;
-  float* ctile = fl + m.l_ct;
+  float* ctile = fl;                       // pooling: conv tile over the consumed window
+  float* ptile = fl + CT_PIX * CT_PITCH;   // pooling: staged fp32 pooled tile
   uint32_t* pk = reinterpret_cast<uint32_t*>(fl + m.l_pk);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
   const int ct = blockIdx.x % m.co_tiles;
   const int co_blk = ct * 32;
 
-  // weights of the block's 32 channels, [ci][2 KS2 taps][32] (padding taps 0)
-  for (int i = tid; i < m.cin * 2 * KS2 * 32; i += 256) {
-    const int c = i & 31, r = i >> 5, ci = r / (2 * KS2), kq = r - ci * (2 * KS2), co = co_blk + c;
-    wB[i] = (kq < KK && co < m.cout) ? m.wt[((int64_t)co * m.cin + ci) * KK + kq] : 0.0f;
+  // weights of the block's 32 channels, [ci][k-step][half][32] (padding taps 0)
+  for (int i = tid; i < m.cin * KS2 * 64; i += 256) {
+    const int c = i & 31, h = (i >> 5) & 1, r = i >> 6, ci = r / KS2, st = r - ci * KS2, co = co_blk + c;
+    const int tap = step_tap<KSZ, S>(st, h);
+    wB[i] = (tap >= 0 && co < m.cout) ? m.wt[((int64_t)co * m.cin + ci) * G::KK + tap] : 0.0f;
   }
   // per-channel epilogue parameters of this lane's channel
   const int co_l = co_blk + l32;
   const bool cok = co_l < m.cout;
   const float bk = cok ? m.bn_k[co_l] : 0.0f, bb = cok ? m.bn_b[co_l] : 0.0f;
+  // Wait for these loads here: used inside the item loop's conditional
+  // blocks, a value still counted as in flight makes the compiler wait
+  // for every load in flight there, the next window's prefetch included.
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
 
-  // The input window is cin * WIN floats; thread t owns elements t + 256 j.
-  // Their offset inside one image, and their window row / column, are the
-  // same for every item, so they are computed once.
+  // The input window is cin * WIN elements; thread t owns elements t + 256 j.
+  // Their offset inside one image, their window row / column and their LDS
+  // slot are the same for every item, so they are computed once.
   const int welems = m.cin * WIN;
   const int64_t img_elems = (int64_t)m.cin * m.h * m.w;
   int eoff[F32M_NJ];      // ci * h * w + yy * w + xx (window origin at 0, 0)
   uint32_t eyx[F32M_NJ];  // yy << 16 | xx, or all ones past the window
+  int edst[F32M_NJ];      // LDS slot (past the window: the spare slot after it)
 #pragma unroll
   for (int j = 0; j < F32M_NJ; ++j) {
     const int e = tid + 256 * j;
     eoff[j] = 0;
     eyx[j] = 0xFFFFFFFFu;
+    edst[j] = m.cin * CIP;
     if (e < welems) {
       const int ci = e / WIN, r = e - ci * WIN, yy = r / IW, xx = r - (r / IW) * IW;
       eoff[j] = (ci * m.h + yy) * m.w + xx;
       eyx[j] = ((uint32_t)yy << 16) | (uint32_t)xx;
+      edst[j] = S == 2 ? ci * CIP + (yy & 1) * G::HRP + (yy >> 1) * S2_WP + (xx & 1) * S2_HW + (xx >> 1) : e;
     }
   }
   float wval[F32M_NJ];
@@ -126,69 +190,72 @@ __global__ __launch_bounds__(256, 2) void conv_f32_mfma_kernel(const F32M m) {
     *cy0 = POOL ? 2 * *ty * PT_H - 1 : *ty * PT_H0;
     *cx0 = POOL ? 2 * *tx * PT_W - 1 : *tx * PT_W0;
   };
+  // One buffer load per element through a resource over the tile's image:
+  // elements outside the image or past the window get an offset past the
+  // buffer's end and read 0 without a memory access, so the loads go out
+  // back to back with no mask applied after them.
   auto load_window = [&](int item) __attribute__((always_inline)) {
     int img, ty, tx, cy0, cx0;
     origin(item, &img, &ty, &tx, &cy0, &cx0);
     const int iy0 = cy0 * S - m.pad, ix0 = cx0 * S - m.pad;
-    const float* xb = m.x + (int64_t)img * img_elems;
-    const int64_t org = (int64_t)iy0 * m.w + ix0;  // may be negative: added only to in-image elements
-    if (iy0 >= 0 && iy0 + G::IH <= m.h && ix0 >= 0 && ix0 + IW <= m.w) {
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(m.x + (int64_t)img * img_elems), (short)0, (int)(img_elems * 4), 0x00020000);
+    const int org = iy0 * m.w + ix0;  // may be negative: added only to in-image elements
+    const bool inside = iy0 >= 0 && iy0 + G::IH <= m.h && ix0 >= 0 && ix0 + IW <= m.w;
 #pragma unroll
-      for (int j = 0; j < F32M_NJ; ++j) wval[j] = eyx[j] != 0xFFFFFFFFu ? xb[org + eoff[j]] : 0.0f;
-    } else {
-#pragma unroll
-      for (int j = 0; j < F32M_NJ; ++j) {
+    for (int j = 0; j < F32M_NJ; ++j) {
+      bool ok = eyx[j] != 0xFFFFFFFFu;
+      if (!inside) {
         const int gy = iy0 + (int)(eyx[j] >> 16), gx = ix0 + (int)(eyx[j] & 0xFFFFu);
-        const bool ok = eyx[j] != 0xFFFFFFFFu && gy >= 0 && gy < m.h && gx >= 0 && gx < m.w;
-        wval[j] = ok ? xb[org + eoff[j]] : 0.0f;
+        ok = ok && gy >= 0 && gy < m.h && gx >= 0 && gx < m.w;
       }
+      const int voff = ok ? (org + eoff[j]) * 4 : 0x7FFFFFF0;
+      wval[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, voff, 0, 0));
     }
   };
   const int first = blockIdx.x / m.co_tiles, step_items = gridDim.x / m.co_tiles;
   if (first < m.items) load_window(first);
 
-  // per-lane pixel bases of the wave's two M-tiles (the unused pooled row
-  // reads pixel 0; its result is dropped)
-  int pb[2];
+  // per-lane operand bases of the wave's two M-tiles (the unused pooled row
+  // reads pixel 0; its result is dropped): lanes 32-63 read the k-step's
+  // second tap through base A (next column phase / next column) or base B
+  // (odd-row phase / next window row)
+  int bA[2], bB[2];
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
     const int pi = (wave * 2 + t) * 32 + l32;
     const int pc = pi < G::CT_H * CT_W ? pi : 0;
-    pb[t] = (pc / CT_W) * S * IW + (pc % CT_W) * S;
+    const int pr = pc / CT_W, pcol = pc - (pc / CT_W) * CT_W;
+    const int pb = S == 2 ? pr * S2_WP + pcol : pr * IW + pcol;
+    bA[t] = pb + half * (S == 2 ? S2_HW : 1);
+    bB[t] = pb + half * (S == 2 ? G::HRP : IW - (KSZ - 1));
   }
-  // lanes of the upper half take the second tap of each k-step: one window
-  // column further, or the first column of the next row
-  const int dh_col = half, dh_row = half * (IW - (KSZ - 1));
 
   for (int item = first; item < m.items; item += step_items) {
     int img, ty, tx, cy0, cx0;
     origin(item, &img, &ty, &tx, &cy0, &cx0);
     lds_barrier();  // the previous item's LDS tiles are consumed
 #pragma unroll
-    for (int j = 0; j < F32M_NJ; ++j)
-      if (eyx[j] != 0xFFFFFFFFu) xin[tid + 256 * j] = wval[j];
+    for (int j = 0; j < F32M_NJ; ++j) xin[edst[j]] = wval[j];  // elements past the window land on the spare slot
     lds_barrier();
     if (item + step_items < m.items) load_window(item + step_items);
 
     // ---- MFMAs: this wave's 2 M-tiles x 32 channels ----
     v16f acc0 = {}, acc1 = {};
     for (int ci = 0; ci < m.cin; ++ci) {
-      const float* xc0 = xin + ci * WIN + pb[0];
-      const float* xc1 = xin + ci * WIN + pb[1];
-      const float* x0c = xc0 + dh_col;  // a k-step whose two taps share a row
-      const float* x1c = xc1 + dh_col;
-      const float* x0r = xc0 + dh_row;  // a k-step whose second tap starts the next row
-      const float* x1r = xc1 + dh_row;
-      const float* wc = wB + ci * (2 * KS2 * 32) + half * 32 + l32;
+      const float* xa0 = xin + ci * CIP + bA[0];
+      const float* xa1 = xin + ci * CIP + bA[1];
+      const float* xb0 = xin + ci * CIP + bB[0];
+      const float* xb1 = xin + ci * CIP + bB[1];
+      const float* wc = wB + ci * (KS2 * 64) + half * 32 + l32;
 #pragma unroll
       for (int st = 0; st < KS2; ++st) {
-        const int t0 = 2 * st;
-        const bool wrap = (t0 % KSZ) == KSZ - 1;  // taps 2 st and 2 st + 1 on different rows
-        const int o = tap_off<KSZ, IW>(t0);
-        float a0 = wrap ? x0r[o] : x0c[o];
-        float a1 = wrap ? x1r[o] : x1c[o];
-        if (st == KS2 - 1 && (KK % 2 == 1) && half) {
-          a0 = 0.0f;  // the padding tap of an odd KK: keep the operand of its zero weight finite
+        const int o = tap_off<KSZ, S, POOL>(step_tap<KSZ, S>(st, 0));
+        const bool rowb = step_row<KSZ, S>(st);
+        float a0 = rowb ? xb0[o] : xa0[o];
+        float a1 = rowb ? xb1[o] : xa1[o];
+        if (step_tap<KSZ, S>(st, 1) < 0 && half) {
+          a0 = 0.0f;  // the padding tap: keep the operand of its zero weight finite
           a1 = 0.0f;
         }
         const float bv = wc[st * 64];
@@ -200,72 +267,87 @@ __global__ __launch_bounds__(256, 2) void conv_f32_mfma_kernel(const F32M m) {
     // ---- epilogue ----
     // register v of lane l: channel co_blk + l % 32, tile pixel 32 T + 8 (v / 4) + 4 (l / 32) + v % 4
     if constexpr (POOL) {
+      lds_barrier();  // every wave's operand reads are done: the conv tile overwrites the window
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int pi = (wave * 2 + t) * 32 + 8 * (v / 4) + 4 * half + (v % 4);
           float z = fmaf(bk, t == 0 ? acc0[v] : acc1[v], bb);
-          if (m.relu) z = (z > 0.0f) ? z : 0.0f;
-          if (pi < G::CT_H * CT_W) ctile[l32 * CT_STRIDE + pi] = z;
+          z = (m.relu && !(z > 0.0f)) ? 0.0f : z;
+          // the unused pixel 255 holds -inf: the pooling reads it for taps
+          // outside the conv output
+          if (t == 1 && v == 15) z = (wave == 3 && half) ? -INFINITY : z;
+          ctile[pi * CT_PITCH + l32] = z;
         }
-      }
-      if constexpr (OB > 0) {
-        for (int i = tid; i < PT_H * PT_W * planes_of(OB); i += 256) pk[i] = 0u;
       }
       lds_barrier();
-      // pooling: thread -> (pooled pixel of the tile, the wave's 8 channels)
-      const int pp = tid & 63, cq = wave;
-      const int pyl = pp / PT_W, pxl = pp - (pp / PT_W) * PT_W;
-      const int py = ty * PT_H + pyl, px = tx * PT_W + pxl;
+      // pooling: lane -> channel, wave / half -> one pooled column (the
+      // halves two columns apart), all PT_H pooled rows of it, from the row
+      // maxima of the 15 conv rows
+      const int pxl = ((wave >> 1) << 2) + (wave & 1) + 2 * half;
+      const int px = tx * PT_W + pxl;
       const bool interior = cy0 >= 0 && cy0 + G::CT_H <= m.ho && cx0 >= 0 && cx0 + CT_W <= m.wo;
-      if (pp < PT_H * PT_W && py < m.oh && px < m.ow) {
-        constexpr int P = OB > 0 ? planes_of(OB) : 1;
-        uint32_t bits[P];
+      bool vx[3];
 #pragma unroll
-        for (int p = 0; p < P; ++p) bits[p] = 0u;
-        const float* cb = ctile + cq * 8 * CT_STRIDE + (2 * pyl) * CT_W + 2 * pxl;
-        // window taps inside the conv output (all of them in an interior tile)
-        bool vy[3], vx[3];
+      for (int d = 0; d < 3; ++d) {
+        const int gx = cx0 + 2 * pxl + d;
+        vx[d] = interior || (gx >= 0 && gx < m.wo);
+      }
+      float rmax[G::CT_H];
+      if (interior) {
 #pragma unroll
-        for (int d = 0; d < 3; ++d) {
-          const int gy = cy0 + 2 * pyl + d, gx = cx0 + 2 * pxl + d;
-          vy[d] = interior || (gy >= 0 && gy < m.ho);
-          vx[d] = interior || (gx >= 0 && gx < m.wo);
+        for (int r = 0; r < G::CT_H; ++r) {
+          const float* cp = ctile + (r * CT_W + 2 * pxl) * CT_PITCH + l32;
+          rmax[r] = fmaxf(fmaxf(cp[0], cp[CT_PITCH]), cp[2 * CT_PITCH]);  // a NaN never replaces the maximum
         }
+      } else {
+        // taps outside the conv output read the -inf of pixel 255
+        const float* sent = ctile + 255 * CT_PITCH + l32;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int co = co_blk + cq * 8 + j;
+        for (int r = 0; r < G::CT_H; ++r) {
+          const int gy = cy0 + r;
+          const bool vy = gy >= 0 && gy < m.ho;
+          const float* cp = ctile + (r * CT_W + 2 * pxl) * CT_PITCH + l32;
           float mx = -INFINITY;
 #pragma unroll
-          for (int dy = 0; dy < 3; ++dy)
-#pragma unroll
-            for (int dx = 0; dx < 3; ++dx) {
-              const float v = cb[j * CT_STRIDE + dy * CT_W + dx];
-              if (vy[dy] && vx[dx]) mx = fmaxf(mx, v);  // a NaN never replaces the maximum
-            }
-          if (co < m.cout) {
-            if (m.out) m.out[(((int64_t)img * m.cout + co) * m.oh + py) * m.ow + px] = mx;
-            if constexpr (OB > 0) {
-              const uint32_t qv = quant_planes<OB>(hardtanh(mx), m.othr);
-#pragma unroll
-              for (int p = 0; p < P; ++p) bits[p] |= ((qv >> p) & 1u) << j;
-            }
-          }
-        }
-        if constexpr (OB > 0) {
-#pragma unroll
-          for (int p = 0; p < P; ++p) atomicOr(&pk[pp * P + p], bits[p] << (8 * cq));
+          for (int d = 0; d < 3; ++d) mx = fmaxf(mx, *((vy && vx[d]) ? cp + d * CT_PITCH : sent));
+          rmax[r] = mx;
         }
       }
-      if constexpr (OB > 0) {
-        constexpr int P = planes_of(OB);
+#pragma unroll
+      for (int p = 0; p < PT_H; ++p) {
+        const float z = fmaxf(fmaxf(rmax[2 * p], rmax[2 * p + 1]), rmax[2 * p + 2]);
+        const int py = ty * PT_H + p;
+        if (m.out) ptile[l32 * PO_PITCH + p * PT_W + pxl] = z;
+        if constexpr (OB > 0) {
+          // one ballot per plane: lanes 0-31 give the word of (py, px) of
+          // the lower half, lanes 32-63 that of the upper half
+          constexpr int P = planes_of(OB);
+          const uint32_t qv = cok ? quant_planes<OB>(hardtanh(z), m.othr) : 0u;
+          const bool ok = py < m.oh && px < m.ow;
+#pragma unroll
+          for (int q = 0; q < P; ++q) {
+            const uint64_t bl = __ballot((qv >> q) & 1u);
+            const uint32_t word = half ? (uint32_t)(bl >> 32) : (uint32_t)bl;
+            if (l32 == 0 && ok)
+              m.out_packed[((((int64_t)img * m.oh + py) * m.ow + px) * m.out_cw + ct) * P + q] = word;
+          }
+        }
+      }
+      if (m.out) {
         lds_barrier();
-        for (int i = tid; i < PT_H * PT_W * P; i += 256) {
-          const int qq = i / P, p = i - (i / P) * P;
-          const int qy = ty * PT_H + qq / PT_W, qx = tx * PT_W + qq % PT_W;
-          if (qy < m.oh && qx < m.ow)
-            m.out_packed[((((int64_t)img * m.oh + qy) * m.ow + qx) * m.out_cw + ct) * P + p] = pk[i];
+        // the staged pooled tile out in rows of 8 pixels: thread -> (pooled
+        // pixel of the tile, the wave's 8 channels)
+        const int pp = tid & 63;
+        const int pyl = pp / PT_W, pxo = pp - (pp / PT_W) * PT_W;
+        const int py = ty * PT_H + pyl, pxg = tx * PT_W + pxo;
+        if (pp < PT_H * PT_W && py < m.oh && pxg < m.ow) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const int c = wave * 8 + j, co = co_blk + c;
+            if (co < m.cout) m.out[(((int64_t)img * m.cout + co) * m.oh + py) * m.ow + pxg] = ptile[c * PO_PITCH + pp];
+          }
         }
       }
     } else {
@@ -338,12 +420,16 @@ int device_cus_f() {
   return v;
 }
 
-// Window of a tile for kernel size k and stride s (run-time mirror of Geo).
-void geo_rt(int k, int s, int pool, int* ih, int* iw) {
+// Window of a tile for kernel size k and stride s, and its LDS floats per
+// input channel (run-time mirror of Geo).
+void geo_rt(int k, int s, int pool, int* ih, int* iw, int* cip) {
   const int ct_h = pool ? 2 * PT_H + 1 : PT_H0, ct_w = pool ? 2 * PT_W + 1 : PT_W0;
   *ih = (ct_h - 1) * s + k;
   *iw = (ct_w - 1) * s + k;
+  *cip = s == 2 ? up_32mod64(((*ih + 1) / 2) * S2_WP) + (*ih / 2) * S2_WP : *ih * *iw;
 }
+
+size_t f32m_lds(const F32M& m, int pool);
 
 bool f32m_plan(int n, int cin, int h, int w, int cout, int k, int stride, int pad, int pool, F32M* m) {
   memset(m, 0, sizeof(*m));
@@ -359,10 +445,12 @@ bool f32m_plan(int n, int cin, int h, int w, int cout, int k, int stride, int pa
   if (h + 2 * pad < k || w + 2 * pad < k) return false;
   m->ho = (h + 2 * pad - k) / stride + 1;
   m->wo = (w + 2 * pad - k) / stride + 1;
-  int ih, iw;
-  geo_rt(k, stride, pool, &ih, &iw);
+  int ih, iw, cip;
+  geo_rt(k, stride, pool, &ih, &iw, &cip);
   if ((int64_t)cin * ih * iw > 256 * F32M_NJ) return false;  // the window's register share
-  if ((int64_t)cin * h * w >= ((int64_t)1 << 31) || ih >= (1 << 16) || iw >= (1 << 16)) return false;
+  // one image's bytes fit a buffer resource, with the out-of-range offset
+  // 0x7FFFFFF0 past its end
+  if ((int64_t)cin * h * w * 4 >= 0x7FFFFFF0 || ih >= (1 << 16) || iw >= (1 << 16)) return false;
   if (pool) {
     m->oh = (m->ho - 1) / 2 + 1;
     m->ow = (m->wo - 1) / 2 + 1;
@@ -378,16 +466,18 @@ bool f32m_plan(int n, int cin, int h, int w, int cout, int k, int stride, int pa
   const int64_t items = (int64_t)n * m->tiles_y * m->tiles_x;
   if (items * m->co_tiles >= ((int64_t)1 << 31)) return false;
   m->items = (int)items;
+  // LDS: the staged window (with pooling also the conv tile and the staged
+  // pooled tile over it), the weights, then (plain tiles) the packed staging
   const int taps2 = 2 * ((k * k + 1) / 2);  // padded taps per input channel
-  m->l_w = (cin * ih * iw + 3) & ~3;
-  m->l_ct = m->l_w + cin * taps2 * 32;
-  m->l_pk = m->l_ct + (pool ? 32 * CT_STRIDE : 0);
-  const int pk_words = pool ? PT_H * PT_W * 4 : PT_H0 * PT_W0 * 4;
-  return (size_t)(m->l_pk + pk_words) * 4 <= F32M_LDS_MAX;
+  int64_t region = (int64_t)cin * cip + 1;  // + the spare slot of the elements past the window
+  if (pool) region = std::max<int64_t>(region, (int64_t)CT_PIX * CT_PITCH + 32 * PO_PITCH);
+  m->l_w = (int)((region + 3) & ~(int64_t)3);
+  m->l_pk = m->l_w + cin * taps2 * 32;
+  return f32m_lds(*m, pool) <= F32M_LDS_MAX;
 }
 
 size_t f32m_lds(const F32M& m, int pool) {
-  return (size_t)(m.l_pk + (pool ? PT_H * PT_W * 4 : PT_H0 * PT_W0 * 4)) * 4;
+  return (size_t)(m.l_pk + (pool ? 0 : PT_H0 * PT_W0 * 4)) * 4;
 }
 
 template <int KSZ, int S, int POOL>
