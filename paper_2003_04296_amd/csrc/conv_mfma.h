@@ -1489,12 +1489,16 @@ __global__ __launch_bounds__(1024, 1) void conv_mfma_pp_kernel(const MfmaArgs m)
         const int co32 = co_w + 32 * j;
         if (st && co32 < a.cout) {
           const int T = wm * MT + i;
-          if (a.mode == QCONV_EPI_INT32)
+          if (a.mode == QCONV_EPI_INT32) {
             tile_epilogue_swap<K_INT32, 0>(m, acc[i][j], pimg0, pu0, T, co32, co_blk, prm, plane);
-          else if (a.mode == QCONV_EPI_SCALE_F32)
+          } else if (a.mode == QCONV_EPI_SCALE_F32) {
             tile_epilogue_swap<K_SCALE, 0>(m, acc[i][j], pimg0, pu0, T, co32, co_blk, prm, plane);
-          else
+          } else if (a.mode == QCONV_EPI_BN_PACK) {
+            // the packed output alone (its width is the input's: OB)
+            if constexpr (OB > 0) tile_epilogue_swap<K_PACK, 0, OB>(m, acc[i][j], pimg0, pu0, T, co32, co_blk, prm, plane);
+          } else {
             bn_tile(std::integral_constant<int, 0>{}, acc[i][j], T, co32, nullptr);
+          }
         }
         if constexpr (TT < NI) expand_one(std::integral_constant<int, TT>{});
       });

@@ -138,7 +138,9 @@ size_t block_lds(const MfmaArgs& m) { return 2 * PARAM_BYTES + (size_t)m.buf_byt
 // one or more 256-row items per CU the unsplit shapes are faster, with fewer
 // the split one); split-K too when the 256-row input tile does not fit the
 // staging buffer.
-int pick_cfg(const ConvArgs& a) {
+bool use_pp(const MfmaArgs& m, int cfg, int cus);
+
+int pick_cfg_base(const ConvArgs& a) {
   const int big = a.cout <= 64 ? 1 : 0;
   MfmaArgs m;
   if (!plan(a, big, &m)) {
@@ -158,6 +160,19 @@ int pick_cfg(const ConvArgs& a) {
     if (plan(a, 2, &s)) return 2;
   }
   return big;
+}
+
+// The store-overlapped kernel needs two items per CU: a layer whose
+// 128-channel items are too few for it takes 64-channel items when those
+// are enough (its epilogue then runs beside the other group's MFMAs instead
+// of after them).
+int pick_cfg(const ConvArgs& a) {
+  const int cfg = pick_cfg_base(a);
+  if (cfg != 0) return cfg;
+  MfmaArgs m0, m1;
+  const int cus = device_cus();
+  if (plan(a, 0, &m0) && !use_pp(m0, 0, cus) && plan(a, 1, &m1) && use_pp(m1, 1, cus)) return 1;
+  return 0;
 }
 
 // The swapped orientation serves unpacked, unpooled outputs whose byte size
@@ -190,17 +205,27 @@ size_t pp_lds(const MfmaArgs& m, int cfg) {
   return PARAM_BYTES + (size_t)m.c.kh * m.c.kw * m.ksteps * bco * 32 + (size_t)m.buf_bytes * 2;
 }
 
-// The ping-pong kernel serves 256-row shapes with unpacked, unpooled outputs
-// whose channels fit one stage and whose weights fit next to two halo
-// buffers, when every block gets at least one item per group.
+// The ping-pong kernel serves 256-row shapes with unpooled outputs whose
+// channels fit one stage and whose weights fit next to two halo buffers,
+// when every block gets at least one item per group.
 bool use_pp(const MfmaArgs& m, int cfg, int cus) {
   if (cfg == 2 || m.c.mfma_op == OP_F16 || !use_swap(m) || m.nchunks != 1 || m.act_bytes == 0) return false;
-  // unpacked outputs; a packed copy of a BN output rides along when its
-  // width is the input's (the case of a network of one activation width)
-  if (m.c.mode == QCONV_EPI_BN_PACK) return false;
-  if (m.c.out_packed != nullptr && (m.c.mode != QCONV_EPI_BN_F32 || m.c.out_bits != m.c.a_bits)) return false;
+  // packed outputs (alone, or as the copy of a BN output) of the input's
+  // width (the case of a network of one activation width)
+  if (m.c.out_packed != nullptr &&
+      ((m.c.mode != QCONV_EPI_BN_F32 && m.c.mode != QCONV_EPI_BN_PACK) || m.c.out_bits != m.c.a_bits))
+    return false;
   if (pp_lds(m, cfg) > (size_t)LDS_PER_CU) return false;
-  return (int64_t)m.tiles_px * m.tiles_co >= 2 * (int64_t)cus;
+  if ((int64_t)m.tiles_px * m.tiles_co < 2 * (int64_t)cus) return false;
+  // a packed output alone: only where the base kernel's own shape leaves
+  // fewer than two items per CU (measured on ResNet-18 and ConvNet layers:
+  // with 2-3 items per CU of the base kernel its blocks overlap each other
+  // better than the two groups do; with one item per CU the groups win)
+  if (m.c.mode == QCONV_EPI_BN_PACK) {
+    MfmaArgs b;
+    if (plan(m.c, pick_cfg_base(m.c), &b) && (int64_t)b.tiles_px * b.tiles_co >= 2 * (int64_t)cus) return false;
+  }
+  return true;
 }
 
 

@@ -434,6 +434,60 @@ def test_pp_kernel_packed_copy(dev, ci, bits, resid):
     assert tail_bits_zero(outp.cpu().numpy(), cout, ab)
 
 
+PP_PACK_CASES = [
+    # n, cin, h, w, cout, k, stride, pad: layers whose base-kernel items are
+    # fewer than two per CU, so that a packed output alone takes the
+    # store-overlapped kernel (on 64-channel items)
+    (64, 128, 28, 28, 128, 3, 1, 1),   # ResNet-18's 128-channel layer shape
+    (64, 96, 28, 30, 100, 3, 1, 1),    # ragged channels, cin padded to a k-step, ragged last items
+    (66, 64, 28, 28, 128, 3, 1, 1),    # odd item count per image row of blocks
+]
+
+
+@pytest.mark.parametrize("bits", [(2, 1), (1, 1), (3, 3), (2, 2)])
+@pytest.mark.parametrize("ci", [0, 1, 2])
+def test_pp_kernel_packed_output(dev, ci, bits):
+    """BN -> Q(HardTanh(z)) packed output alone (a network layer feeding only
+    the next quantized conv) on the store-overlapped kernel."""
+    case = PP_PACK_CASES[ci]
+    n, cin, h, w, cout, k, s, p = case
+    ab, wb = bits
+    name = q.kernel_name(n, cin, h, w, cout, k, s, p, ab, wb, mode=q.EPI_BN_PACK, out_bits=ab, packed_out=True)
+    assert name.startswith("conv_mfma_pp_kernel<1,") and name.endswith(f", {ab}>"), name
+    x, wt = _inputs(360 + ci + ab, n, cin, h, w, cout, k)
+    kk, bb = _bn(360 + ci, cout)
+    ho, wo = q.out_size(h, k, s, p), q.out_size(w, k, s, p)
+    act = q.pack_act(x.to(dev), ab)
+    wq, _ = q.pack_weight(wt.to(dev), wb)
+    _, outp = q.conv(act, wq, n, cin, h, w, cout, k, s, p, ab, wb, mode=q.EPI_BN_PACK, bn_k=kk.to(dev),
+                     bn_b=bb.to(dev), out_bits=ab)
+    torch.cuda.synchronize()
+    acc, _ = _oracle_acc(x, wt, ab, wb, s, p)
+    z = oracle.epi_bn(acc, kk.numpy(), bb.numpy(), oracle.level_shift(ab) + oracle.level_shift(wb))
+    np.testing.assert_array_equal(unpack_act(outp.cpu().numpy(), n, cout, ho, wo, ab),
+                                  oracle.quantize(oracle.hardtanh(z), ab))
+    assert tail_bits_zero(outp.cpu().numpy(), cout, ab)
+
+
+def test_pp_kernel_takes_64_channel_items_when_128_are_too_few(dev):
+    """A 128-channel layer whose 256-row x 128-channel items are fewer than two
+    per CU runs the store-overlapped kernel on 256 x 64 items, bit-exact."""
+    n, cin, h, w, cout = 64, 128, 28, 28, 128
+    name = q.kernel_name(n, cin, h, w, cout, 3, 1, 1, 2, 2, mode=q.EPI_BN_PACK, out_bits=2, packed_out=True)
+    assert name == "conv_mfma_pp_kernel<1, 2, 1, 2>", name
+    x, wt = _inputs(371, n, cin, h, w, cout, 3)
+    kk, bb = _bn(371, cout)
+    act = q.pack_act(x.to(dev), 2)
+    wq, _ = q.pack_weight(wt.to(dev), 2)
+    _, outp = q.conv(act, wq, n, cin, h, w, cout, 3, 1, 1, 2, 2, mode=q.EPI_BN_PACK, bn_k=kk.to(dev),
+                     bn_b=bb.to(dev), out_bits=2)
+    torch.cuda.synchronize()
+    acc, _ = _oracle_acc(x, wt, 2, 2, 1, 1)
+    z = oracle.epi_bn(acc, kk.numpy(), bb.numpy(), 0)
+    np.testing.assert_array_equal(unpack_act(outp.cpu().numpy(), n, cout, h, w, 2),
+                                  oracle.quantize(oracle.hardtanh(z), 2))
+
+
 def test_pp_kernel_repeated_launches_agree(dev):
     """Back-to-back launches on one stream (the second overlapping the first's
     drained stores) give identical outputs, also after an unrelated launch."""
