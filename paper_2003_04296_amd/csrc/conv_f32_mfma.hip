@@ -55,6 +55,7 @@ constexpr int CT_PITCH = 40;          // LDS floats per pixel of the pooling con
 constexpr int CT_PIX = 256;           // pixel slots of the pooling conv tile
 constexpr int PO_PITCH = PT_H * PT_W + 1;  // LDS floats per channel of the staged pooled tile
 constexpr int F32M_NJ = 16;           // input window elements per thread (windows up to 4096 floats)
+constexpr int NCT_MAX = 4;            // 32-channel tiles per block over one staged window (plain tiles)
 constexpr size_t F32M_LDS_MAX = 80 * 1024;  // two blocks per CU
 constexpr int S2_HW = 32;             // stride 2: offset of the odd-column phase within a row
 constexpr int S2_WP = 81;             // stride 2: row pitch (17 mod 64)
@@ -123,6 +124,7 @@ struct F32M {
   int relu;
   int oh, ow;  // layer output (pooled when pooling)
   int tiles_y, tiles_x, co_tiles, items;
+  int nct, co_groups;  // 32-channel tiles per block (plain tiles: up to 4 over one staged window), blocks per item
   float* out;
   uint32_t* out_packed;
   int out_cw;
@@ -142,19 +144,29 @@ __global__ __launch_bounds__(256, 2) void conv_f32_mfma_kernel(const F32M m) {
   uint32_t* pk = reinterpret_cast<uint32_t*>(fl + m.l_pk);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
-  const int ct = blockIdx.x % m.co_tiles;
-  const int co_blk = ct * 32;
+  // the block's channel tiles ct0 .. ct0 + nct - 1 (pooled tiles: one; the
+  // last group of a layer whose tile count is not a multiple of m.nct has
+  // fewer)
+  const int ct0 = (blockIdx.x % m.co_groups) * (POOL ? 1 : m.nct);
+  const int nct = POOL ? 1 : min(m.nct, m.co_tiles - ct0);
 
-  // weights of the block's 32 channels, [ci][k-step][half][32] (padding taps 0)
-  for (int i = tid; i < m.cin * KS2 * 64; i += 256) {
-    const int c = i & 31, h = (i >> 5) & 1, r = i >> 6, ci = r / KS2, st = r - ci * KS2, co = co_blk + c;
+  // weights of the block's channels, [tile][ci][k-step][half][32] (padding
+  // taps and channels past cout 0)
+  for (int i = tid; i < nct * m.cin * KS2 * 64; i += 256) {
+    const int c = i & 31, h = (i >> 5) & 1, r = i >> 6, cq = r / (m.cin * KS2), r2 = r - cq * (m.cin * KS2);
+    const int ci = r2 / KS2, st = r2 - ci * KS2, co = (ct0 + cq) * 32 + c;
     const int tap = step_tap<KSZ, S>(st, h);
     wB[i] = (tap >= 0 && co < m.cout) ? m.wt[((int64_t)co * m.cin + ci) * G::KK + tap] : 0.0f;
   }
-  // per-channel epilogue parameters of this lane's channel
-  const int co_l = co_blk + l32;
-  const bool cok = co_l < m.cout;
-  const float bk = cok ? m.bn_k[co_l] : 0.0f, bb = cok ? m.bn_b[co_l] : 0.0f;
+  // per-channel epilogue parameters of this lane's channel in each tile
+  float bkv[NCT_MAX], bbv[NCT_MAX];
+#pragma unroll
+  for (int cq = 0; cq < NCT_MAX; ++cq) {
+    const int co = (ct0 + cq) * 32 + l32;
+    const bool ok = cq < nct && co < m.cout;
+    bkv[cq] = ok ? m.bn_k[co] : 0.0f;
+    bbv[cq] = ok ? m.bn_b[co] : 0.0f;
+  }
   // Wait for these loads here: used inside the item loop's conditional
   // blocks, a value still counted as in flight makes the compiler wait
   // for every load in flight there, the next window's prefetch included.
@@ -213,7 +225,7 @@ __global__ __launch_bounds__(256, 2) void conv_f32_mfma_kernel(const F32M m) {
       wval[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, voff, 0, 0));
     }
   };
-  const int first = blockIdx.x / m.co_tiles, step_items = gridDim.x / m.co_tiles;
+  const int first = blockIdx.x / m.co_groups, step_items = gridDim.x / m.co_groups;
   if (first < m.items) load_window(first);
 
   // per-lane operand bases of the wave's two M-tiles (the unused pooled row
@@ -240,6 +252,19 @@ __global__ __launch_bounds__(256, 2) void conv_f32_mfma_kernel(const F32M m) {
     lds_barrier();
     if (item + step_items < m.items) load_window(item + step_items);
 
+    if constexpr (!POOL && OB > 0) {
+      for (int i = tid; i < PT_H0 * PT_W0 * nct * planes_of(OB); i += 256) pk[i] = 0u;
+    }
+    for (int cq = 0; cq < nct; ++cq) {
+    const int ct = ct0 + cq, co_blk = ct * 32, co_l = co_blk + l32;
+    const bool cok = co_l < m.cout;
+    float bk = bkv[0], bb = bbv[0];
+#pragma unroll
+    for (int j = 1; j < NCT_MAX; ++j)
+      if (cq == j) {
+        bk = bkv[j];
+        bb = bbv[j];
+      }
     // ---- MFMAs: this wave's 2 M-tiles x 32 channels ----
     v16f acc0 = {}, acc1 = {};
     for (int ci = 0; ci < m.cin; ++ci) {
@@ -247,7 +272,7 @@ __global__ __launch_bounds__(256, 2) void conv_f32_mfma_kernel(const F32M m) {
       const float* xa1 = xin + ci * CIP + bA[1];
       const float* xb0 = xin + ci * CIP + bB[0];
       const float* xb1 = xin + ci * CIP + bB[1];
-      const float* wc = wB + ci * (KS2 * 64) + half * 32 + l32;
+      const float* wc = wB + (cq * m.cin + ci) * (KS2 * 64) + half * 32 + l32;
 #pragma unroll
       for (int st = 0; st < KS2; ++st) {
         const int o = tap_off<KSZ, S, POOL>(step_tap<KSZ, S>(st, 0));
@@ -354,8 +379,7 @@ __global__ __launch_bounds__(256, 2) void conv_f32_mfma_kernel(const F32M m) {
       // one M-tile = one conv row of 32 columns: lane l holds columns
       // 8 (v / 4) + 4 (l / 32) + v % 4 of its channel
       if constexpr (OB > 0) {
-        for (int i = tid; i < PT_H0 * PT_W0 * planes_of(OB); i += 256) pk[i] = 0u;
-        lds_barrier();
+        if (cq == 0) lds_barrier();  // the packed staging is zeroed
       }
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
@@ -391,23 +415,27 @@ __global__ __launch_bounds__(256, 2) void conv_f32_mfma_kernel(const F32M m) {
                 // lanes 0-31: the 32 channels of column col + i, lanes 32-63: of column col + 4 + i
                 const uint64_t bl = __ballot((qv >> p) & 1u);
                 if (lane == 0) {
-                  pk[(row * PT_W0 + 8 * g + i) * P + p] = (uint32_t)bl;
-                  pk[(row * PT_W0 + 8 * g + 4 + i) * P + p] = (uint32_t)(bl >> 32);
+                  pk[((row * PT_W0 + 8 * g + i) * nct + cq) * P + p] = (uint32_t)bl;
+                  pk[((row * PT_W0 + 8 * g + 4 + i) * nct + cq) * P + p] = (uint32_t)(bl >> 32);
                 }
               }
             }
           }
         }
       }
-      if constexpr (OB > 0) {
-        constexpr int P = planes_of(OB);
-        lds_barrier();
-        for (int i = tid; i < PT_H0 * PT_W0 * P; i += 256) {
-          const int qq = i / P, p = i - (i / P) * P;
-          const int qy = cy0 + qq / PT_W0, qx = cx0 + qq % PT_W0;
-          if (qy < m.oh && qx < m.ow)
-            m.out_packed[((((int64_t)img * m.oh + qy) * m.ow + qx) * m.out_cw + ct) * P + p] = pk[i];
-        }
+    }
+    }  // channel tiles
+    if constexpr (!POOL && OB > 0) {
+      // every channel tile's words of a pixel, stored together (one
+      // contiguous run per pixel when the block holds all its channels)
+      constexpr int P = planes_of(OB);
+      lds_barrier();
+      const int wpp = nct * P;  // staged words per pixel
+      for (int i = tid; i < PT_H0 * PT_W0 * wpp; i += 256) {
+        const int qq = i / wpp, r = i - qq * wpp;
+        const int qy = cy0 + qq / PT_W0, qx = cx0 + qq % PT_W0;
+        if (qy < m.oh && qx < m.ow)
+          m.out_packed[(((int64_t)img * m.oh + qy) * m.ow + qx) * m.out_cw * P + ct0 * P + r] = pk[i];
       }
     }
   }
@@ -467,17 +495,24 @@ bool f32m_plan(int n, int cin, int h, int w, int cout, int k, int stride, int pa
   if (items * m->co_tiles >= ((int64_t)1 << 31)) return false;
   m->items = (int)items;
   // LDS: the staged window (with pooling also the conv tile and the staged
-  // pooled tile over it), the weights, then (plain tiles) the packed staging
+  // pooled tile over it), the weights, then (plain tiles) the packed
+  // staging; plain tiles take as many channel tiles per block (up to 4) as
+  // fit, so that a window staged once feeds all of them
   const int taps2 = 2 * ((k * k + 1) / 2);  // padded taps per input channel
   int64_t region = (int64_t)cin * cip + 1;  // + the spare slot of the elements past the window
   if (pool) region = std::max<int64_t>(region, (int64_t)CT_PIX * CT_PITCH + 32 * PO_PITCH);
   m->l_w = (int)((region + 3) & ~(int64_t)3);
-  m->l_pk = m->l_w + cin * taps2 * 32;
-  return f32m_lds(*m, pool) <= F32M_LDS_MAX;
+  for (int nct = pool ? 1 : std::min(m->co_tiles, NCT_MAX); nct >= 1; --nct) {
+    m->nct = nct;
+    m->co_groups = ceil_div(m->co_tiles, nct);
+    m->l_pk = m->l_w + nct * cin * taps2 * 32;
+    if (f32m_lds(*m, pool) <= F32M_LDS_MAX) return true;
+  }
+  return false;
 }
 
 size_t f32m_lds(const F32M& m, int pool) {
-  return (size_t)(m.l_pk + (pool ? 0 : PT_H0 * PT_W0 * 4)) * 4;
+  return (size_t)(m.l_pk + (pool ? 0 : PT_H0 * PT_W0 * 4 * m.nct)) * 4;
 }
 
 template <int KSZ, int S, int POOL>
@@ -521,9 +556,9 @@ int launch_conv_f32_mfma(const float* x, const float* w, int n, int cin, int h, 
   m.out_cw = ceil_div(cout, 32);
   m.othr = othr;
   const int ob = out_packed ? out_bits : 0;
-  const int blocks_per = 2 * device_cus_f() / m.co_tiles;
+  const int blocks_per = 2 * device_cus_f() / m.co_groups;
   const int64_t want = (int64_t)(blocks_per < 1 ? 1 : blocks_per);
-  const int grid = (int)((want < m.items ? want : m.items) * m.co_tiles);
+  const int grid = (int)((want < m.items ? want : m.items) * m.co_groups);
   const size_t lds = f32m_lds(m, pool);
   if (pool) {
     if (stride == 1) {

@@ -132,6 +132,8 @@ PLAIN = [
     (2, 3, 20, 36, 70, 3, 1, 1, True, 0),     # fp32 output (+ a fused 2-bit quantize)
     (2, 4, 17, 9, 32, 3, 1, 0, False, 3),     # ragged rows and columns, 3-bit levels
     (3, 5, 40, 21, 40, 5, 1, 2, True, 2),     # 5 x 5 taps, ragged channel tile
+    (2, 3, 24, 40, 150, 3, 1, 1, True, 2),    # five channel tiles: a block of four and one of one
+    (1, 2, 12, 70, 160, 5, 1, 2, False, 1),   # five full channel tiles, 5 x 5 taps, wide rows
 ]
 
 
