@@ -128,7 +128,7 @@ struct F32M {
   float* out;
   uint32_t* out_packed;
   int out_cw;
-  Thr othr;
+  Thr othr;  // requantization thresholds for |z| (HardTanh folded in)
   int l_w, l_pk;  // LDS float offsets: weights, packed staging (window / conv tile region at 0)
 };
 
@@ -252,9 +252,6 @@ __global__ __launch_bounds__(256, 2) void conv_f32_mfma_kernel(const F32M m) {
     lds_barrier();
     if (item + step_items < m.items) load_window(item + step_items);
 
-    if constexpr (!POOL && OB > 0) {
-      for (int i = tid; i < PT_H0 * PT_W0 * nct * planes_of(OB); i += 256) pk[i] = 0u;
-    }
     for (int cq = 0; cq < nct; ++cq) {
     const int ct = ct0 + cq, co_blk = ct * 32, co_l = co_blk + l32;
     const bool cok = co_l < m.cout;
@@ -349,14 +346,13 @@ __global__ __launch_bounds__(256, 2) void conv_f32_mfma_kernel(const F32M m) {
           // one ballot per plane: lanes 0-31 give the word of (py, px) of
           // the lower half, lanes 32-63 that of the upper half
           constexpr int P = planes_of(OB);
-          const uint32_t qv = cok ? quant_planes<OB>(hardtanh(z), m.othr) : 0u;
-          const bool ok = py < m.oh && px < m.ow;
+          uint64_t bl[P];
+          plane_ballots<OB>(z, cok, m.othr, bl);
+          if (l32 == 0 && py < m.oh && px < m.ow) {
 #pragma unroll
-          for (int q = 0; q < P; ++q) {
-            const uint64_t bl = __ballot((qv >> q) & 1u);
-            const uint32_t word = half ? (uint32_t)(bl >> 32) : (uint32_t)bl;
-            if (l32 == 0 && ok)
-              m.out_packed[((((int64_t)img * m.oh + py) * m.ow + px) * m.out_cw + ct) * P + q] = word;
+            for (int q = 0; q < P; ++q)
+              m.out_packed[((((int64_t)img * m.oh + py) * m.ow + px) * m.out_cw + ct) * P + q] =
+                  half ? (uint32_t)(bl[q] >> 32) : (uint32_t)bl[q];
           }
         }
       }
@@ -378,49 +374,67 @@ __global__ __launch_bounds__(256, 2) void conv_f32_mfma_kernel(const F32M m) {
     } else {
       // one M-tile = one conv row of 32 columns: lane l holds columns
       // 8 (v / 4) + 4 (l / 32) + v % 4 of its channel
-      if constexpr (OB > 0) {
-        if (cq == 0) lds_barrier();  // the packed staging is zeroed
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        float z0 = fmaf(bk, acc0[v], bb), z1 = fmaf(bk, acc1[v], bb);
+        if (m.relu) {
+          z0 = (z0 > 0.0f) ? z0 : 0.0f;
+          z1 = (z1 > 0.0f) ? z1 : 0.0f;
+        }
+        acc0[v] = z0;
+        acc1[v] = z1;
       }
+      if (m.out != nullptr) {
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const int row = wave * 2 + t;
-        const int oy = cy0 + row;
+        for (int t = 0; t < 2; ++t) {
+          const int oy = cy0 + wave * 2 + t;
+          if (oy < m.oh && cok) {
+            float* orow = m.out + (((int64_t)img * m.cout + co_l) * m.oh + oy) * m.ow;
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int col = 8 * g + 4 * half;
-          float z[4];
+            for (int g = 0; g < 4; ++g) {
+              const int ox = cx0 + 8 * g + 4 * half;
+              float z[4];
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            z[i] = fmaf(bk, t == 0 ? acc0[4 * g + i] : acc1[4 * g + i], bb);
-            if (m.relu) z[i] = (z[i] > 0.0f) ? z[i] : 0.0f;
-          }
-          const int ox = cx0 + col;
-          if (oy < m.oh && cok && m.out) {
-            float* o = m.out + (((int64_t)img * m.cout + co_l) * m.oh + oy) * m.ow + ox;
-            if (m.ow % 4 == 0 && ox + 4 <= m.ow) {
-              *reinterpret_cast<float4*>(o) = make_float4(z[0], z[1], z[2], z[3]);
-            } else {
+              for (int i = 0; i < 4; ++i) z[i] = t == 0 ? acc0[4 * g + i] : acc1[4 * g + i];
+              if (m.ow % 4 == 0 && ox + 4 <= m.ow) {
+                *reinterpret_cast<float4*>(orow + ox) = make_float4(z[0], z[1], z[2], z[3]);
+              } else {
 #pragma unroll
-              for (int i = 0; i < 4; ++i)
-                if (ox + i < m.ow) o[i] = z[i];
-            }
-          }
-          if constexpr (OB > 0) {
-            constexpr int P = planes_of(OB);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const uint32_t qv = cok ? quant_planes<OB>(hardtanh(z[i]), m.othr) : 0u;
-#pragma unroll
-              for (int p = 0; p < P; ++p) {
-                // lanes 0-31: the 32 channels of column col + i, lanes 32-63: of column col + 4 + i
-                const uint64_t bl = __ballot((qv >> p) & 1u);
-                if (lane == 0) {
-                  pk[((row * PT_W0 + 8 * g + i) * nct + cq) * P + p] = (uint32_t)bl;
-                  pk[((row * PT_W0 + 8 * g + 4 + i) * nct + cq) * P + p] = (uint32_t)(bl >> 32);
-                }
+                for (int i = 0; i < 4; ++i)
+                  if (ox + i < m.ow) orow[ox + i] = z[i];
               }
             }
           }
+        }
+      }
+      if constexpr (OB > 0) {
+        // one ballot per (value, plane): lanes 0-31 give the word of column
+        // 8 g + i, lanes 32-63 that of column 8 g + 4 + i; the words go to
+        // lane 32 t + column of a register per plane, stored in one pass
+        constexpr int P = planes_of(OB);
+        uint32_t pw[P] = {};
+        Unroll<0, 8>::run([&](auto tg) {
+          constexpr int T = decltype(tg)::value / 4, GG = decltype(tg)::value % 4, B = 32 * T + 8 * GG;
+          uint64_t bl[4][P];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float z = T == 0 ? acc0[4 * GG + i] : acc1[4 * GG + i];
+            plane_ballots<OB>(z, cok, m.othr, bl[i]);
+          }
+#pragma unroll
+          for (int p = 0; p < P; ++p)
+            pw[p] = writelanes8<B, B + 1, B + 2, B + 3, B + 4, B + 5, B + 6, B + 7>(
+                pw[p], (uint32_t)bl[0][p], (uint32_t)bl[1][p], (uint32_t)bl[2][p], (uint32_t)bl[3][p],
+                (uint32_t)(bl[0][p] >> 32), (uint32_t)(bl[1][p] >> 32), (uint32_t)(bl[2][p] >> 32),
+                (uint32_t)(bl[3][p] >> 32));
+        });
+        uint32_t* d = pk + (((wave * 2 + half) * PT_W0 + l32) * nct + cq) * P;
+        if constexpr (P == 1) {
+          d[0] = pw[0];
+        } else if constexpr (P == 2) {
+          *reinterpret_cast<uint2*>(d) = make_uint2(pw[0], pw[1]);
+        } else {
+          *reinterpret_cast<uint4*>(d) = make_uint4(pw[0], pw[1], pw[2], pw[3]);
         }
       }
     }
@@ -554,7 +568,7 @@ int launch_conv_f32_mfma(const float* x, const float* w, int n, int cin, int h, 
   m.out = out;
   m.out_packed = out_packed;
   m.out_cw = ceil_div(cout, 32);
-  m.othr = othr;
+  m.othr = thr_unclamped(othr);
   const int ob = out_packed ? out_bits : 0;
   const int blocks_per = 2 * device_cus_f() / m.co_groups;
   const int64_t want = (int64_t)(blocks_per < 1 ? 1 : blocks_per);

@@ -114,11 +114,7 @@ bool plan(const ConvArgs& a, int cfg, MfmaArgs* m) {
   m->tiles_co = ceil_div(a.cout, cfg_block_co(cfg));
   if (m->tiles_px < 1 || m->tiles_co < 1) return false;  // never an empty launch
   m->halo_bytes = m->slot_pix * m->pix_bytes * m->ipb;
-  m->ht_needed = 0;
-  if (a.out_packed) {
-    const Thr& t = a.othr;
-    m->ht_needed = (a.out_bits == 2 && t.t0 >= 1.0f) || (a.out_bits == 3 && t.t2 >= 1.0f);
-  }
+  m->ht_needed = a.out_packed && hardtanh_needed(a.out_bits, a.othr);
   const int64_t ab = (int64_t)a.n * a.h * a.w * a.cw * act_words(a.a_bits) * 4;
   m->act_bytes = ab < ((int64_t)1 << 31) ? (int)ab : 0;
   const int64_t ob = (int64_t)a.n * a.cout * m->upi * 4;

@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "../../include/qconv.h"
 
 namespace qc {
@@ -59,6 +61,89 @@ __device__ __forceinline__ float hardtanh(float v) {
   if (v > 1.0f) v = 1.0f;
   if (v < -1.0f) v = -1.0f;
   return v;
+}
+
+// The bitplane compares may take z itself instead of HardTanh(z) unless a
+// threshold reaches 1: below 1, |HardTanh(z)| <= t exactly when |z| <= t, and
+// the sign is kept.
+inline bool hardtanh_needed(int bits, Thr t) {
+  return (bits == 2 && t.t0 >= 1.0f) || (bits == 3 && t.t2 >= 1.0f);
+}
+
+// Thresholds that give the compares on |z| the results of those on
+// |HardTanh(z)| = min(|z|, 1) for every z, NaN included: one below 1 is
+// kept, one at or above 1 (which |HardTanh(z)| never exceeds) becomes +inf.
+inline Thr thr_unclamped(Thr t) {
+  auto f = [](float v) { return v >= 1.0f ? __builtin_inff() : v; };
+  return Thr{f(t.t0), f(t.t1), f(t.t2)};
+}
+
+// Compile-time loop: f(integral_constant<I>) for I in [B, E), so that the
+// accumulator tiles are only ever indexed with constants.
+template <int B, int E>
+struct Unroll {
+  template <class F>
+  __device__ __forceinline__ static void run(F&& f) {
+    f(std::integral_constant<int, B>{});
+    Unroll<B + 1, E>::run(f);
+  }
+};
+template <int E>
+struct Unroll<E, E> {
+  template <class F>
+  __device__ __forceinline__ static void run(F&&) {}
+};
+
+// Ballots of the bitplanes of Q(HardTanh(z)) over the wave (Eqs. 4, 21, 22):
+// the same compares as the quantizer, one ballot each, combined with scalar
+// bit operations.  `ok` = the lane's channel and unit exist; its ballot is
+// taken once and masks the others, so that each compare's lane mask is the
+// ballot itself.
+template <int OB>
+__device__ __forceinline__ void plane_ballots(float z, bool ok, Thr t, uint64_t* b) {
+  const uint64_t om = __builtin_amdgcn_ballot_w64(ok);
+  const uint64_t s = __builtin_amdgcn_ballot_w64(z > 0.0f) & om;
+  if constexpr (OB == 1) {
+    b[0] = s;
+  } else if constexpr (OB == 2) {
+    const uint64_t nz = __builtin_amdgcn_ballot_w64(!(fabsf(z) <= t.t0)) & om;
+    b[0] = s & nz;
+    b[1] = nz;
+  } else {
+    const float az = fabsf(z);
+    const uint64_t a1 = __builtin_amdgcn_ballot_w64(!(az <= t.t0)) & om;
+    const uint64_t a2 = __builtin_amdgcn_ballot_w64(!(az <= t.t1)) & om;
+    const uint64_t a3 = __builtin_amdgcn_ballot_w64(!(az <= t.t2)) & om;
+    b[0] = s & a1;
+    b[1] = a3;
+    b[2] = a2 & ~a3;
+    b[3] = a1 & ~a2;
+  }
+}
+
+// Eight v_writelane_b32: lanes L0..L3 of w take lo0..lo3, lanes H0..H3 take
+// hi0..hi3 (wave-uniform values).  The lanes are inline constants, so the
+// value is the instruction's only scalar operand.  The values usually come
+// straight from a VALU compare; s_nop 4 provides the wait states a VALU
+// write of an SGPR needs before v_writelane reads it, which the compiler does
+// not insert across inline assembly.
+template <int L0, int L1, int L2, int L3, int H0, int H1, int H2, int H3>
+__device__ __forceinline__ uint32_t writelanes8(uint32_t w, uint32_t lo0, uint32_t lo1, uint32_t lo2,
+                                                uint32_t lo3, uint32_t hi0, uint32_t hi1, uint32_t hi2,
+                                                uint32_t hi3) {
+  asm("s_nop 4\n\t"
+      "v_writelane_b32 %0, %1, %9\n\t"
+      "v_writelane_b32 %0, %2, %10\n\t"
+      "v_writelane_b32 %0, %3, %11\n\t"
+      "v_writelane_b32 %0, %4, %12\n\t"
+      "v_writelane_b32 %0, %5, %13\n\t"
+      "v_writelane_b32 %0, %6, %14\n\t"
+      "v_writelane_b32 %0, %7, %15\n\t"
+      "v_writelane_b32 %0, %8, %16"
+      : "+v"(w)
+      : "s"(lo0), "s"(lo1), "s"(lo2), "s"(lo3), "s"(hi0), "s"(hi1), "s"(hi2), "s"(hi3), "i"(L0), "i"(L1),
+        "i"(L2), "i"(L3), "i"(H0), "i"(H1), "i"(H2), "i"(H3));
+  return w;
 }
 
 __host__ __device__ inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
