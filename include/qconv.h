@@ -166,7 +166,9 @@ typedef enum {
   QCONV_ALGO_AUTO = 0,     /* library choice: fp4 matrix cores where supported
                               (int8 ones where fp4 would not be exact, see
                               QCONV_ALGO_MFMA_FP4), the bitplane kernel for
-                              K = cin*kh*kw <= 256                             */
+                              K = cin*kh*kw <= 256 where its LDS-tiled XNOR
+                              form applies (1-2 bit operands, 1x1 or 3x3,
+                              stride <= 2, unpacked unpooled outputs)       */
   QCONV_ALGO_BITPLANE = 1, /* VALU XNOR/AND + popcount over bitplanes         */
   QCONV_ALGO_MFMA_I8 = 2,  /* int8 matrix cores on the expanded level codes   */
   QCONV_ALGO_MFMA_FP4 = 3, /* fp4 (E2M1) matrix cores on the same codes; they

@@ -252,10 +252,15 @@ int prepare_conv(const qconv_desc* d, const uint32_t* act_packed, const uint32_t
   }
   // AUTO: the fp4 matrix cores (int8 ones, whose int32 accumulator is exact
   // at any size, past the fp4 bound), except for tiny contractions (K <= 256,
-  // the 1x1 shortcut convolutions of ResNet-18), where staging an input tile
-  // in LDS costs more than the whole bitplane product (measured 18-19 us on
-  // the bitplane kernel against 21-29 us on the matrix cores for those layers)
-  if (d->algo == QCONV_ALGO_AUTO && d->n > 0 && K > 256) {
+  // the 1x1 shortcut convolutions of ResNet-18) that the LDS-tiled XNOR
+  // kernel serves, where staging a matrix-core input tile costs more than
+  // the whole bitplane product (measured 18-19 us on the bitplane kernels
+  // against 21-29 us on the matrix cores for those layers).  Small
+  // contractions the XNOR kernel does not serve (packed or pooled outputs,
+  // 3-bit operands) would fall to the one-lane-per-pixel kernel, which the
+  // matrix cores beat (1x1, K = 64 and 128, packed 2-bit outputs: 11-12 us
+  // against 22-30 us).
+  if (d->algo == QCONV_ALGO_AUTO && d->n > 0 && (K > 256 || !xnor_supports(a))) {
     a.mfma_op = fp4_exact ? OP_FP4 : OP_I8;
     if (mfma_supports(a)) return fp4_exact ? QCONV_ALGO_MFMA_FP4 : QCONV_ALGO_MFMA_I8;
   }

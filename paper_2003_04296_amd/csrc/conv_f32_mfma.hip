@@ -570,7 +570,7 @@ int launch_conv_f32_mfma(const float* x, const float* w, int n, int cin, int h, 
   m.out_cw = ceil_div(cout, 32);
   m.othr = thr_unclamped(othr);
   const int ob = out_packed ? out_bits : 0;
-  const int blocks_per = 2 * device_cus_f() / m.co_groups;
+  const int blocks_per = (pool ? 2 : 3) * device_cus_f() / m.co_groups;
   const int64_t want = (int64_t)(blocks_per < 1 ? 1 : blocks_per);
   const int grid = (int)((want < m.items ? want : m.items) * m.co_groups);
   const size_t lds = f32m_lds(m, pool);

@@ -123,6 +123,20 @@ def test_auto_takes_the_bitplane_kernel_for_tiny_contractions():
     assert q.resolve_algo(64, 64, 28, 28, 128, 1, 2, 0, 2, 2, algo=q.ALGO_MFMA_FP4) == q.ALGO_MFMA_FP4
 
 
+def test_auto_keeps_small_contractions_the_xnor_kernel_cannot_take_on_the_matrix_cores():
+    """K <= 256 goes to the bitplane algorithm only where its LDS-tiled XNOR
+    form applies; packed or pooled outputs and 3-bit operands stay on the fp4
+    matrix cores (the one-lane-per-pixel kernel is slower there)."""
+    fp4 = q.ALGO_MFMA_FP4
+    assert q.resolve_algo(64, 64, 56, 56, 64, 1, 1, 0, 2, 2, mode=q.EPI_BN_PACK, out_bits=2) == fp4
+    assert q.resolve_algo(64, 128, 28, 28, 128, 1, 1, 0, 1, 1, mode=q.EPI_BN_PACK, out_bits=1) == fp4
+    assert q.resolve_algo(64, 64, 28, 28, 128, 1, 2, 0, 3, 3, mode=q.EPI_BN_F32) == fp4
+    assert q.resolve_algo(64, 16, 28, 28, 64, 3, 1, 1, 1, 1, mode=q.EPI_BN_F32, flags=q.EPI_POOL2) == fp4
+    # the same shapes with an unpacked output and 1-2 bit operands keep the XNOR kernel
+    assert q.resolve_algo(64, 64, 56, 56, 64, 1, 1, 0, 2, 2, mode=q.EPI_BN_F32) == q.ALGO_BITPLANE
+    assert q.resolve_algo(64, 16, 28, 28, 64, 3, 1, 1, 1, 1, mode=q.EPI_BN_F32) == q.ALGO_BITPLANE
+
+
 FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails validation first
 
 
