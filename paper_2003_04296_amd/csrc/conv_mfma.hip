@@ -57,7 +57,11 @@ bool plan(const ConvArgs& a, int cfg, MfmaArgs* m) {
   int best_units = -1;
   MfmaArgs best = *m;
   for (int wide = 0; wide < 2 && best_units < 0; ++wide) {
-  if (wide && op != OP_F16) break;
+  // the wide buffer (one block per CU) serves the fp16 tiles and the
+  // 256-row tiles of stride-2 layers, whose input rows are twice as many
+  // (ResNet-18's 64 -> 128 stride-2 layer at batch 64 took 26 us on 64-row
+  // split-K items, 15 us on 256-row ones)
+  if (wide && op != OP_F16 && (cfg == 2 || a.stride == 1)) break;
   const size_t lim = wide ? (size_t)MAX_LDS_WIDE : (size_t)MAX_LDS;
   for (int cwc = min(chunk_max, cw_round); cwc >= wpstep; cwc /= 2) {
     if (cwc % wpstep) break;

@@ -469,6 +469,38 @@ def test_pp_kernel_packed_output(dev, ci, bits):
     assert tail_bits_zero(outp.cpu().numpy(), cout, ab)
 
 
+STRIDE2_WIDE_CASES = [
+    # n, cin, h, w, cout, k, stride, pad: ResNet-18's stride-2 3x3 layers at
+    # batch 64, whose 256-row input tiles (twice the input rows of a stride-1
+    # tile) are staged in the wide halo buffer
+    (64, 64, 56, 56, 128, 3, 2, 1),
+    (64, 128, 28, 28, 256, 3, 2, 1),
+]
+
+
+@pytest.mark.parametrize("ci", [0, 1])
+def test_stride2_layers_on_256_row_tiles(dev, ci):
+    """BN -> packed 2-bit output of the stride-2 layers on 256-row items
+    (not the 64-row split-K shape), bit for bit against the oracle."""
+    n, cin, h, w, cout, k, s, p = STRIDE2_WIDE_CASES[ci]
+    name = q.kernel_name(n, cin, h, w, cout, k, s, p, 2, 2, mode=q.EPI_BN_PACK, out_bits=2, packed_out=True)
+    cfg = int(name.split("<")[1].split(",")[2])
+    assert cfg != 2, name
+    x, wt = _inputs(380 + ci, n, cin, h, w, cout, k)
+    kk, bb = _bn(380 + ci, cout)
+    ho, wo = q.out_size(h, k, s, p), q.out_size(w, k, s, p)
+    act = q.pack_act(x.to(dev), 2)
+    wq, _ = q.pack_weight(wt.to(dev), 2)
+    _, outp = q.conv(act, wq, n, cin, h, w, cout, k, s, p, 2, 2, mode=q.EPI_BN_PACK, bn_k=kk.to(dev),
+                     bn_b=bb.to(dev), out_bits=2)
+    torch.cuda.synchronize()
+    acc, _ = _oracle_acc(x, wt, 2, 2, s, p)
+    z = oracle.epi_bn(acc, kk.numpy(), bb.numpy(), oracle.level_shift(2) + oracle.level_shift(2))
+    np.testing.assert_array_equal(unpack_act(outp.cpu().numpy(), n, cout, ho, wo, 2),
+                                  oracle.quantize(oracle.hardtanh(z), 2))
+    assert tail_bits_zero(outp.cpu().numpy(), cout, 2)
+
+
 def test_pp_kernel_takes_64_channel_items_when_128_are_too_few(dev):
     """A 128-channel layer whose 256-row x 128-channel items are fewer than two
     per CU runs the store-overlapped kernel on 256 x 64 items, bit-exact."""
