@@ -160,25 +160,35 @@ class ConvWorkload:
         return n * c * h * w * 4 + q.packed_act_words(n, c, h, w, self.case.a_bits) * 4
 
 
-def measured_traffic(workload: str, kernel: str):
-    """HBM bytes per launch of `kernel` on `workload` from the committed
-    rocprofv3 counter runs, or None when there is no record or the kernel's
-    sources changed since the counters were taken."""
+def measured_traffic(workload: str, kernel: str, layer=None):
+    """HBM bytes per launch of `kernel` on `workload` (of network layer `layer`
+    when given) from the committed rocprofv3 counter runs, or None when there
+    is no record or the kernel's sources changed since the counters were
+    taken."""
     import hashlib
 
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path)).get(workload)
-    if not rec or rec["kernel"] != kernel:
+    if not rec:
         return None
-    h = hashlib.sha256()
-    for src in rec["sources"]:
-        fp = os.path.join(ROOT, src)
-        if not os.path.exists(fp):
+
+    def unchanged(sources, digest):
+        h = hashlib.sha256()
+        for src in sources:
+            fp = os.path.join(ROOT, src)
+            if not os.path.exists(fp):
+                return False
+            h.update(open(fp, "rb").read())
+        return h.hexdigest() == digest
+
+    if layer is not None and str(layer) in rec.get("layers", {}):
+        lr = rec["layers"][str(layer)]
+        if lr["kernel"] != kernel or not unchanged(rec["layer_sources"], rec["layer_sources_sha256"]):
             return None
-        h.update(open(fp, "rb").read())
-    if h.hexdigest() != rec["sources_sha256"]:
+        return lr["fetch_bytes"] + lr["write_bytes"]
+    if rec["kernel"] != kernel or not unchanged(rec["sources"], rec["sources_sha256"]):
         return None
     return rec["fetch_bytes"] + rec["write_bytes"]
 
@@ -439,14 +449,14 @@ def net_entry(wl, dev, stream, steps, warmup, cpu, cpu_budget=8.0):
         layers.append({"layer": li, "kind": net.layers[li]["kind"], "kernel": kname, "avg_us": round(t * 1e6, 2),
                        "ideal_us": round(ideal * 1e6, 2), "frac": round(ideal / t, 4), "ops": int(ops),
                        "bytes": int(nb), "bound": cb if peak and ops / (peak * 1e9) >= nb / (HBM_PEAK_GBS * 1e9)
-                       else "hbm", "_peak": peak})
+                       else "hbm", "traffic": measured_traffic(name, kname, li), "_peak": peak})
     dom = max(layers, key=lambda r: r["avg_us"])
     peak = dom.pop("_peak")
     for r in layers:
         r.pop("_peak", None)
     rf = roofline(dom["kernel"], dom["ops"], dom["bytes"], dom["avg_us"] / 1e6, peak,
                   dom["bound"] if dom["bound"] != "hbm" else ("fp32" if dom["kind"] == "conv_f32" else "mfma"),
-                  measured_traffic(name, dom["kernel"]))
+                  measured_traffic(name, dom["kernel"], dom["layer"]))
     rf.update({"layer": dom["layer"],
                "network": {"ideal_us": round(tot_ideal * 1e6, 2), "forward_us": round(t_fwd * 1e6, 2),
                            "frac": round(tot_ideal / t_fwd, 4),
