@@ -239,7 +239,10 @@ int qconv_forward(const qconv_desc* d, const uint32_t* act_packed, const uint32_
 
 /* The concrete algorithm (QCONV_ALGO_BITPLANE / _MFMA_I8 / _MFMA_FP4) that
  * qconv_forward would run for d and epi (d->algo may be AUTO), or a negative
- * status if the call would be rejected.  Launches nothing. */
+ * status if the call would be rejected.  For QCONV_EPI_BN_F32 the answer is
+ * that of a call without a packed copy (out_packed NULL; with one, AUTO may
+ * choose differently for K <= 256: qconv_kernel_name takes it as an
+ * argument).  Launches nothing. */
 int qconv_resolve_algo(const qconv_desc* d, const qconv_epilogue* epi);
 
 /* Name of the GPU kernel instantiation qconv_forward would launch for d and
