@@ -155,10 +155,15 @@ int pick_cfg_base(const ConvArgs& a) {
   }
   const int64_t blocks = (int64_t)m.tiles_px * m.tiles_co;
   const int steps = a.kh * a.kw * m.ksteps;
-  if (blocks < device_cus() && steps >= 8) {
+  // fewer 128-channel items than CUs, or (stride 1) than two per CU
+  if ((blocks < device_cus() || (a.stride == 1 && blocks < 2 * device_cus())) && steps >= 8) {
     // 64-channel blocks double the block count; when that gives every CU a
     // block they beat the split-K shape (ResNet-18 3x3 layers: 512 ch at
-    // 7x7, batch 256, 59 -> 43 us; 256 ch at 14x14, batch 64, 22 -> 18 us)
+    // 7x7, batch 256, 59 -> 43 us; 256 ch at 14x14, batch 64, 22 -> 18 us),
+    // and at one 128-channel item per CU they beat it too, three blocks per
+    // CU against two (ConvNet's 256 -> 512 layer at 8x8 23.7 -> 21.6 us,
+    // its pooled 512 -> 512 layer 36.9 -> 34.0 us; ResNet-18's 128-channel
+    // 28x28 layer 15.9 -> 14.8 us; its stride-2 layers measured slower)
     MfmaArgs h;
     if (big == 0 && plan(a, 1, &h) && (int64_t)h.tiles_px * h.tiles_co >= device_cus()) return 1;
     MfmaArgs s;

@@ -435,12 +435,13 @@ def test_pp_kernel_packed_copy(dev, ci, bits, resid):
 
 
 PP_PACK_CASES = [
-    # n, cin, h, w, cout, k, stride, pad: layers whose base-kernel items are
-    # fewer than two per CU, so that a packed output alone takes the
-    # store-overlapped kernel (on 64-channel items)
-    (64, 128, 28, 28, 128, 3, 1, 1),   # ResNet-18's 128-channel layer shape
-    (64, 96, 28, 30, 100, 3, 1, 1),    # ragged channels, cin padded to a k-step, ragged last items
-    (66, 64, 28, 28, 128, 3, 1, 1),    # odd item count per image row of blocks
+    # n, cin, h, w, cout, k, stride, pad: stride-2 layers whose base-kernel
+    # items are fewer than two per CU, so that a packed output alone takes the
+    # store-overlapped kernel (on 64-channel items; stride-1 layers of that
+    # size take the base kernel's 64-channel items, three blocks per CU)
+    (64, 64, 56, 56, 128, 3, 2, 1),    # ResNet-18's 64 -> 128 stride-2 layer
+    (64, 64, 54, 60, 100, 3, 2, 1),    # ragged channels, a 27 x 30 output: ragged last items
+    (66, 64, 56, 58, 120, 3, 2, 1),    # odd batch, ragged channels and rows
 ]
 
 
@@ -501,12 +502,14 @@ def test_stride2_layers_on_256_row_tiles(dev, ci):
     assert tail_bits_zero(outp.cpu().numpy(), cout, 2)
 
 
-def test_pp_kernel_takes_64_channel_items_when_128_are_too_few(dev):
-    """A 128-channel layer whose 256-row x 128-channel items are fewer than two
-    per CU runs the store-overlapped kernel on 256 x 64 items, bit-exact."""
+def test_128_channel_layer_takes_64_channel_items_when_128_are_too_few(dev):
+    """A 128-channel stride-1 layer whose 256-row x 128-channel items are
+    fewer than two per CU runs 256 x 64 items (three blocks per CU) on the
+    base kernel, bit-exact; the same layer with stride 2 runs them on the
+    store-overlapped kernel (PP_PACK_CASES)."""
     n, cin, h, w, cout = 64, 128, 28, 28, 128
     name = q.kernel_name(n, cin, h, w, cout, 3, 1, 1, 2, 2, mode=q.EPI_BN_PACK, out_bits=2, packed_out=True)
-    assert name == "conv_mfma_pp_kernel<1, 2, 1, 2>", name
+    assert name == "conv_mfma_kernel<1, 2, 1, 1>", name
     x, wt = _inputs(371, n, cin, h, w, cout, 3)
     kk, bb = _bn(371, cout)
     act = q.pack_act(x.to(dev), 2)
