@@ -769,7 +769,7 @@ int qnet_layer_kernel(const qnet* net, int layer, int batch, char* buf, int len)
   } else if (l.kind == L_QUANTIZE) {
     snprintf(name, sizeof(name), "pack_act_lds_kernel<%d>", l.out_bits);
   } else if (l.kind == L_AVGPOOL) {
-    snprintf(name, sizeof(name), "avgpool_f32_kernel");
+    snprintf(name, sizeof(name), "%s", si.h * si.w <= 60 ? "avgpool_lds_kernel" : "avgpool_f32_kernel");
   } else {
     snprintf(name, sizeof(name), "fc_f32_kernel<%d>", si.bits);
   }

@@ -192,6 +192,38 @@ __global__ __launch_bounds__(256) void avgpool_f32_kernel(const float* __restric
   y[i] = s / (float)hw;
 }
 
+// The same sums for small maps (hw <= AVG_LDS_HW): a block's 64 planes are
+// contiguous in memory, so its 256 threads first copy them into LDS with
+// coalesced loads (all of a thread's loads issued before its first store);
+// one thread per plane then sums it in order from LDS (a plane's values are
+// hw words apart, odd for the odd hw of the pooled maps in use, so the 64
+// lanes' reads fall in distinct banks).
+constexpr int AVG_LDS_HW = 60;
+constexpr int AVG_PLANES = 64;
+__global__ __launch_bounds__(256) void avgpool_lds_kernel(const float* __restrict__ x, int64_t nc, int hw,
+                                                          float* __restrict__ y) {
+  constexpr int PER = AVG_PLANES * AVG_LDS_HW / 256;  // values per thread at most
+  __shared__ float t[AVG_PLANES * AVG_LDS_HW];
+  const int64_t p0 = (int64_t)blockIdx.x * AVG_PLANES;
+  const int np = (int)min((int64_t)AVG_PLANES, nc - p0);
+  const int total = np * hw;
+  const float* src = x + p0 * hw;
+  float v[PER];
+#pragma unroll
+  for (int u = 0; u < PER; ++u) v[u] = src[min((int)threadIdx.x + 256 * u, total - 1)];
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int e = (int)threadIdx.x + 256 * u;
+    if (e < total) t[e] = v[u];
+  }
+  __syncthreads();
+  if ((int)threadIdx.x >= np) return;
+  const float* r = t + threadIdx.x * hw;
+  float s = 0.0f;
+  for (int j = 0; j < hw; ++j) s += r[j];
+  y[p0 + threadIdx.x] = s / (float)hw;
+}
+
 // Last FC.  Each output of each image is one sequential fmaf chain over the
 // inputs, so the run time is set by the chain length, not by the flops: a
 // wave owns ONE output for 64 images (lane = image) and a block of 4 waves
@@ -355,7 +387,10 @@ int launch_maxpool_f32(const float* x, int n, int c, int h, int w, int k, int st
 int launch_avgpool_f32(const float* x, int n, int c, int h, int w, float* y, hipStream_t s) {
   const int64_t nc = (int64_t)n * c;
   if (nc == 0) return QCONV_OK;
-  avgpool_f32_kernel<<<(unsigned)((nc + 255) / 256), 256, 0, s>>>(x, nc, h * w, y);
+  if (h * w <= AVG_LDS_HW)
+    avgpool_lds_kernel<<<(unsigned)((nc + AVG_PLANES - 1) / AVG_PLANES), 256, 0, s>>>(x, nc, h * w, y);
+  else
+    avgpool_f32_kernel<<<(unsigned)((nc + 255) / 256), 256, 0, s>>>(x, nc, h * w, y);
   return hip_status();
 }
 

@@ -839,6 +839,24 @@ def test_fc_f32_binary_input(dev, n, c, out):
     np.testing.assert_array_equal(got, oracle.fc_f32(lv, wt.numpy(), b.numpy()))
 
 
+@pytest.mark.parametrize("n,c,h,w", [(3, 300, 7, 7), (2, 129, 1, 1), (5, 100, 6, 10), (2, 70, 61, 1), (1, 257, 8, 8)])
+def test_avgpool_head(dev, n, c, h, w):
+    """Average pool -> FC, bit-exact: planes of up to 60 values are summed
+    from LDS (a ragged last block of planes), larger ones from memory."""
+    g = synth.generator(720 + n + c + h * w)
+    x = synth.normal(g, (n, c, h, w), 1.0)
+    fw = synth.normal(g, (7, c), 2.0 / c)
+    net = q.Net(c, h, w, q.F32_FMAF_CHAIN)
+    t = net.avgpool(0)
+    net.fc_f32(t, fw.to(dev))
+    assert net.layer_kernel(0, n) == ("avgpool_lds_kernel" if h * w <= 60 else "avgpool_f32_kernel"), net.layer_kernel(0, n)
+    ws = torch.empty(max(net.workspace_bytes(n), 1), dtype=torch.uint8, device=dev)
+    logits = torch.empty((n, 7), dtype=torch.float32, device=dev)
+    net.forward(x.to(dev), logits, ws)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(logits.cpu().numpy(), oracle.fc_f32(oracle.avgpool_f32(x.numpy()), fw.numpy()))
+
+
 @pytest.mark.parametrize("pk,ps,pp", [(3, 2, 1), (2, 2, 0), (4, 3, 1)])
 @pytest.mark.parametrize("n,cin,hw,cout,k,s,p", [(2, 3, 32, 128, 3, 1, 1), (1, 3, 37, 64, 7, 2, 3), (3, 5, 9, 40, 3, 2, 0),
                                                  (1, 3, 64, 96, 7, 2, 3), (2, 40, 18, 33, 5, 1, 2)])
