@@ -256,40 +256,44 @@ __global__ __launch_bounds__(256) void fc_f32_kernel(const void* __restrict__ xi
   const int oc = min(o, out - 1);
   const int ob = blockIdx.y * 4;
   float acc = 0.0f;
+  // Every load of a chunk is issued before the first LDS store, and the
+  // loads of chunk c + 1 are issued before the chain over chunk c, so they
+  // arrive under it.  Indices are clamped into the chunk (and the batch), so
+  // no load is guarded; values staged past L (or past the batch) are never
+  // read.  Weights: thread -> row tid / 64 (rows past out repeat the last
+  // one), columns tid % 64 + 64 u.  Inputs: thread -> row tid / 4, columns
+  // tid % 4 + 4 u.
+  constexpr int WU = CI / 64;
+  constexpr int XCOLS = X_BITS ? FC_CW_BIN : CI;
+  constexpr int XU = XCOLS / 4;
+  constexpr int XLD = X_BITS ? FC_XLD_BIN : FC_XLD;
+  float wv[WU];
+  uint32_t xv[XU];
+  auto load = [&](int c0) __attribute__((always_inline)) {
+    const int L = min(CI, in - c0);
+    const int xl = X_BITS ? ((L + 31) >> 5) : L;  // valid columns of the input tile
+    const float* wrow = w + (int64_t)min(ob + (tid >> 6), out - 1) * in + c0;
+#pragma unroll
+    for (int u = 0; u < WU; ++u) wv[u] = wrow[min((tid & 63) + 64 * u, L - 1)];
+    const int r = min(tid >> 2, nb - 1);
+    const uint32_t* xrow;
+    if constexpr (X_BITS == 0)
+      xrow = static_cast<const uint32_t*>(xin) + (int64_t)(b0 + r) * in + c0;
+    else
+      xrow = static_cast<const uint32_t*>(xin) + (int64_t)(b0 + r) * ((in + 31) >> 5) + (c0 >> 5);
+#pragma unroll
+    for (int u = 0; u < XU; ++u) xv[u] = xrow[min((tid & 3) + 4 * u, xl - 1)];
+  };
+  load(0);
   for (int c0 = 0; c0 < in; c0 += CI) {
     const int L = min(CI, in - c0);  // inputs in this chunk
     __syncthreads();
-    // Every load of the chunk is issued before the first LDS store.  Indices
-    // are clamped into the chunk (and the batch), so no load is guarded;
-    // values staged past L (or past the batch) are never read.
-    // Weights: thread -> row tid / 64 (rows past out repeat the last one),
-    // columns tid % 64 + 64 u.  Inputs: thread -> row tid / 4, columns
-    // tid % 4 + 4 u.
-    constexpr int WU = CI / 64;
-    constexpr int XCOLS = X_BITS ? FC_CW_BIN : CI;
-    constexpr int XU = XCOLS / 4;
-    constexpr int XLD = X_BITS ? FC_XLD_BIN : FC_XLD;
-    const int xl = X_BITS ? ((L + 31) >> 5) : L;  // valid columns of the input tile
-    float wv[WU];
-    uint32_t xv[XU];
-    {
-      const float* wrow = w + (int64_t)min(ob + (tid >> 6), out - 1) * in + c0;
-#pragma unroll
-      for (int u = 0; u < WU; ++u) wv[u] = wrow[min((tid & 63) + 64 * u, L - 1)];
-      const int r = min(tid >> 2, nb - 1);
-      const uint32_t* xrow;
-      if constexpr (X_BITS == 0)
-        xrow = static_cast<const uint32_t*>(xin) + (int64_t)(b0 + r) * in + c0;
-      else
-        xrow = static_cast<const uint32_t*>(xin) + (int64_t)(b0 + r) * ((in + 31) >> 5) + (c0 >> 5);
-#pragma unroll
-      for (int u = 0; u < XU; ++u) xv[u] = xrow[min((tid & 3) + 4 * u, xl - 1)];
-    }
 #pragma unroll
     for (int u = 0; u < WU; ++u) ws[(tid >> 6) * CI + (tid & 63) + 64 * u] = wv[u];
 #pragma unroll
     for (int u = 0; u < XU; ++u) xs[(tid >> 2) * XLD + (tid & 3) + 4 * u] = xv[u];
     __syncthreads();
+    if (c0 + CI < in) load(c0 + CI);
     const float* wr = ws + wave * CI;
     if constexpr (X_BITS == 0) {
       const float* xr = reinterpret_cast<const float*>(xs) + lane * FC_XLD;
