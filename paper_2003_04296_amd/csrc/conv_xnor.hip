@@ -37,7 +37,7 @@ namespace qc {
 
 namespace {
 
-constexpr int XT = 8;         // output tile side
+constexpr int XT = 8;         // output tile side of 3x3 layers (th = tw = 8)
 constexpr int XNC = 8;        // channels per thread
 constexpr int XMP = 4;        // pixels per thread (one row segment)
 constexpr int XCHUNK_LDS = 48 * 1024;  // LDS budget of one block's staged chunk
@@ -45,10 +45,11 @@ constexpr int XCHUNK_LDS = 48 * 1024;  // LDS budget of one block's staged chunk
 struct XArgs {
   ConvArgs c;
   int tiles_x, tiles_y, co_tiles;
+  int th, tw, gshift;  // output tile rows x columns (th * tw = 64); log2 of the 4-pixel groups per row
   int cwc, nchunks;  // input words staged per chunk
   int hr, hc, hcs;   // halo rows, columns, LDS words per (word, plane) row segment
   int half;          // stride 2: columns stored by parity, odd ones from `half`
-  int k1;            // 1x1 kernel: only the sampled pixels are staged (halo = the 8 x 8 tile)
+  int k1;            // 1x1 kernel: only the sampled pixels are staged (halo = the tile)
   int act_words;     // LDS words of the staged activations (per chunk)
   int nblocks;
   int xcd_remap;     // renumber blocks so consecutive logical ids share an XCD
@@ -78,14 +79,14 @@ __global__ __launch_bounds__(256) void conv_xnor_kernel(const XArgs x) {
   const int ty = rest % x.tiles_y;
   const int img = rest / x.tiles_y;
   const int co_blk = ct * CO_B;
-  const int oy0 = ty * XT, ox0 = tx * XT;
+  const int oy0 = ty * x.th, ox0 = tx * x.tw;
   const int iy0 = oy0 * a.stride - a.pad, ix0 = ox0 * a.stride - a.pad;
 
   const int tid = threadIdx.x;
   const int ks = tid % KS;
-  const int pg = (tid / KS) % 16;  // pixel group: row pg / 2, columns 4 (pg % 2) ..
+  const int pg = (tid / KS) % 16;  // pixel group: row pg / (tw / 4), columns 4 (pg % (tw / 4)) ..
   const int cg = tid / (16 * KS);  // channel group: channels 8 cg .. 8 cg + 7 of the block
-  const int prow = pg >> 1, pcol = (pg & 1) * XMP;
+  const int prow = pg >> x.gshift, pcol = (pg & ((1 << x.gshift) - 1)) * XMP;
 
   uint32_t* act_l = xlds;                   // [cwc][PA][hr][hcs]
   uint32_t* wt_l = xlds + x.act_words;      // [tap][cwc][CO_B][PW]
@@ -329,15 +330,34 @@ bool xnor_plan(const ConvArgs& a, int ks, XArgs* x) {
   if (a.pool || a.out_packed || a.mode == QCONV_EPI_BN_PACK) return false;
   if (!((a.kh == 1 && a.kw == 1) || (a.kh == 3 && a.kw == 3)) || a.stride > 2 || a.n == 0) return false;
   const int co_b = 128 / ks;
-  x->tiles_x = ceil_div(a.wo, XT);
-  x->tiles_y = ceil_div(a.ho, XT);
-  x->co_tiles = ceil_div(a.cout, co_b);
   x->k1 = a.kh == 1 ? 1 : 0;
+  // 1x1 layers stage only the sampled pixels, so their tile may be wider than
+  // tall at no staging cost: of 2 x 32, 4 x 16 and 8 x 8 the shape with the
+  // fewest pixel slots over the output, the widest on ties (longer runs of
+  // each output row in one store: ResNet-18's 28 x 28 shortcut output in
+  // rows of 28 instead of 8); 3x3 layers keep 8 x 8 (the least halo)
+  x->tw = XT;
   if (x->k1) {
-    x->hr = x->hc = x->hcs = XT;
+    int64_t best = -1;
+    for (int tw : {32, 16, 8}) {
+      const int64_t slots = (int64_t)ceil_div(a.wo, tw) * ceil_div(a.ho, 64 / tw);
+      if (best < 0 || slots < best) {
+        best = slots;
+        x->tw = tw;
+      }
+    }
+  }
+  x->th = 64 / x->tw;
+  x->gshift = x->tw == 32 ? 3 : (x->tw == 16 ? 2 : 1);
+  x->tiles_x = ceil_div(a.wo, x->tw);
+  x->tiles_y = ceil_div(a.ho, x->th);
+  x->co_tiles = ceil_div(a.cout, co_b);
+  if (x->k1) {
+    x->hr = x->th;
+    x->hc = x->hcs = x->tw;
   } else {
-    x->hr = (XT - 1) * a.stride + a.kh;
-    x->hc = (XT - 1) * a.stride + a.kw;
+    x->hr = (x->th - 1) * a.stride + a.kh;
+    x->hc = (x->tw - 1) * a.stride + a.kw;
     x->half = (x->hc + 1) / 2;
     x->hcs = a.stride == 2 ? 2 * x->half : x->hc;
   }

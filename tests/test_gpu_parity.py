@@ -239,7 +239,22 @@ XNOR_CASES = [
     (3, 520, 9, 11, 70, 3, 1, 1),     # several staged chunks of words, ragged tiles and channels
     (2, 33, 30, 30, 40, 3, 2, 1),     # stride 2 with odd halo columns, ragged last word
     (5, 96, 7, 7, 300, 1, 1, 0),      # 1x1 stride 1, three channel tiles
+    (3, 70, 27, 27, 50, 1, 2, 0),     # 1x1 stride 2 on 4 x 16 tiles (14 x 14 output), ragged words and channels
+    (2, 40, 4, 60, 36, 1, 1, 0),      # 1x1 on 2 x 32 tiles, a ragged last column tile
 ]
+
+
+def _xnor_tiles(k, ho, wo):
+    """Output tiles of the XNOR kernel: 8 x 8 for 3x3 layers; for 1x1 layers
+    the one of 2 x 32, 4 x 16, 8 x 8 with the fewest tiles (widest on ties)."""
+    if k != 1:
+        return -(-ho // 8) * -(-wo // 8)
+    best = None
+    for tw in (32, 16, 8):
+        t = -(-wo // tw) * -(-ho // (64 // tw))
+        if best is None or t < best:
+            best = t
+    return best
 
 
 def _expected_ks(case):
@@ -247,7 +262,7 @@ def _expected_ks(case):
     ho, wo = (h + 2 * p - k) // s + 1, (w + 2 * p - k) // s + 1
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     for ks in (1, 2, 4):
-        if n * -(-ho // 8) * -(-wo // 8) * -(-cout // (128 // ks)) >= 2 * cus:
+        if n * _xnor_tiles(k, ho, wo) * -(-cout // (128 // ks)) >= 2 * cus:
             return ks
     return 4
 
