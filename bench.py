@@ -49,7 +49,10 @@ VALU_LANE_OPS = 256 * 64 * 2.4e9
 HBM_PEAK_GBS = 8000.0
 FP32_PEAK_GOPS = 157.3e3  # fp32 vector and fp32 matrix cores alike
 # dense matrix-core peaks (ops = 2 per MAC), in G: int8 5.0 POP/s, fp4 10.1 PFLOP/s, fp16 2.5 PFLOP/s
-MFMA_PEAK_GOPS = {"mfma_i8": 5.0e6, "mfma_fp4": 10.1e6, "mfma_f16": 2.5e6}
+MFMA_PEAK_GOPS = {"mfma_i8": 5.0e6, "mfma_fp4": 10.1e6, "mfma_f16": 2.5e6, "mfma_bf16": 2.5e6}
+# an fp32 conv through exact three-way bf16 splits costs six bf16 products
+# per multiply-add: its roofline is the bf16 peak over six, in fp32 conv-ops
+BF16X6_PEAK_GOPS = MFMA_PEAK_GOPS["mfma_bf16"] / 6
 # Minimal VALU recipe (lane-ops per 32-channel word pair) of the bitplane
 # product on gfx950, where v_bitop3_b32 fuses any 3-input bit function:
 #   1W1A: xor, bcnt                         -> 2
@@ -390,6 +393,8 @@ def layer_work(net, li, batch, dev):
     if kind == "conv_f32":
         k = L["k"]
         ops = 2.0 * n * co * ho * wo * ci * k * k
+        if "bf16x6" in kname:
+            return ops, bin_ + co * ci * k * k * 4 + bout + extra, BF16X6_PEAK_GOPS, "mfma_bf16x6", kname
         return ops, bin_ + co * ci * k * k * 4 + bout + extra, FP32_PEAK_GOPS, "fp32", kname
     if kind == "qconv":
         k, s, p = L["k"], L["stride"], L["pad"]
@@ -416,6 +421,7 @@ def net_entry(wl, dev, stream, steps, warmup, cpu, cpu_budget=8.0):
     """Whole forward (images/s) plus each layer against its own roofline."""
     from paper_2003_04296_amd.nets import build_convnet, build_resnet18
 
+    f32_note = None
     if wl == "convnet":
         params = synth.convnet_params(seed=1003, batch=256)
         qn = build_convnet(params, dev)
@@ -428,6 +434,8 @@ def net_entry(wl, dev, stream, steps, warmup, cpu, cpu_budget=8.0):
         params = synth.resnet18_params(seed=1004, batch=64)
         qn = build_resnet18(params, dev)
         name, dtype = "resnet18_2w2a_batch64_224x224", ALGO_DTYPE["mfma_fp4"]
+        f32_note = ("stem: fp32 conv as exact three-way bf16 splits, six bf16 x bf16 -> f32 products "
+                    "per multiply-add (fp32 accuracy)")
     x = params["x"].to(dev)
     batch = x.shape[0]
     logits = torch.empty((batch, qn.out_features), dtype=torch.float32, device=dev)
@@ -464,6 +472,8 @@ def net_entry(wl, dev, stream, steps, warmup, cpu, cpu_budget=8.0):
     e = {"workload": name, "value": round(batch / dt, 1), "unit": "images/s", "ms_per_step": round(dt * 1e3, 4),
          "dtype": dtype, "config": {"batch": batch, "weights": "packed once before timing"}, "roofline": rf,
          "layers": layers}
+    if f32_note:
+        e["config"]["f32_layers"] = f32_note
     if cpu:
         e["cpu_baseline"] = cpu_baseline_net(params, wl, cpu_budget)
     return e

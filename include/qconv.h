@@ -309,8 +309,18 @@ void qnet_destroy(qnet* net);
  *     does not fit (its LDS holds the input window, cin * k * k weights of
  *     32 channels and a pooled tile) fall back to the chain.
  *   QNET_F32_FMAF_CHAIN: each output one fmaf chain over (ci, kh, kw) from
- *     +0, a fixed order that makes networks reproducible bit for bit. */
-enum { QNET_F32_FMAF_CHAIN = 0, QNET_F32_MFMA = 1 };
+ *     +0, a fixed order that makes networks reproducible bit for bit.
+ *   QNET_F32_BF16X6: as QNET_F32_MFMA, except that a 7 x 7 / 2 conv with its
+ *     3 x 3 / 2 pooling fused and cin <= 3 (the ResNet stem) runs on the bf16
+ *     matrix cores: every input and weight is split exactly into three bf16
+ *     parts (x = x0 + x1 + x2, each part the leading 8 significant bits of
+ *     what is left) and the six partial products xi wj with i + j <= 2 are
+ *     summed in fp32 (x0 w0 apart from the five smaller ones).  The three
+ *     dropped products are below 2^-20 |x w|, so results stay within fp32
+ *     rounding of the exact sum: |err| <= (gamma_K + 2^-19) sum |x w|.
+ *     Inputs and weights must be finite (an inf or NaN makes the outputs
+ *     whose windows hold it NaN). */
+enum { QNET_F32_FMAF_CHAIN = 0, QNET_F32_MFMA = 1, QNET_F32_BF16X6 = 2 };
 int qnet_set_f32_algo(qnet* net, int algo);
 
 /* fp32 conv (zero padding; the sum over (ci, kh, kw) as qnet_set_f32_algo

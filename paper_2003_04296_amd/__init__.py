@@ -18,7 +18,7 @@ QCONV_ESCRATCH = -6
 ALGO_AUTO, ALGO_BITPLANE, ALGO_MFMA_I8, ALGO_MFMA_FP4, ALGO_MFMA_F16 = 0, 1, 2, 3, 4
 EPI_INT32, EPI_SCALE_F32, EPI_BN_F32, EPI_BN_PACK = 0, 1, 2, 3
 EPI_POOL2, EPI_RESIDUAL = 1, 2
-F32_FMAF_CHAIN, F32_MFMA = 0, 1
+F32_FMAF_CHAIN, F32_MFMA, F32_BF16X6 = 0, 1, 2
 OP_NAMES = {1: "XNOR", 2: "SHIFT", 3: "XNOR-ADDER", 4: "SHIFT-ADDER", 5: "MAC"}
 
 EXPORTED = (

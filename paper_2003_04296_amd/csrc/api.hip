@@ -388,7 +388,16 @@ int run_layers(const qnet* net, const float* x, int batch, float* logits, char* 
 bool conv_uses_mfma(const qnet* net, const QLayer& l) {
   if (l.kind != L_CONV_F32 || !l.f32_mfma) return false;
   const QTensor& s = net->t[l.src];
-  return conv_f32_mfma_supports(1, s.c, s.h, s.w, l.cout, l.k, l.stride, l.pad, l.pool_dst > 0 ? 1 : 0);
+  return conv_f32_mfma_supports(1, s.c, s.h, s.w, l.cout, l.k, l.stride, l.pad, l.pool_dst > 0 ? 1 : 0, 0);
+}
+
+// The matrix-core arithmetic of such a layer: 1 (exact bf16 splits, six
+// partial products) when the network asks for it and the layer is a pooled
+// geometry that kernel takes, else 0 (fp32 matrix cores).
+int conv_mfma_alg(const qnet* net, const QLayer& l) {
+  if (net->f32_algo != QNET_F32_BF16X6 || l.pool_dst <= 0) return 0;
+  const QTensor& s = net->t[l.src];
+  return conv_f32_mfma_supports(1, s.c, s.h, s.w, l.cout, l.k, l.stride, l.pad, 1, 1) ? 1 : 0;
 }
 }  // namespace
 
@@ -462,13 +471,14 @@ int qnet_add_conv_f32(qnet* net, int src, const float* w, int cout, int k, int s
   if (ho < 1 || wo < 1) return QCONV_EINVAL;
   // matrix cores when the network asks for them and the kernel fits the layer
   // unpooled or pooled (a fused pooling decides which, see conv_uses_mfma)
-  l.f32_mfma = net->f32_algo == QNET_F32_MFMA && (conv_f32_mfma_supports(1, s.c, s.h, s.w, cout, k, stride, pad, 0) ||
-                                                  conv_f32_mfma_supports(1, s.c, s.h, s.w, cout, k, stride, pad, 1));
+  l.f32_mfma = net->f32_algo != QNET_F32_FMAF_CHAIN && (conv_f32_mfma_supports(1, s.c, s.h, s.w, cout, k, stride, pad, 0, 0) ||
+                                                  conv_f32_mfma_supports(1, s.c, s.h, s.w, cout, k, stride, pad, 1, 0));
   return add_tensor(net, l, {cout, ho, wo, out_bits});
 }
 
 int qnet_set_f32_algo(qnet* net, int algo) {
-  if (!net || (algo != QNET_F32_FMAF_CHAIN && algo != QNET_F32_MFMA) || !net->L.empty()) return QCONV_EINVAL;
+  if (!net || (algo != QNET_F32_FMAF_CHAIN && algo != QNET_F32_MFMA && algo != QNET_F32_BF16X6) || !net->L.empty())
+    return QCONV_EINVAL;
   net->f32_algo = algo;
   return QCONV_OK;
 }
@@ -491,7 +501,7 @@ int qnet_add_maxpool_f32(qnet* net, int src, int k, int stride, int pad) {
     QLayer& prod = net->L[src - 1];
     const QTensor& ps = net->t[prod.src];
     if (prod.kind == L_CONV_F32 && prod.f32_mfma && prod.out_bits == 0 && prod.pool_dst < 0 && prod.pack_dst < 0 &&
-        conv_f32_mfma_supports(1, ps.c, ps.h, ps.w, prod.cout, prod.k, prod.stride, prod.pad, 1)) {
+        conv_f32_mfma_supports(1, ps.c, ps.h, ps.w, prod.cout, prod.k, prod.stride, prod.pad, 1, 0)) {
       prod.pool_dst = (int)net->t.size();
       l.fused = 1;
     }
@@ -526,7 +536,7 @@ int qnet_add_quantize(qnet* net, int src, int bits) {
   } else if (src > 0 && prod.kind == L_CONV_F32 && prod.f32_mfma && prod.out_bits == 0 && prod.pool_dst < 0 &&
              prod.pack_dst < 0) {
     const QTensor& ps = net->t[prod.src];
-    if (conv_f32_mfma_supports(1, ps.c, ps.h, ps.w, prod.cout, prod.k, prod.stride, prod.pad, 0)) {
+    if (conv_f32_mfma_supports(1, ps.c, ps.h, ps.w, prod.cout, prod.k, prod.stride, prod.pad, 0, 0)) {
       prod.pack_dst = id;
       l.fused = 1;
     }
@@ -667,7 +677,7 @@ int run_layers(const qnet* net, const float* x, int batch, float* logits, char* 
                                       : (l.pack_dst > 0 ? static_cast<uint32_t*>(ptr(l.pack_dst)) : nullptr);
           rc = launch_conv_f32_mfma(static_cast<const float*>(ptr(l.src)), l.wf, batch, si.c, si.h, si.w, l.cout, l.k,
                                     l.stride, l.pad, l.bn_k, l.bn_b, l.relu, pool ? 1 : 0, outf, outp, ob,
-                                    dflt[ob ? ob : 1], s);
+                                    dflt[ob ? ob : 1], conv_mfma_alg(net, l), s);
           break;
         }
         float* wt = reinterpret_cast<float*>(ws + woff[i]);
@@ -750,7 +760,8 @@ int qnet_layer_kernel(const qnet* net, int layer, int batch, char* buf, int len)
   } else if (l.kind == L_CONV_F32) {
     if (conv_uses_mfma(net, l)) {
       const int ob = l.out_bits ? l.out_bits : (l.pack_dst > 0 ? net->t[l.pack_dst].bits : 0);
-      snprintf(name, sizeof(name), "conv_f32_mfma_kernel<%d, %d, %d, %d>", l.k, l.stride, l.pool_dst > 0 ? 1 : 0, ob);
+      snprintf(name, sizeof(name), "conv_f32_%s_kernel<%d, %d, %d, %d>", conv_mfma_alg(net, l) ? "bf16x6" : "mfma", l.k,
+               l.stride, l.pool_dst > 0 ? 1 : 0, ob);
     } else {
       snprintf(name, sizeof(name), "conv_f32_kernel<%d, %d>", l.out_bits, (l.out_bits == 0 && l.cout > 32) ? 64 : 32);
     }

@@ -63,6 +63,32 @@ constexpr int S2_WP = 81;             // stride 2: row pitch (17 mod 64)
 // smallest v >= x with v = 32 (mod 64)
 __host__ __device__ constexpr int up_32mod64(int x) { return x <= 32 ? 32 : ((x - 32 + 63) / 64) * 64 + 32; }
 
+// bf16x6 (the 7 x 7 / 2 pooled geometry): the window is held as three bf16
+// planes of the exact split x = x0 + x1 + x2, rows of X6_RPW words (two
+// bf16 each) and channels of X6_CIPW words; 21 words per row keep the 32
+// pixels of each half of a wave's read in 32 distinct banks.
+constexpr int X6_RPW = 21;
+constexpr int X6_CIPW = 35 * X6_RPW;  // 35 window rows of the pooled 7 x 7 / 2 tile
+constexpr int X6_PLW = 3 * X6_CIPW + 1;  // words per plane: up to 3 input channels and a spare word
+
+// Exact split of an fp32 value into three bf16 parts, x = p0 + p1 + p2:
+// p0 is x cut to its top 16 bits (the leading 8 significand bits), the
+// remainder x - p0 is exact in fp32 (same sign and exponent range), and so
+// is the second cut; what is left has at most 8 significant bits, so it is
+// itself a bf16.  Cutting rather than rounding keeps every part no larger
+// than what it splits, and no part overflows.  A non-finite x keeps its
+// first part (a NaN made quiet) and zero for the others.
+__device__ __forceinline__ void split_bf16x3(float x, uint32_t& h0, uint32_t& h1, uint32_t& h2) {
+  const uint32_t u = __float_as_uint(x);
+  const float r1 = x - __uint_as_float(u & 0xFFFF0000u);
+  const uint32_t v = __float_as_uint(r1);
+  const float r2 = r1 - __uint_as_float(v & 0xFFFF0000u);
+  const bool fin = (u & 0x7F800000u) != 0x7F800000u;
+  h0 = (!fin && (u & 0x007FFFFFu)) ? 0x7FC0u : (u >> 16);
+  h1 = fin ? (v >> 16) : 0u;
+  h2 = fin ? (__float_as_uint(r2) >> 16) : 0u;
+}
+
 template <int KSZ, int S, int POOL>
 struct Geo {
   static constexpr int CT_H = POOL ? 2 * PT_H + 1 : PT_H0;  // conv pixels of a tile
@@ -132,13 +158,28 @@ struct F32M {
   int l_w, l_pk;  // LDS float offsets: weights, packed staging (window / conv tile region at 0)
 };
 
-template <int KSZ, int S, int POOL, int OB>
-__global__ __launch_bounds__(256, 2) void conv_f32_mfma_kernel(const F32M m) {
+// ALG 0: the fp32 matrix cores.  ALG 1 (bf16x6; the pooled 7 x 7 / 2
+// geometry only): each window element and weight is split exactly into
+// three bf16 parts, x = x0 + x1 + x2 and w = w0 + w1 + w2, and the six
+// partial products with i + j <= 2 are summed on the bf16 matrix cores
+// (v_mfma_f32_32x32x16_bf16), x0 w0 in one accumulator and the five
+// smaller ones in a second, added at the end.  The three dropped products
+// are below 2^-20 |x w| together, so each output stays within fp32
+// rounding of the exact sum (the bound is derived with the tests).  A
+// k-step of 16 is two (ci, ky) tap rows: lanes 0-31 take row 2 j, lanes
+// 32-63 row 2 j + 1, each as 4 words of two bf16 (taps kx, kx + 1; the
+// eighth slot, past the row, is masked to zero).
+template <int ALG, int KSZ, int S, int POOL, int OB>
+__device__ __forceinline__ void f32m_body(const F32M& m) {
+  static_assert(ALG == 0 || (KSZ == 7 && S == 2 && POOL == 1), "bf16x6 geometry");
   using G = Geo<KSZ, S, POOL>;
   constexpr int KS2 = G::KS2, IW = G::IW, WIN = G::WIN, CIP = G::CIP, CT_W = G::CT_W;
   extern __shared__ __attribute__((aligned(16))) float fl[];
   float* xin = fl;
   float* wB = fl + m.l_w;
+  uint16_t* xh = reinterpret_cast<uint16_t*>(fl);             // bf16x6: the window's three planes
+  const uint32_t* xw = reinterpret_cast<const uint32_t*>(fl);
+  uint16_t* wh = reinterpret_cast<uint16_t*>(fl + m.l_w);     // bf16x6: the weights' parts
   float* ctile = fl;                       // pooling: conv tile over the consumed window
   float* ptile = fl + CT_PIX * CT_PITCH;   // pooling: staged fp32 pooled tile
   uint32_t* pk = reinterpret_cast<uint32_t*>(fl + m.l_pk);
@@ -150,13 +191,42 @@ __global__ __launch_bounds__(256, 2) void conv_f32_mfma_kernel(const F32M m) {
   const int ct0 = (blockIdx.x % m.co_groups) * (POOL ? 1 : m.nct);
   const int nct = POOL ? 1 : min(m.nct, m.co_tiles - ct0);
 
-  // weights of the block's channels, [tile][ci][k-step][half][32] (padding
-  // taps and channels past cout 0)
-  for (int i = tid; i < nct * m.cin * KS2 * 64; i += 256) {
-    const int c = i & 31, h = (i >> 5) & 1, r = i >> 6, cq = r / (m.cin * KS2), r2 = r - cq * (m.cin * KS2);
-    const int ci = r2 / KS2, st = r2 - ci * KS2, co = (ct0 + cq) * 32 + c;
-    const int tap = step_tap<KSZ, S>(st, h);
-    wB[i] = (tap >= 0 && co < m.cout) ? m.wt[((int64_t)co * m.cin + ci) * G::KK + tap] : 0.0f;
+  // bf16x6: tap rows (ci, ky) of the contraction and its k-steps of two rows
+  const int x6_rows = m.cin * KSZ, x6_steps = (x6_rows + 1) / 2;
+  if constexpr (ALG == 0) {
+    // weights of the block's channels, [tile][ci][k-step][half][32] (padding
+    // taps and channels past cout 0)
+    for (int i = tid; i < nct * m.cin * KS2 * 64; i += 256) {
+      const int c = i & 31, h = (i >> 5) & 1, r = i >> 6, cq = r / (m.cin * KS2), r2 = r - cq * (m.cin * KS2);
+      const int ci = r2 / KS2, st = r2 - ci * KS2, co = (ct0 + cq) * 32 + c;
+      const int tap = step_tap<KSZ, S>(st, h);
+      wB[i] = (tap >= 0 && co < m.cout) ? m.wt[((int64_t)co * m.cin + ci) * G::KK + tap] : 0.0f;
+    }
+  } else {
+    // the three parts of the weights as B operands: k-step j holds, per
+    // part, 64 lanes x 8 bf16 (lane = row half x channel; slot e = tap kx,
+    // slot 7 zero), 1536 bf16 per k-step; with an odd row count the last
+    // k-step holds only its first row's 32 lanes per part
+    const int last_lanes = (x6_rows & 1) ? 32 : 64;
+    for (int i = tid; i < 64 * x6_steps; i += 256) {
+      const int j = i >> 6, ln = i & 63, ll = j == x6_steps - 1 ? last_lanes : 64;
+      if (ln >= ll) continue;
+      const int g = 2 * j + (ln >> 5), ci = g / KSZ, ky = g - ci * KSZ, co = ct0 * 32 + (ln & 31);
+      uint32_t pw[3][4];
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        uint32_t a[3], b[3];
+        const float* wr = m.wt + (((int64_t)co * m.cin + ci) * KSZ + ky) * KSZ;
+        const bool ok = co < m.cout;
+        split_bf16x3(ok ? wr[e] : 0.0f, a[0], a[1], a[2]);
+        split_bf16x3(ok && e + 1 < KSZ ? wr[e + 1] : 0.0f, b[0], b[1], b[2]);
+#pragma unroll
+        for (int q = 0; q < 3; ++q) pw[q][e / 2] = a[q] | (b[q] << 16);
+      }
+#pragma unroll
+      for (int q = 0; q < 3; ++q)
+        *reinterpret_cast<uint4*>(wh + j * 1536 + (q * ll + ln) * 8) = make_uint4(pw[q][0], pw[q][1], pw[q][2], pw[q][3]);
+    }
   }
   // per-channel epilogue parameters of this lane's channel in each tile
   float bkv[NCT_MAX], bbv[NCT_MAX];
@@ -185,12 +255,15 @@ __global__ __launch_bounds__(256, 2) void conv_f32_mfma_kernel(const F32M m) {
     const int e = tid + 256 * j;
     eoff[j] = 0;
     eyx[j] = 0xFFFFFFFFu;
-    edst[j] = m.cin * CIP;
+    edst[j] = ALG ? m.cin * X6_CIPW * 2 : m.cin * CIP;
     if (e < welems) {
       const int ci = e / WIN, r = e - ci * WIN, yy = r / IW, xx = r - (r / IW) * IW;
       eoff[j] = (ci * m.h + yy) * m.w + xx;
       eyx[j] = ((uint32_t)yy << 16) | (uint32_t)xx;
-      edst[j] = S == 2 ? ci * CIP + (yy & 1) * G::HRP + (yy >> 1) * S2_WP + (xx & 1) * S2_HW + (xx >> 1) : e;
+      if constexpr (ALG == 1)
+        edst[j] = (ci * X6_CIPW + yy * X6_RPW) * 2 + xx;  // bf16 slot in each plane
+      else
+        edst[j] = S == 2 ? ci * CIP + (yy & 1) * G::HRP + (yy >> 1) * S2_WP + (xx & 1) * S2_HW + (xx >> 1) : e;
     }
   }
   float wval[F32M_NJ];
@@ -242,13 +315,33 @@ __global__ __launch_bounds__(256, 2) void conv_f32_mfma_kernel(const F32M m) {
     bA[t] = pb + half * (S == 2 ? S2_HW : 1);
     bB[t] = pb + half * (S == 2 ? G::HRP : IW - (KSZ - 1));
   }
+  // bf16x6: word offset of each M-tile's pixel in a plane (window row 2 r,
+  // word c: taps kx, kx + 1 of column 2 c + kx)
+  int pbw[2];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int pi = (wave * 2 + t) * 32 + l32;
+    const int pc = pi < G::CT_H * CT_W ? pi : 0;
+    const int pr = pc / CT_W;
+    pbw[t] = 2 * pr * X6_RPW + (pc - pr * CT_W);
+  }
 
   for (int item = first; item < m.items; item += step_items) {
     int img, ty, tx, cy0, cx0;
     origin(item, &img, &ty, &tx, &cy0, &cx0);
     lds_barrier();  // the previous item's LDS tiles are consumed
 #pragma unroll
-    for (int j = 0; j < F32M_NJ; ++j) xin[edst[j]] = wval[j];  // elements past the window land on the spare slot
+    for (int j = 0; j < F32M_NJ; ++j) {  // elements past the window land on the spare slot
+      if constexpr (ALG == 1) {
+        uint32_t p0, p1, p2;
+        split_bf16x3(wval[j], p0, p1, p2);
+        xh[edst[j]] = (uint16_t)p0;
+        xh[2 * X6_PLW + edst[j]] = (uint16_t)p1;
+        xh[4 * X6_PLW + edst[j]] = (uint16_t)p2;
+      } else {
+        xin[edst[j]] = wval[j];
+      }
+    }
     lds_barrier();
     if (item + step_items < m.items) load_window(item + step_items);
 
@@ -264,6 +357,63 @@ __global__ __launch_bounds__(256, 2) void conv_f32_mfma_kernel(const F32M m) {
       }
     // ---- MFMAs: this wave's 2 M-tiles x 32 channels ----
     v16f acc0 = {}, acc1 = {};
+    if constexpr (ALG == 1) {
+      typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+      auto mm = [](uint4 a, uint4 b, v16f c) __attribute__((always_inline)) {
+        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, a), __builtin_bit_cast(v8bf, b), c, 0,
+                                                       0, 0);
+      };
+      v16f cor0 = {}, cor1 = {};
+      // one k-step: B parts from wj (ll lanes per part, this lane's at lb),
+      // A parts of both M-tiles from word offset rb (zero: all operands 0)
+      auto kstep = [&](const uint16_t* wj, int ll, int lb, int rb, bool zero) __attribute__((always_inline)) {
+        uint4 b[3], a0[3], a1[3];
+#pragma unroll
+        for (int q = 0; q < 3; ++q) b[q] = *reinterpret_cast<const uint4*>(wj + (q * ll + lb) * 8);
+        const uint32_t* r0 = xw + rb + pbw[0];
+        const uint32_t* r1 = xw + rb + pbw[1];
+#pragma unroll
+        for (int q = 0; q < 3; ++q) {
+          const int o = q * X6_PLW;
+          a0[q] = make_uint4(r0[o], r0[o + 1], r0[o + 2], r0[o + 3] & 0xFFFFu);  // slot 7 (past the row) is 0
+          a1[q] = make_uint4(r1[o], r1[o + 1], r1[o + 2], r1[o + 3] & 0xFFFFu);
+          if (zero) {
+            a0[q] = make_uint4(0u, 0u, 0u, 0u);
+            a1[q] = make_uint4(0u, 0u, 0u, 0u);
+          }
+        }
+        // the five small products first, into their own accumulator
+        cor0 = mm(a0[2], b[0], cor0);
+        cor1 = mm(a1[2], b[0], cor1);
+        cor0 = mm(a0[1], b[1], cor0);
+        cor1 = mm(a1[1], b[1], cor1);
+        cor0 = mm(a0[0], b[2], cor0);
+        cor1 = mm(a1[0], b[2], cor1);
+        cor0 = mm(a0[1], b[0], cor0);
+        cor1 = mm(a1[1], b[0], cor1);
+        cor0 = mm(a0[0], b[1], cor0);
+        cor1 = mm(a1[0], b[1], cor1);
+        acc0 = mm(a0[0], b[0], acc0);
+        acc1 = mm(a1[0], b[0], acc1);
+      };
+      // this lane's tap row 2 j + half as (ci, ky) and its word offset
+      int ky = half, rb = half * X6_RPW;
+      const int nfull = x6_rows >> 1;
+      for (int j = 0; j < nfull; ++j) {
+        kstep(wh + j * 1536, 64, lane, rb, false);
+        ky += 2;
+        rb += 2 * X6_RPW;
+        if (ky >= KSZ) {
+          ky -= KSZ;
+          rb += X6_CIPW - KSZ * X6_RPW;
+        }
+      }
+      // an odd row count: the last row alone, lanes 32-63 with zero
+      // activations (read at row 0) against the first half's weights
+      if (x6_rows & 1) kstep(wh + nfull * 1536, 32, l32, half ? 0 : rb, half != 0);
+      acc0 += cor0;
+      acc1 += cor1;
+    } else {
     for (int ci = 0; ci < m.cin; ++ci) {
       const float* xa0 = xin + ci * CIP + bA[0];
       const float* xa1 = xin + ci * CIP + bA[1];
@@ -285,6 +435,7 @@ __global__ __launch_bounds__(256, 2) void conv_f32_mfma_kernel(const F32M m) {
         acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, bv, acc1, 0, 0, 0);
       }
     }
+    }  // ALG
 
     // ---- epilogue ----
     // register v of lane l: channel co_blk + l % 32, tile pixel 32 T + 8 (v / 4) + 4 (l / 32) + v % 4
@@ -455,6 +606,16 @@ __global__ __launch_bounds__(256, 2) void conv_f32_mfma_kernel(const F32M m) {
   }
 }
 
+template <int KSZ, int S, int POOL, int OB>
+__global__ __launch_bounds__(256, 2) void conv_f32_mfma_kernel(const F32M m) {
+  f32m_body<0, KSZ, S, POOL, OB>(m);
+}
+
+template <int KSZ, int S, int POOL, int OB>
+__global__ __launch_bounds__(256, 2) void conv_f32_bf16x6_kernel(const F32M m) {
+  f32m_body<1, KSZ, S, POOL, OB>(m);
+}
+
 int device_cus_f() {
   int dev = 0, v = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 256;
@@ -473,11 +634,12 @@ void geo_rt(int k, int s, int pool, int* ih, int* iw, int* cip) {
 
 size_t f32m_lds(const F32M& m, int pool);
 
-bool f32m_plan(int n, int cin, int h, int w, int cout, int k, int stride, int pad, int pool, F32M* m) {
+bool f32m_plan(int n, int cin, int h, int w, int cout, int k, int stride, int pad, int pool, int alg, F32M* m) {
   memset(m, 0, sizeof(*m));
   if (n < 1 || cin < 1 || pad < 0 || cout < 1) return false;
   if (k != 3 && k != 5 && k != 7) return false;               // instantiated kernel sizes
   if (!(stride == 1 || (stride == 2 && pool))) return false;  // instantiated strides
+  if (alg && !(k == 7 && stride == 2 && pool && cin <= 3)) return false;  // the bf16x6 geometry
   m->n = n;
   m->cin = cin;
   m->h = h;
@@ -513,13 +675,14 @@ bool f32m_plan(int n, int cin, int h, int w, int cout, int k, int stride, int pa
   // staging; plain tiles take as many channel tiles per block (up to 4) as
   // fit, so that a window staged once feeds all of them
   const int taps2 = 2 * ((k * k + 1) / 2);  // padded taps per input channel
-  int64_t region = (int64_t)cin * cip + 1;  // + the spare slot of the elements past the window
+  int64_t region = alg ? 3 * X6_PLW : (int64_t)cin * cip + 1;  // + the spare slot of the elements past the window
   if (pool) region = std::max<int64_t>(region, (int64_t)CT_PIX * CT_PITCH + 32 * PO_PITCH);
   m->l_w = (int)((region + 3) & ~(int64_t)3);
   for (int nct = pool ? 1 : std::min(m->co_tiles, NCT_MAX); nct >= 1; --nct) {
     m->nct = nct;
     m->co_groups = ceil_div(m->co_tiles, nct);
-    m->l_pk = m->l_w + nct * cin * taps2 * 32;
+    const int x6_rows = cin * k;  // bf16x6: 1536 bf16 per k-step of two tap rows, 768 for a last single row
+    m->l_pk = m->l_w + (alg ? ((x6_rows / 2) * 1536 + (x6_rows & 1) * 768) / 2 : nct * cin * taps2 * 32);
     if (f32m_lds(*m, pool) <= F32M_LDS_MAX) return true;
   }
   return false;
@@ -530,7 +693,7 @@ size_t f32m_lds(const F32M& m, int pool) {
 }
 
 template <int KSZ, int S, int POOL>
-int launch_geo(const F32M& m, int ob, int grid, size_t lds, hipStream_t s) {
+int launch_geo(const F32M& m, int ob, int alg, int grid, size_t lds, hipStream_t s) {
   auto go = [&](auto kern) -> int {
     if (lds > 64 * 1024 && hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                                hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -539,6 +702,16 @@ int launch_geo(const F32M& m, int ob, int grid, size_t lds, hipStream_t s) {
     kern<<<dim3((unsigned)grid), 256, lds, s>>>(m);
     return hip_status();
   };
+  if constexpr (KSZ == 7 && S == 2 && POOL == 1) {
+    if (alg) {
+      switch (ob) {
+        case 0: return go(conv_f32_bf16x6_kernel<KSZ, S, POOL, 0>);
+        case 1: return go(conv_f32_bf16x6_kernel<KSZ, S, POOL, 1>);
+        case 2: return go(conv_f32_bf16x6_kernel<KSZ, S, POOL, 2>);
+        default: return go(conv_f32_bf16x6_kernel<KSZ, S, POOL, 3>);
+      }
+    }
+  }
   switch (ob) {
     case 0: return go(conv_f32_mfma_kernel<KSZ, S, POOL, 0>);
     case 1: return go(conv_f32_mfma_kernel<KSZ, S, POOL, 1>);
@@ -549,17 +722,17 @@ int launch_geo(const F32M& m, int ob, int grid, size_t lds, hipStream_t s) {
 
 }  // namespace
 
-bool conv_f32_mfma_supports(int n, int cin, int h, int w, int cout, int k, int stride, int pad, int pool) {
+bool conv_f32_mfma_supports(int n, int cin, int h, int w, int cout, int k, int stride, int pad, int pool, int alg) {
   F32M m;
-  return f32m_plan(n > 0 ? n : 1, cin, h, w, cout, k, stride, pad, pool, &m);
+  return f32m_plan(n > 0 ? n : 1, cin, h, w, cout, k, stride, pad, pool, alg, &m);
 }
 
 int launch_conv_f32_mfma(const float* x, const float* w, int n, int cin, int h, int wd, int cout, int k, int stride,
                          int pad, const float* bn_k, const float* bn_b, int relu, int pool, float* out,
-                         uint32_t* out_packed, int out_bits, Thr othr, hipStream_t s) {
+                         uint32_t* out_packed, int out_bits, Thr othr, int alg, hipStream_t s) {
   F32M m;
   if (n == 0) return QCONV_OK;
-  if (!f32m_plan(n, cin, h, wd, cout, k, stride, pad, pool, &m)) return QCONV_EUNSUPPORTED;
+  if (!f32m_plan(n, cin, h, wd, cout, k, stride, pad, pool, alg, &m)) return QCONV_EUNSUPPORTED;
   m.x = x;
   m.wt = w;
   m.bn_k = bn_k;
@@ -576,17 +749,17 @@ int launch_conv_f32_mfma(const float* x, const float* w, int n, int cin, int h, 
   const size_t lds = f32m_lds(m, pool);
   if (pool) {
     if (stride == 1) {
-      if (k == 3) return launch_geo<3, 1, 1>(m, ob, grid, lds, s);
-      if (k == 5) return launch_geo<5, 1, 1>(m, ob, grid, lds, s);
-      return launch_geo<7, 1, 1>(m, ob, grid, lds, s);
+      if (k == 3) return launch_geo<3, 1, 1>(m, ob, alg, grid, lds, s);
+      if (k == 5) return launch_geo<5, 1, 1>(m, ob, alg, grid, lds, s);
+      return launch_geo<7, 1, 1>(m, ob, alg, grid, lds, s);
     }
-    if (k == 3) return launch_geo<3, 2, 1>(m, ob, grid, lds, s);
-    if (k == 5) return launch_geo<5, 2, 1>(m, ob, grid, lds, s);
-    return launch_geo<7, 2, 1>(m, ob, grid, lds, s);
+    if (k == 3) return launch_geo<3, 2, 1>(m, ob, alg, grid, lds, s);
+    if (k == 5) return launch_geo<5, 2, 1>(m, ob, alg, grid, lds, s);
+    return launch_geo<7, 2, 1>(m, ob, alg, grid, lds, s);
   }
-  if (k == 3) return launch_geo<3, 1, 0>(m, ob, grid, lds, s);
-  if (k == 5) return launch_geo<5, 1, 0>(m, ob, grid, lds, s);
-  return launch_geo<7, 1, 0>(m, ob, grid, lds, s);
+  if (k == 3) return launch_geo<3, 1, 0>(m, ob, alg, grid, lds, s);
+  if (k == 5) return launch_geo<5, 1, 0>(m, ob, alg, grid, lds, s);
+  return launch_geo<7, 1, 0>(m, ob, alg, grid, lds, s);
 }
 
 }  // namespace qc

@@ -303,10 +303,12 @@ int launch_conv_f32(const float* x, const float* wt_t /* [cin][k][k][cout_pad64]
                     uint32_t* out_packed, hipStream_t s);
 // fp32 conv on the matrix cores with BN, ReLU, optional 3x3 / 2 max pooling
 // (pad 1) and an optional packed Q(HardTanh(.)) copy (conv_f32_mfma.hip).
-bool conv_f32_mfma_supports(int n, int cin, int h, int w, int cout, int k, int stride, int pad, int pool);
+// alg 0: fp32 matrix cores; alg 1: exact bf16 splits, six partial products
+// on the bf16 matrix cores (pooled 7 x 7 / 2 layers with cin <= 3 only).
+bool conv_f32_mfma_supports(int n, int cin, int h, int w, int cout, int k, int stride, int pad, int pool, int alg);
 int launch_conv_f32_mfma(const float* x, const float* w, int n, int cin, int h, int wd, int cout, int k, int stride,
                          int pad, const float* bn_k, const float* bn_b, int relu, int pool, float* out,
-                         uint32_t* out_packed, int out_bits, Thr othr, hipStream_t s);
+                         uint32_t* out_packed, int out_bits, Thr othr, int alg, hipStream_t s);
 int launch_transpose_conv_weight(const float* w, int cout, int cin, int k, float* wt_t,
                                  hipStream_t s);
 int launch_maxpool_f32(const float* x, int n, int c, int h, int w, int k, int stride, int pad,

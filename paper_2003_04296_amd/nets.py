@@ -9,7 +9,7 @@ from __future__ import annotations
 
 import torch
 
-from . import F32_MFMA, Net, fold_bn, pack_weight
+from . import F32_BF16X6, F32_MFMA, Net, fold_bn, pack_weight
 
 
 def _dev_bn(bn, device):
@@ -88,12 +88,14 @@ def build_convnet(p: dict, device, a_bits: int = 1, w_bits: int = 1, f32_algo: i
     return QNetwork(net, (3, hw, hw), fo["w"].shape[0], device, ids)
 
 
-def build_resnet18(p: dict, device, a_bits: int = 2, w_bits: int = 2, f32_algo: int = F32_MFMA) -> QNetwork:
+def build_resnet18(p: dict, device, a_bits: int = 2, w_bits: int = 2, f32_algo: int = F32_BF16X6) -> QNetwork:
     """fp32 stem conv 7x7/2 -> BN -> ReLU -> max pool 3x3/2; eight basic
     blocks with quantized convs (q = Q(x); y = Q(BN1(q*W1)); out = BN2(y*W2)
-    + shortcut, shortcut = x or BN_d(q*W_d)); average pool; fp32 FC.  With the
-    matrix-core fp32 algorithm (default) the stem's max pooling and the first
-    block's quantize run in the stem conv's epilogue."""
+    + shortcut, shortcut = x or BN_d(q*W_d)); average pool; fp32 FC.  With a
+    matrix-core fp32 algorithm the stem's max pooling and the first block's
+    quantize run in the stem conv's epilogue; the default runs the stem on
+    the bf16 matrix cores through exact three-way splits (fp32 accuracy, see
+    QNET_F32_BF16X6 in include/qconv.h)."""
     _, _, hh, ww = p["x"].shape
     net = Net(3, hh, ww, f32_algo)
     ids = {}

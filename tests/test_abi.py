@@ -296,12 +296,13 @@ def test_binding_checks_threshold_counts(bits, vals):
     assert arr is not None and list(arr) == [0.0] * {2: 1, 3: 3}[bits]
 
 
-@pytest.mark.parametrize("algo", [q.F32_MFMA, q.F32_FMAF_CHAIN])
+@pytest.mark.parametrize("algo", [q.F32_MFMA, q.F32_BF16X6, q.F32_FMAF_CHAIN])
 def test_stem_fusion_bookkeeping(algo):
     """A 7x7/2 fp32 stem followed by 3x3/2 max pooling and a 2-bit quantize:
-    with the matrix-core algorithm both later layers are written by the stem's
-    epilogue and launch nothing; with the fmaf chains each launches its own
-    kernel.  Host-side only (nothing is launched)."""
+    with the matrix-core algorithms both later layers are written by the
+    stem's epilogue and launch nothing (the bf16x6 one in its own kernel);
+    with the fmaf chains each launches its own kernel.  Host-side only
+    (nothing is launched)."""
     L = q.lib()
     net = q.Net(3, 224, 224, algo)
     h = net._h
@@ -311,12 +312,34 @@ def test_stem_fusion_bookkeeping(algo):
     assert (t1, t2, t3) == (1, 2, 3)
     fused = [L.qnet_layer_fused_into(h, i) for i in range(3)]
     names = [net.layer_kernel(i, 8) for i in range(3)]
-    if algo == q.F32_MFMA:
+    if algo != q.F32_FMAF_CHAIN:
         assert fused == [0, 0, 0]
-        assert names == ["conv_f32_mfma_kernel<7, 2, 1, 2>", "", ""]
+        kind = "bf16x6" if algo == q.F32_BF16X6 else "mfma"
+        assert names == [f"conv_f32_{kind}_kernel<7, 2, 1, 2>", "", ""]
     else:
         assert fused == [0, 1, 2]
         assert names[0].startswith("conv_f32_kernel<") and names[1] and names[2]
+    assert L.qnet_set_f32_algo(h, q.F32_MFMA) == q.QCONV_EINVAL  # layers already added
     assert L.qnet_layer_fused_into(h, 3) == q.QCONV_EINVAL
     assert L.qnet_layer_fused_into(h, -1) == q.QCONV_EINVAL
     assert L.qnet_layer_fused_into(None, 0) == q.QCONV_EINVAL
+
+
+def test_bf16x6_only_takes_the_pooled_7x7_stride_2_geometry():
+    """Under the bf16x6 algorithm, layers outside its geometry (3x3 stride 1,
+    an unpooled conv, more than 3 input channels) keep the fp32 matrix
+    cores; an unknown algorithm value is refused."""
+    L = q.lib()
+    net = q.Net(3, 32, 32, q.F32_BF16X6)
+    t1 = L.qnet_add_conv_f32(net._h, 0, FAKE, 128, 3, 1, 1, FAKE, FAKE, 0, 1)
+    assert t1 == 1 and net.layer_kernel(0, 4) == "conv_f32_mfma_kernel<3, 1, 0, 1>"
+    net4 = q.Net(4, 64, 64, q.F32_BF16X6)
+    t1 = L.qnet_add_conv_f32(net4._h, 0, FAKE, 64, 7, 2, 3, FAKE, FAKE, 1, 0)
+    L.qnet_add_maxpool_f32(net4._h, t1, 3, 2, 1)
+    assert net4.layer_kernel(0, 2).startswith("conv_f32_kernel<")  # the window of 4 channels: the chain
+    net1 = q.Net(1, 64, 64, q.F32_BF16X6)
+    t1 = L.qnet_add_conv_f32(net1._h, 0, FAKE, 40, 7, 2, 3, FAKE, FAKE, 1, 0)
+    L.qnet_add_maxpool_f32(net1._h, t1, 3, 2, 1)
+    assert net1.layer_kernel(0, 2) == "conv_f32_bf16x6_kernel<7, 2, 1, 0>"
+    with pytest.raises(q.QconvError):
+        q.Net(3, 8, 8, 3)

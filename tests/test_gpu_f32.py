@@ -7,7 +7,13 @@ order, so the fp32 results are compared with the exact (float64) value of
 the oracle's layer within the standard bound of recursive summation in any
 order, |err| <= gamma_K * sum |x w| (gamma_K = K u / (1 - K u), u = 2^-24),
 carried through the BN scale, plus two ulps of the result for BN's and the
-final rounding.  Pooling takes maxima, so a pooled output is within the
+final rounding.  The bf16x6 algorithm splits x and w exactly into three bf16
+parts each and drops the products x1 w2, x2 w1 and x2 w2, together below
+2^-20 |x w|; its five kept small products sum in their own accumulator
+(at most 5K terms, together below 2^-5.9 |x w|, so their rounding stays
+below gamma_5K 2^-5.9 sum |x w| < 2^-20.4 sum |x w| for K <= 147) and one
+more rounding adds them to the main sum: its bound gains
+(2^-19 + u) sum |x w|.  Pooling takes maxima, so a pooled output is within the
 largest bound of its window.  A quantized copy may differ from the oracle's
 level only where that bound straddles a threshold.  Networks built this way
 are checked as the readings for fp32 first layers say: the fp32 layer within
@@ -35,13 +41,17 @@ def dev():
     return torch.device("cuda:0")
 
 
-def _ref(x, w, k, b, s, p, relu):
-    """(exact conv -> BN -> ReLU in float64, error bound of an fp32 sum in any order)."""
+def _ref(x, w, k, b, s, p, relu, x6=False):
+    """(exact conv -> BN -> ReLU in float64, error bound of an fp32 sum in any
+    order; x6: plus the bf16x6 split's share)."""
     acc = oracle.conv_f64(x, w, s, p)
     mag = oracle.conv_f64(np.abs(x), np.abs(w), s, p)
     K = w.shape[1] * w.shape[2] * w.shape[3]
     u = 2.0 ** -24
     gamma = K * u / (1 - K * u)
+    if x6:
+        assert K <= 147
+        gamma += 2.0 ** -19 + u
     kk = k.astype(np.float64)[None, :, None, None]
     z = kk * acc + b.astype(np.float64)[None, :, None, None]
     bound = np.abs(kk) * gamma * mag + 4 * u * np.abs(z) + 1e-37
@@ -96,15 +106,23 @@ POOLED = [
     (2, 3, 224, 224, 64, 7, 2, 3),   # the ResNet-18 stem
     (3, 3, 37, 41, 40, 7, 2, 3),     # ragged pooled tiles, a ragged channel tile
     (2, 5, 30, 30, 33, 5, 1, 2),     # stride 1, 15 x 15 pooled outputs
+    (2, 1, 29, 31, 36, 7, 2, 3),     # one input channel: an odd count of tap rows
+    (2, 2, 40, 33, 64, 7, 2, 2),     # two input channels: an even count
 ]
 
 
+def _kernel_name(algo, cin, k, s, pool, ob):
+    x6 = algo == q.F32_BF16X6 and pool and k == 7 and s == 2 and cin <= 3
+    return f"conv_f32_{'bf16x6' if x6 else 'mfma'}_kernel<{k}, {s}, {pool}, {ob}>"
+
+
+@pytest.mark.parametrize("algo", [q.F32_MFMA, q.F32_BF16X6])
 @pytest.mark.parametrize("case", POOLED)
 @pytest.mark.parametrize("bits", [1, 2, 3])
-def test_stem_conv_pool_quantize(dev, case, bits):
+def test_stem_conv_pool_quantize(dev, case, bits, algo):
     n, cin, h, w, cout, k, s, p = case
     x, wt, kk, bb = _inputs(70 + sum(case), n, cin, h, w, cout, k)
-    net = q.Net(cin, h, w, q.F32_MFMA)
+    net = q.Net(cin, h, w, algo)
     t1 = net.conv_f32(0, wt.to(dev), kk.to(dev), bb.to(dev), stride=s, pad=p, relu=True)
     t2 = net.maxpool_f32(t1, 3, 2, 1)
     t3 = net.quantize(t2, bits)
@@ -112,13 +130,14 @@ def test_stem_conv_pool_quantize(dev, case, bits):
     fw = synth.normal(synth.generator(71), (5, cout), 1.0 / cout)
     net.fc_f32(t4, fw.to(dev))
     assert net.layers[1]["fused_into"] == 0 and net.layers[2]["fused_into"] == 0
-    assert net.layer_kernel(0, n) == f"conv_f32_mfma_kernel<{k}, {s}, 1, {bits}>", net.layer_kernel(0, n)
+    assert net.layer_kernel(0, n) == _kernel_name(algo, cin, k, s, 1, bits), net.layer_kernel(0, n)
     assert net.layer_kernel(1, n) == "" and net.layer_kernel(2, n) == ""
     ws = torch.empty(net.workspace_bytes(n), dtype=torch.uint8, device=dev)
     logits = torch.empty((n, 5), dtype=torch.float32, device=dev)
     net.forward(x.to(dev), logits, ws)
     torch.cuda.synchronize()
-    z, bound = _ref(x.numpy(), wt.numpy(), kk.numpy(), bb.numpy(), s, p, True)
+    x6 = "bf16x6" in net.layer_kernel(0, n)
+    z, bound = _ref(x.numpy(), wt.numpy(), kk.numpy(), bb.numpy(), s, p, True, x6)
     zp, bp = _pool(z), _pool(bound)
     got = _view(ws, net, t2, n)
     assert np.all(np.abs(got.astype(np.float64) - zp) <= bp), float(np.max(np.abs(got - zp) - bp))
@@ -181,18 +200,20 @@ def test_wide_window_falls_back_to_the_chain(dev):
     np.testing.assert_array_equal(_view(ws, net, t1, n), want)
 
 
-def test_resnet18_matrix_core_stem(dev):
-    """ResNet-18 2W2A (batch 2) with the fused matrix-core stem: the stem's
-    pooled output within its bound and the logits within 1e-3 relative."""
+@pytest.mark.parametrize("algo", [q.F32_MFMA, q.F32_BF16X6])
+def test_resnet18_matrix_core_stem(dev, algo):
+    """ResNet-18 2W2A (batch 2) with the fused matrix-core stem (fp32 or
+    bf16x6 matrix cores): the stem's pooled output within its bound and the
+    logits within 1e-3 relative."""
     from paper_2003_04296_amd.nets import build_resnet18
 
     p = synth.resnet18_params(seed=1004, batch=2)
-    qn = build_resnet18(p, dev)
-    assert qn.net.layer_kernel(0, 2) == "conv_f32_mfma_kernel<7, 2, 1, 2>", qn.net.layer_kernel(0, 2)
+    qn = build_resnet18(p, dev, f32_algo=algo)
+    assert qn.net.layer_kernel(0, 2) == _kernel_name(algo, 3, 7, 2, 1, 2), qn.net.layer_kernel(0, 2)
     logits = qn.forward(p["x"].to(dev)).cpu().numpy()
     st = p["stem"]
     ko, bo = oracle.bn_fold({kk: (v.numpy() if hasattr(v, "numpy") else v) for kk, v in st["bn"].items()})
-    z, bound = _ref(p["x"].numpy(), st["w"].numpy(), ko, bo, 2, 3, True)
+    z, bound = _ref(p["x"].numpy(), st["w"].numpy(), ko, bo, 2, 3, True, algo == q.F32_BF16X6)
     zp, bp = _pool(z), _pool(bound)
     got, _ = qn.tensor(qn.ids["stem"], 2)
     got = got.cpu().numpy()
