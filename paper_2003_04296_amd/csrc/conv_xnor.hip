@@ -31,6 +31,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <type_traits>
+
 #include "qconv_internal.h"
 
 namespace qc {
@@ -90,6 +92,8 @@ __global__ __launch_bounds__(256) void conv_xnor_kernel(const XArgs x) {
 
   uint32_t* act_l = xlds;                   // [cwc][PA][hr][hcs]
   uint32_t* wt_l = xlds + x.act_words;      // [tap][cwc][CO_B][PW]
+  // the epilogue's per-channel parameters: [0, CO_B) k or s_c, [CO_B, 2 CO_B) b
+  float* ep_l = reinterpret_cast<float*>(xlds + x.act_words + a.kh * a.kw * x.cwc * CO_B * PW);
   const int taps = a.kh * a.kw;
   const int plane_words = x.hr * x.hcs;
 
@@ -116,47 +120,84 @@ __global__ __launch_bounds__(256) void conv_xnor_kernel(const XArgs x) {
   for (int chunk = 0; chunk < x.nchunks; ++chunk) {
     const int cw0 = chunk * x.cwc;
     const int ncw = min(x.cwc, a.cw - cw0);
-    // ---- stage the halo words of this chunk (0 outside the image = Q(0)) ----
     const int hpix = x.hr * x.hc;
-    for (int it = tid; it < hpix * ncw; it += 256) {
+    const int wrows = taps * ncw;
+    // halo word `it` of this chunk (0 outside the image = Q(0)): its LDS
+    // slot and, inside the image, its source
+    auto halo_item = [&](int it, const uint32_t** src) __attribute__((always_inline)) {
       const int c = it % ncw;  // consecutive threads: consecutive words of one pixel
       const int hp = it / ncw;
       const int hrow = hp / x.hc, hcol = hp - (hp / x.hc) * x.hc;
       const int step = x.k1 ? a.stride : 1;
       const int iy = iy0 + hrow * step, ix = ix0 + hcol * step;
-      uint32_t v[PA];
-#pragma unroll
-      for (int p = 0; p < PA; ++p) v[p] = 0u;
-      if (iy >= 0 && iy < a.h && ix >= 0 && ix < a.w) {
-        const uint32_t* src = actb + ((int64_t)iy * a.w + ix) * apix + (int64_t)(cw0 + c) * PA;
-        if constexpr (PA == 1) {
-          v[0] = src[0];
-        } else {
-          const uint2 u = *reinterpret_cast<const uint2*>(src);
-          v[0] = u.x;
-          v[1] = u.y;
-        }
-      }
+      *src = (iy >= 0 && iy < a.h && ix >= 0 && ix < a.w)
+                 ? actb + ((int64_t)iy * a.w + ix) * apix + (int64_t)(cw0 + c) * PA
+                 : nullptr;
       const int col = x.k1 ? hcol : halo_col(hcol, a.stride, x.half);
-#pragma unroll
-      for (int p = 0; p < PA; ++p) act_l[(c * PA + p) * plane_words + hrow * x.hcs + col] = v[p];
-    }
-    // ---- stage the weights of this chunk: [tap][word][channel][plane] ----
-    const int wrows = taps * ncw;
-    for (int it = tid; it < wrows * CO_B; it += 256) {
+      return c * PA * plane_words + hrow * x.hcs + col;
+    };
+    // weight word `it` of this chunk, [tap][word][channel][plane] (rows past
+    // cout are 0 in the packed layout: cop >= co_blk + CO_B)
+    auto wt_item = [&](int it, const uint32_t** src) __attribute__((always_inline)) {
       const int col = it % CO_B;
       const int r = it / CO_B;
       const int tap = r / ncw, c = r - (r / ncw) * ncw;
-      const int co = co_blk + col;  // rows past cout are 0 in the packed layout (cop >= co_blk + CO_B)
-      const uint32_t* src = a.wt + ((int64_t)(tap * a.cw + cw0 + c) * a.cop + co) * PW;
-      uint32_t* dst = wt_l + ((tap * x.cwc + c) * CO_B + col) * PW;
-      if constexpr (PW == 1) {
-        dst[0] = src[0];
+      *src = a.wt + ((int64_t)(tap * a.cw + cw0 + c) * a.cop + co_blk + col) * PW;
+      return ((tap * x.cwc + c) * CO_B + col) * PW;
+    };
+    auto ld = [](const uint32_t* src, uint32_t* v, auto np) __attribute__((always_inline)) {
+      constexpr int NP = decltype(np)::value;
+      if constexpr (NP == 1) {
+        v[0] = src ? src[0] : 0u;
       } else {
-        const uint2 u = *reinterpret_cast<const uint2*>(src);
-        dst[0] = u.x;
-        dst[1] = u.y;
+        const uint2 u = src ? *reinterpret_cast<const uint2*>(src) : make_uint2(0u, 0u);
+        v[0] = u.x;
+        v[1] = u.y;
       }
+    };
+    // ---- stage the chunk: the first halo word and weight word of every
+    // thread are both in flight before either is stored ----
+    {
+      uint32_t va[PA], vw[PW];
+      const uint32_t *sa = nullptr, *sw = nullptr;
+      int da = 0, dw = 0;
+      if (tid < hpix * ncw) da = halo_item(tid, &sa);
+      if (tid < wrows * CO_B) dw = wt_item(tid, &sw);
+      ld(sa, va, std::integral_constant<int, PA>());
+      if (tid < wrows * CO_B) ld(sw, vw, std::integral_constant<int, PW>());
+      // with the first chunk, the epilogue parameters of the block's channels
+      const bool pt = chunk == 0 && tid < 2 * CO_B && a.mode != QCONV_EPI_INT32;
+      float pv = 0.0f;
+      if (pt) {
+        const int col = tid % CO_B, co = co_blk + col;
+        const float* src = a.mode == QCONV_EPI_SCALE_F32 ? a.scale : (tid < CO_B ? a.bn_k : a.bn_b);
+        if (co < a.cout && (tid < CO_B || a.mode != QCONV_EPI_SCALE_F32)) pv = src[co];
+      }
+      if (pt) ep_l[tid] = pv;
+      if (tid < hpix * ncw) {
+#pragma unroll
+        for (int p = 0; p < PA; ++p) act_l[da + p * plane_words] = va[p];
+      }
+      if (tid < wrows * CO_B) {
+#pragma unroll
+        for (int p = 0; p < PW; ++p) wt_l[dw + p] = vw[p];
+      }
+    }
+    for (int it = tid + 256; it < hpix * ncw; it += 256) {
+      const uint32_t* sa;
+      const int da = halo_item(it, &sa);
+      uint32_t va[PA];
+      ld(sa, va, std::integral_constant<int, PA>());
+#pragma unroll
+      for (int p = 0; p < PA; ++p) act_l[da + p * plane_words] = va[p];
+    }
+    for (int it = tid + 256; it < wrows * CO_B; it += 256) {
+      const uint32_t* sw;
+      const int dw = wt_item(it, &sw);
+      uint32_t vw[PW];
+      ld(sw, vw, std::integral_constant<int, PW>());
+#pragma unroll
+      for (int p = 0; p < PW; ++p) wt_l[dw + p] = vw[p];
     }
     __syncthreads();
 
@@ -288,12 +329,13 @@ __global__ __launch_bounds__(256) void conv_xnor_kernel(const XArgs x) {
       continue;
     }
     float z[XMP];
+    const int cl = cg * XNC + n;
     if (a.mode == QCONV_EPI_SCALE_F32) {
-      const float sc = a.scale[co];
+      const float sc = ep_l[cl];
 #pragma unroll
       for (int i = 0; i < XMP; ++i) z[i] = sc * ((float)acc[i] * inv);
     } else {
-      const float kk = a.bn_k[co], bb = a.bn_b[co];
+      const float kk = ep_l[cl], bb = ep_l[CO_B + cl];
 #pragma unroll
       for (int i = 0; i < XMP; ++i) z[i] = fmaf(kk, (float)acc[i] * inv, bb);
       if (a.residual_on) {
@@ -380,7 +422,7 @@ bool xnor_plan(const ConvArgs& a, int ks, XArgs* x) {
 
 size_t xnor_lds(const XArgs& x, int ks) {
   const int co_b = 128 / ks;
-  return ((size_t)x.act_words + (size_t)x.c.kh * x.c.kw * x.cwc * co_b * planes_of(x.c.w_bits)) * 4;
+  return ((size_t)x.act_words + (size_t)x.c.kh * x.c.kw * x.cwc * co_b * planes_of(x.c.w_bits) + 2 * co_b) * 4;
 }
 
 int device_cus_x() {
