@@ -287,15 +287,22 @@ __device__ __forceinline__ void f32m_body(const F32M& m) {
         (void*)(m.x + (int64_t)img * img_elems), (short)0, (int)(img_elems * 4), 0x00020000);
     const int org = iy0 * m.w + ix0;  // may be negative: added only to in-image elements
     const bool inside = iy0 >= 0 && iy0 + G::IH <= m.h && ix0 >= 0 && ix0 + IW <= m.w;
+    // two straight runs of loads (a window inside the image needs no
+    // bounds test) rather than a branch around each element's test
+    if (inside) {
 #pragma unroll
-    for (int j = 0; j < F32M_NJ; ++j) {
-      bool ok = eyx[j] != 0xFFFFFFFFu;
-      if (!inside) {
-        const int gy = iy0 + (int)(eyx[j] >> 16), gx = ix0 + (int)(eyx[j] & 0xFFFFu);
-        ok = ok && gy >= 0 && gy < m.h && gx >= 0 && gx < m.w;
+      for (int j = 0; j < F32M_NJ; ++j) {
+        const int voff = eyx[j] != 0xFFFFFFFFu ? (org + eoff[j]) * 4 : 0x7FFFFFF0;
+        wval[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, voff, 0, 0));
       }
-      const int voff = ok ? (org + eoff[j]) * 4 : 0x7FFFFFF0;
-      wval[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, voff, 0, 0));
+    } else {
+#pragma unroll
+      for (int j = 0; j < F32M_NJ; ++j) {
+        const int gy = iy0 + (int)(eyx[j] >> 16), gx = ix0 + (int)(eyx[j] & 0xFFFFu);
+        const bool ok = eyx[j] != 0xFFFFFFFFu && (unsigned)gy < (unsigned)m.h && (unsigned)gx < (unsigned)m.w;
+        const int voff = ok ? (org + eoff[j]) * 4 : 0x7FFFFFF0;
+        wval[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, voff, 0, 0));
+      }
     }
   };
   const int first = blockIdx.x / m.co_groups, step_items = gridDim.x / m.co_groups;
