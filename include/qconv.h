@@ -318,8 +318,10 @@ void qnet_destroy(qnet* net);
  *     summed in fp32 (x0 w0 apart from the five smaller ones).  The three
  *     dropped products are below 2^-20 |x w|, so results stay within fp32
  *     rounding of the exact sum: |err| <= (gamma_K + 2^-19) sum |x w|.
- *     Inputs and weights must be finite (an inf or NaN makes the outputs
- *     whose windows hold it NaN). */
+ *     Inputs and weights must be finite: an inf or NaN makes NaN in the
+ *     outputs whose windows hold it (and, for an input, in the output one
+ *     column to its left, whose operand slot past its 7 taps reads it
+ *     against a zero weight). */
 enum { QNET_F32_FMAF_CHAIN = 0, QNET_F32_MFMA = 1, QNET_F32_BF16X6 = 2 };
 int qnet_set_f32_algo(qnet* net, int algo);
 

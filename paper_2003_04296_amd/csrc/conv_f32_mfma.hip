@@ -76,17 +76,16 @@ constexpr int X6_PLW = 3 * X6_CIPW + 1;  // words per plane: up to 3 input chann
 // remainder x - p0 is exact in fp32 (same sign and exponent range), and so
 // is the second cut; what is left has at most 8 significant bits, so it is
 // itself a bf16.  Cutting rather than rounding keeps every part no larger
-// than what it splits, and no part overflows.  A non-finite x keeps its
-// first part (a NaN made quiet) and zero for the others.
+// than what it splits, and no part overflows.  A non-finite x makes the
+// remainder NaN (inf - inf, or NaN), so its products spread NaN.
 __device__ __forceinline__ void split_bf16x3(float x, uint32_t& h0, uint32_t& h1, uint32_t& h2) {
   const uint32_t u = __float_as_uint(x);
   const float r1 = x - __uint_as_float(u & 0xFFFF0000u);
   const uint32_t v = __float_as_uint(r1);
   const float r2 = r1 - __uint_as_float(v & 0xFFFF0000u);
-  const bool fin = (u & 0x7F800000u) != 0x7F800000u;
-  h0 = (!fin && (u & 0x007FFFFFu)) ? 0x7FC0u : (u >> 16);
-  h1 = fin ? (v >> 16) : 0u;
-  h2 = fin ? (__float_as_uint(r2) >> 16) : 0u;
+  h0 = u >> 16;
+  h1 = v >> 16;
+  h2 = __float_as_uint(r2) >> 16;
 }
 
 template <int KSZ, int S, int POOL>
@@ -168,7 +167,10 @@ struct F32M {
 // rounding of the exact sum (the bound is derived with the tests).  A
 // k-step of 16 is two (ci, ky) tap rows: lanes 0-31 take row 2 j, lanes
 // 32-63 row 2 j + 1, each as 4 words of two bf16 (taps kx, kx + 1; the
-// eighth slot, past the row, is masked to zero).
+// eighth slot reads the next window column against a zero weight).
+// Inputs and weights must be finite: a non-finite value makes NaN in the
+// outputs it meets (including, through the eighth slot, the pixel to its
+// left's).
 template <int ALG, int KSZ, int S, int POOL, int OB>
 __device__ __forceinline__ void f32m_body(const F32M& m) {
   static_assert(ALG == 0 || (KSZ == 7 && S == 2 && POOL == 1), "bf16x6 geometry");
@@ -337,6 +339,15 @@ __device__ __forceinline__ void f32m_body(const F32M& m) {
     int img, ty, tx, cy0, cx0;
     origin(item, &img, &ty, &tx, &cy0, &cx0);
     lds_barrier();  // the previous item's LDS tiles are consumed
+    if constexpr (ALG == 1) {
+      // the column after the window's last one, which the eighth slot of the
+      // last pixel column reads, is 0 in every row and part (the pooled
+      // epilogue's conv tile overlays these rows)
+      for (int i = tid; i < 3 * m.cin * G::IH; i += 256) {
+        const int q = i / (m.cin * G::IH), r = i - q * (m.cin * G::IH), ci = r / G::IH, yy = r - ci * G::IH;
+        xh[2 * q * X6_PLW + (ci * X6_CIPW + yy * X6_RPW) * 2 + IW] = 0;
+      }
+    }
 #pragma unroll
     for (int j = 0; j < F32M_NJ; ++j) {  // elements past the window land on the spare slot
       if constexpr (ALG == 1) {
@@ -382,8 +393,10 @@ __device__ __forceinline__ void f32m_body(const F32M& m) {
 #pragma unroll
         for (int q = 0; q < 3; ++q) {
           const int o = q * X6_PLW;
-          a0[q] = make_uint4(r0[o], r0[o + 1], r0[o + 2], r0[o + 3] & 0xFFFFu);  // slot 7 (past the row) is 0
-          a1[q] = make_uint4(r1[o], r1[o + 1], r1[o + 2], r1[o + 3] & 0xFFFFu);
+          // slot 7 holds the window column after the row's taps, against a
+          // zero weight (finite inputs: a zero product)
+          a0[q] = make_uint4(r0[o], r0[o + 1], r0[o + 2], r0[o + 3]);
+          a1[q] = make_uint4(r1[o], r1[o + 1], r1[o + 2], r1[o + 3]);
           if (zero) {
             a0[q] = make_uint4(0u, 0u, 0u, 0u);
             a1[q] = make_uint4(0u, 0u, 0u, 0u);
