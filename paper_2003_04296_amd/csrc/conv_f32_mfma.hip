@@ -149,6 +149,7 @@ struct F32M {
   int relu;
   int oh, ow;  // layer output (pooled when pooling)
   int tiles_y, tiles_x, co_tiles, items;
+  FastDiv fd_tx, fd_ty;  // item -> (image, tile row, tile column) without a division
   int nct, co_groups;  // 32-channel tiles per block (plain tiles: up to 4 over one staged window), blocks per item
   float* out;
   uint32_t* out_packed;
@@ -270,10 +271,10 @@ __device__ __forceinline__ void f32m_body(const F32M& m) {
   }
   float wval[F32M_NJ];
   auto origin = [&](int item, int* img, int* ty, int* tx, int* cy0, int* cx0) __attribute__((always_inline)) {
-    *tx = item % m.tiles_x;
-    const int r0 = item / m.tiles_x;
-    *ty = r0 % m.tiles_y;
-    *img = r0 / m.tiles_y;
+    const int r0 = (int)fdiv((uint32_t)item, m.fd_tx);
+    *tx = item - r0 * m.tiles_x;
+    *img = (int)fdiv((uint32_t)r0, m.fd_ty);
+    *ty = r0 - *img * m.tiles_y;
     *cy0 = POOL ? 2 * *ty * PT_H - 1 : *ty * PT_H0;
     *cx0 = POOL ? 2 * *tx * PT_W - 1 : *tx * PT_W0;
   };
@@ -343,9 +344,10 @@ __device__ __forceinline__ void f32m_body(const F32M& m) {
       // the column after the window's last one, which the eighth slot of the
       // last pixel column reads, is 0 in every row and part (the pooled
       // epilogue's conv tile overlays these rows)
-      for (int i = tid; i < 3 * m.cin * G::IH; i += 256) {
-        const int q = i / (m.cin * G::IH), r = i - q * (m.cin * G::IH), ci = r / G::IH, yy = r - ci * G::IH;
-        xh[2 * q * X6_PLW + (ci * X6_CIPW + yy * X6_RPW) * 2 + IW] = 0;
+      if (tid < m.cin * G::IH) {  // at most 3 x 35 rows
+        const int ci = tid / G::IH, yy = tid - ci * G::IH;
+#pragma unroll
+        for (int q = 0; q < 3; ++q) xh[2 * q * X6_PLW + (ci * X6_CIPW + yy * X6_RPW) * 2 + IW] = 0;
       }
     }
 #pragma unroll
@@ -689,7 +691,12 @@ bool f32m_plan(int n, int cin, int h, int w, int cout, int k, int stride, int pa
   m->co_tiles = ceil_div(cout, 32);
   const int64_t items = (int64_t)n * m->tiles_y * m->tiles_x;
   if (items * m->co_tiles >= ((int64_t)1 << 31)) return false;
+  // the multiply-high divisions of an item index are exact
+  if (items * m->tiles_x >= ((int64_t)1 << 32) || (items / m->tiles_x + 1) * m->tiles_y >= ((int64_t)1 << 32))
+    return false;
   m->items = (int)items;
+  m->fd_tx = make_fastdiv((uint32_t)m->tiles_x);
+  m->fd_ty = make_fastdiv((uint32_t)m->tiles_y);
   // LDS: the staged window (with pooling also the conv tile and the staged
   // pooled tile over it), the weights, then (plain tiles) the packed
   // staging; plain tiles take as many channel tiles per block (up to 4) as

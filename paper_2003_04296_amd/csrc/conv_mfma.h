@@ -86,18 +86,6 @@ __host__ __device__ constexpr int halo_items_per_thread(int words, int cfg) {
 // and fp16 shapes spill within 168).
 __host__ __device__ constexpr int blocks_per_cu(int opk, int cfg) { return opk == OP_FP4 && cfg != 0 ? 3 : 2; }
 
-// n / d by a multiply-high, exact whenever n * d < 2^32 (checked on the host
-// against the largest dividend of each use).
-struct FastDiv {
-  uint32_t d, m;
-};
-inline FastDiv make_fastdiv(uint32_t d) {
-  FastDiv f;
-  f.d = d;
-  f.m = d <= 1 ? 0u : (uint32_t)(0xFFFFFFFFu / d + 1u);
-  return f;
-}
-__device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv f) { return f.m ? __umulhi(n, f.m) : n; }
 
 // Operand formats (MfmaOp): what one 32-channel word of a pixel becomes in
 // LDS and how many channels one k-step of the MFMA consumes.

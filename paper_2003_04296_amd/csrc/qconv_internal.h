@@ -70,6 +70,19 @@ inline bool hardtanh_needed(int bits, Thr t) {
   return (bits == 2 && t.t0 >= 1.0f) || (bits == 3 && t.t2 >= 1.0f);
 }
 
+// n / d by a multiply-high, exact whenever n * d < 2^32 (checked on the host
+// against the largest dividend of each use).
+struct FastDiv {
+  uint32_t d, m;
+};
+inline FastDiv make_fastdiv(uint32_t d) {
+  FastDiv f;
+  f.d = d;
+  f.m = d <= 1 ? 0u : (uint32_t)(0xFFFFFFFFu / d + 1u);
+  return f;
+}
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv f) { return f.m ? __umulhi(n, f.m) : n; }
+
 // Thresholds that give the compares on |z| the results of those on
 // |HardTanh(z)| = min(|z|, 1) for every z, NaN included: one below 1 is
 // kept, one at or above 1 (which |HardTanh(z)| never exceeds) becomes +inf.
