@@ -245,3 +245,29 @@ def test_convnet_matrix_core_first_layer(dev):
     assert same.sum() >= 8, int(same.sum())
     np.testing.assert_array_equal(logits[same], want[same])
     print(f"first-layer sign flips: {int((lv != levels[0]).sum())} in {16 - int(same.sum())} of 16 images")
+
+
+@pytest.mark.parametrize("algo", [q.F32_MFMA, q.F32_BF16X6])
+def test_stem_wide_exponent_range(dev, algo):
+    """Inputs and weights spread over 2^-40 .. 2^40 (every element a full
+    24-bit significand at its own scale): the three-way splits stay exact
+    at any exponent, so the pooled output still lies within its bound."""
+    n, cin, h, w, cout, k, s, p = 2, 3, 45, 47, 40, 7, 2, 3
+    x, wt, kk, bb = _inputs(96, n, cin, h, w, cout, k)
+    ex = torch.from_numpy(np.random.default_rng(98).integers(-40, 41, x.shape).astype(np.float32))
+    ew = torch.from_numpy(np.random.default_rng(99).integers(-20, 21, wt.shape).astype(np.float32))
+    x = (x * torch.pow(2.0, ex)).contiguous()
+    wt = (wt * torch.pow(2.0, ew)).contiguous()
+    net = q.Net(cin, h, w, algo)
+    t1 = net.conv_f32(0, wt.to(dev), kk.to(dev), bb.to(dev), stride=s, pad=p, relu=True)
+    t2 = net.maxpool_f32(t1, 3, 2, 1)
+    net.fc_f32(net.avgpool(t2), torch.ones((2, cout)).to(dev))
+    assert net.layer_kernel(0, n) == _kernel_name(algo, cin, k, s, 1, 0), net.layer_kernel(0, n)
+    ws = torch.empty(net.workspace_bytes(n), dtype=torch.uint8, device=dev)
+    net.forward(x.to(dev), torch.empty((n, 2), dtype=torch.float32, device=dev), ws)
+    torch.cuda.synchronize()
+    z, bound = _ref(x.numpy(), wt.numpy(), kk.numpy(), bb.numpy(), s, p, True, algo == q.F32_BF16X6)
+    zp, bp = _pool(z), _pool(bound)
+    got = _view(ws, net, t2, n).astype(np.float64)
+    assert np.all(np.isfinite(got))
+    assert np.all(np.abs(got - zp) <= bp), float(np.max(np.abs(got - zp) - bp))
