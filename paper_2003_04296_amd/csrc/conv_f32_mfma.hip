@@ -1,7 +1,9 @@
 // conv_f32_mfma.hip -- the full-precision first convolution on the fp32
-// matrix cores (v_mfma_f32_32x32x2_f32), with its batch norm, ReLU, an
-// optional 3x3 / 2 max pooling (pad 1) and the packed Q(HardTanh(.)) of the
-// next layer's input fused into the epilogue.  The first layer's input is
+// matrix cores (v_mfma_f32_32x32x2_f32) or, for the pooled 7 x 7 / 2
+// geometry, on the bf16 matrix cores through exact three-way splits (the
+// bf16x6 kernel below), with its batch norm, ReLU, an optional 3x3 / 2 max
+// pooling (pad 1) and the packed Q(HardTanh(.)) of the next layer's input
+// fused into the epilogue.  The first layer's input is
 // the image, which stays unquantized (Sec. III-E; the workloads fix fp32
 // first layers); its sums are taken in the matrix cores' order, so results
 // match the fixed fmaf-chain kernels (fp32_layers.hip) within fp32 rounding,
@@ -164,14 +166,15 @@ struct F32M {
 // partial products with i + j <= 2 are summed on the bf16 matrix cores
 // (v_mfma_f32_32x32x16_bf16), x0 w0 in one accumulator and the five
 // smaller ones in a second, added at the end.  The three dropped products
-// are below 2^-20 |x w| together, so each output stays within fp32
-// rounding of the exact sum (the bound is derived with the tests).  A
+// are below 2^-20 |x w| together, and the small products' own sum rounds
+// below 2^-20.4 sum |x w| for K <= 147, so each output is within
+// (gamma_K + 2^-19 + 2^-24) sum |x w| of the exact sum.  A
 // k-step of 16 is two (ci, ky) tap rows: lanes 0-31 take row 2 j, lanes
 // 32-63 row 2 j + 1, each as 4 words of two bf16 (taps kx, kx + 1; the
 // eighth slot reads the next window column against a zero weight).
 // Inputs and weights must be finite: a non-finite value makes NaN in the
-// outputs it meets (including, through the eighth slot, the pixel to its
-// left's).
+// outputs it meets (including, through the eighth slot, the output one
+// column to its left).
 template <int ALG, int KSZ, int S, int POOL, int OB>
 __device__ __forceinline__ void f32m_body(const F32M& m) {
   static_assert(ALG == 0 || (KSZ == 7 && S == 2 && POOL == 1), "bf16x6 geometry");
